@@ -1,0 +1,211 @@
+"""Benchmark: dense window outputs per second of the exact dense evaluation on one MI355X.
+
+One step = one full dss_eval_dense of a frame that is already resident in HBM:
+Stuff, every convolution (MFMA implicit GEMM or direct), every sliding
+max-pool + Frag, and the final Defrag + Trim -- the same inclusive accounting
+as the paper's runtime experiment (Sect. 6.3).  The default workload is the HD
+frame (3x1080x1920 binary32, conv widths 64/128/256/512), the configuration the
+MFMA-utilisation target is stated for.
+
+Prints ONE JSON line with the throughput, a roofline object for the dominant
+kernel (per-launch HIP-event durations measured inside the timed region), a
+per-kernel breakdown, and the oracle's throughput on a bounded window sample of
+the same frame (CPU baseline, also used as a parity spot check).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_TFLOPS = {"f32": 157.3, "bf16": 2500.0}   # MI355X dense MFMA
+PEAK_HBM_GBS = 8000.0
+
+WORKLOAD_TEXT = {
+    "c1_64x64": "2-D 1x64x64 fp32, conv5x5 1-4 tanh, pool2, conv5x5 4-8 tanh, pool2, conv4x4 8-1 (B=28)",
+    "c2_1d_1m": "1-D 1x1048576 fp32, conv9 1-16-32-64 relu + pool2 x3, conv8 64-2 (B=120)",
+    "c3_512": "2-D 3x512x512 fp32, conv5x5 3-32, pool2, conv5x5 32-64, pool2, conv3x3 64-128, pool2, conv6x6 128-256, conv1x1 256-2 (B=68)",
+    "c4_hd": "2-D 3x1080x1920 fp32 HD frame, conv5x5 3-64, pool2, conv5x5 64-128, pool2, conv3x3 128-256, pool2, conv6x6 256-512, conv1x1 512-2 (B=68)",
+    "c5_4k": "2-D 3x2160x3840 bf16 4K frame, 4x(conv3x3, conv3x3, pool2) 32/64/128/256, conv6x6 256-512, conv1x1 512-4 (B=156)",
+}
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def summarize(recs, steps):
+    by = {}
+    for r in recs:
+        d = by.setdefault(r["kernel"], {"ms": 0.0, "flops": 0.0, "bytes": 0.0, "n": 0})
+        d["ms"] += r["ms"]
+        d["flops"] += r["flops"]
+        d["bytes"] += r["bytes"]
+        d["n"] += 1
+    out = []
+    for k, d in sorted(by.items(), key=lambda kv: -kv[1]["ms"]):
+        e = {"kernel": k, "launches_per_step": d["n"] / steps, "ms_per_step": d["ms"] / steps,
+             "avg_launch_ms": d["ms"] / d["n"]}
+        if d["flops"] > 0:
+            e["tflops"] = d["flops"] / d["ms"] / 1e9
+        if d["bytes"] > 0:
+            e["gbs"] = d["bytes"] / d["ms"] / 1e6
+        out.append((e, d))
+    return out
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", default="c4_hd", choices=sorted(WORKLOAD_TEXT))
+    ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target length of the oracle sample")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one MI355X: the dense evaluation of one frame runs on a single GPU in this "
+              "build (multi-GPU sharding is a design note only); run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_1508_06904_amd import dss, workloads as wl
+
+    torch.cuda.set_device(0)
+    t0 = time.time()
+    w = wl.make(args.config)
+    log("workload %s %s generated in %.1fs" % (args.config, w.x.shape, time.time() - t0))
+    plan = dss.Plan.from_workload(w)
+    C, H, W = w.x.shape
+    g = plan.geometry(H, W)
+    x = torch.from_numpy(w.x).to("cuda")
+    if w.dtype == "bf16":
+        x = x.to(torch.bfloat16)
+    x = x.contiguous()
+    out = torch.empty((g["out_c"], g["out_h"], g["out_w"]), dtype=torch.float32, device="cuda")
+    ws = plan.workspace(H, W)
+    windows = g["out_h"] * g["out_w"]
+
+    for i in range(args.warmup):
+        plan.eval_dense(x, out=out, workspace=ws)
+        torch.cuda.synchronize()
+        log("warmup %d done" % i)
+
+    plan.set_timing(True)
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter()
+    start.record()
+    for _ in range(args.steps):
+        plan.eval_dense(x, out=out, workspace=ws)
+    end.record()
+    torch.cuda.synchronize()
+    wall_s = time.perf_counter() - t_wall
+    ms_total = start.elapsed_time(end)
+    recs = plan.timings()
+    plan.set_timing(False)
+    ms_per_step = ms_total / args.steps
+    log("timed %d steps: %.3f ms/step (host wall %.3f ms/step)" % (args.steps, ms_per_step, 1e3 * wall_s / args.steps))
+
+    kernels = summarize(recs, args.steps)
+    breakdown = [e for e, _ in kernels]
+    dom, domd = kernels[0]
+    if domd["flops"] > 0:
+        ach = (domd["flops"] / domd["n"]) / (domd["ms"] / domd["n"]) / 1e9
+        peak = PEAK_TFLOPS[w.dtype]
+        roof = {"bound": "mfma", "kernel": dom["kernel"], "achieved": ach, "peak": peak, "unit": "TFLOP/s",
+                "frac": ach / peak, "traffic": None,
+                "per_launch": {"flops": domd["flops"] / domd["n"], "avg_ms": domd["ms"] / domd["n"],
+                               "launches_per_step": domd["n"] / args.steps}}
+    else:
+        ach = (domd["bytes"] / domd["n"]) / (domd["ms"] / domd["n"]) / 1e6
+        roof = {"bound": "hbm", "kernel": dom["kernel"], "achieved": ach, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": ach / PEAK_HBM_GBS, "traffic": None,
+                "per_launch": {"bytes": domd["bytes"] / domd["n"], "avg_ms": domd["ms"] / domd["n"]}}
+    conv_ms = sum(d["ms"] for e, d in kernels if d["flops"] > 0) / args.steps
+    conv_tflops = g["conv_flops"] / (conv_ms * 1e9) if conv_ms > 0 else None
+
+    record = {
+        "metric": "dense window outputs/sec at 1 MI355X",
+        "value": windows / (ms_per_step / 1e3),
+        "unit": "windows/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic (seeded), random He-init weights",
+        "config": {"workload": args.config + ": " + WORKLOAD_TEXT[args.config], "input": [C, H, W],
+                   "windows_per_step": windows, "receptive_field": [g["B_h"], g["B_w"]],
+                   "k_star": [g["K_h"], g["K_w"]], "conv_gflop_per_step": g["conv_flops"] / 1e9},
+        "roofline": roof,
+        "conv_aggregate": {"tflops": conv_tflops, "frac_of_peak": (conv_tflops / PEAK_TFLOPS[w.dtype]) if conv_tflops else None,
+                           "ms_per_step": conv_ms},
+        "breakdown": breakdown,
+        "cpu_baseline": None,
+    }
+
+    if not args.no_cpu_baseline:
+        record["cpu_baseline"], record["parity_spot_check"] = cpu_baseline(w, g, out, args.cpu_seconds)
+    print(json.dumps(record), flush=True)
+
+
+def cpu_baseline(w, g, out, target_s):
+    """Times the oracle (plain fp64 EvalStride, OpenMP over windows) on a bounded,
+    seeded sample of this frame's windows that covers every fragment phase, and
+    compares the GPU output at those windows."""
+    import numpy as np
+
+    import oracle
+    from paper_1508_06904_amd import workloads as wl
+
+    layers = w.layers
+    if w.dtype == "bf16":
+        layers = [dict(l, weight=wl.to_bf16_representable(l["weight"])) if l["kind"] == "conv" else l
+                  for l in w.layers]
+    threads = oracle.threads()
+    si, sj = wl.sample_windows(g["out_h"], g["out_w"], g["K_h"], g["K_w"], per_phase=1, seed=1)
+    nprobe = min(len(si), threads)
+    t = time.perf_counter()
+    oracle.eval_stride(layers, w.x, windows=(si[:nprobe], sj[:nprobe]))
+    probe_s = time.perf_counter() - t
+    n = int(max(nprobe, min(4096, target_s / max(probe_s, 1e-6) * nprobe)))
+    if n > len(si):
+        reps = -(-n // max(1, len(si))) + 1
+        si, sj = wl.sample_windows(g["out_h"], g["out_w"], g["K_h"], g["K_w"], per_phase=reps, seed=1)
+    n = min(n, len(si))
+    si, sj = si[:n], sj[:n]
+    log("cpu baseline: %d windows on %d threads (probe %.2fs for %d)" % (n, threads, probe_s, nprobe))
+    t = time.perf_counter()
+    ref = oracle.eval_stride(layers, w.x, windows=(si, sj))
+    cpu_s = time.perf_counter() - t
+    got = out[:, si, sj].T.cpu().numpy().astype(np.float64) if hasattr(out, "cpu") else out
+    err = float(np.abs(got - ref).max() / max(np.abs(ref).max(), 1e-300))
+    H, W = w.x.shape[1:]
+    windows = g["out_h"] * g["out_w"]
+    base = {"value": n / cpu_s, "unit": "windows/s", "cores": threads, "kind": "oracle",
+            "sample": "%d seeded windows of the %dx%d frame covering every fragment phase (i mod %d, j mod %d) "
+                      "plus corners and edge midpoints; fp64 EvalStride per window" % (n, H, W, g["K_h"], g["K_w"]),
+            "seconds": cpu_s, "extrapolated_full_frame_s": windows * cpu_s / n}
+    tol = 2e-2 if w.dtype == "bf16" else 1e-4
+    spot = {"windows": n, "max_abs_err_over_max_abs_oracle": err, "tolerance": tol, "pass": err <= tol}
+    log("cpu baseline %.2f windows/s; parity spot check %.3e (tol %.0e)" % (base["value"], err, tol))
+    return base, spot
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,246 @@
+/*
+ * dss.h -- exact dense signal scanning on AMD MI355X (gfx950).
+ *
+ * Evaluates a pooling CNN on every receptive-field-sized window of a 1-D signal
+ * or 2-D image at once, with results identical to running the ordinary strided
+ * network on each window separately.  The method and its correctness proof are
+ * Thom & Gritschneder, "Rapid Exact Signal Scanning with Deep Convolutional
+ * Neural Networks": the network is applied in a sliding fashion, every pooling
+ * layer is followed by a fragmentation (polyphase reshuffle) of the feature maps,
+ * the input is stuffed with dummy samples so that every fragmentation comes out
+ * even, and a final defragmentation plus trimming restores the dense output
+ * grid (Definition "processing chain", Sect. 4.2; Theorem "processing chain",
+ * Sect. 4.3).
+ *
+ * General conventions
+ *  - All functions are C ABI, no C++ exceptions cross it.  Every function that
+ *    can fail returns a dss_status; on failure dss_last_error() gives a
+ *    human-readable reason for the calling thread.
+ *  - Tensors are dense row-major arrays.  Pointers documented as "device" must
+ *    be HIP device memory of the current device; "host" pointers are ordinary
+ *    memory.  The library never frees caller memory.
+ *  - Work on device memory is enqueued asynchronously on the given HIP stream
+ *    (0 = the null stream); the caller synchronises.  Argument validation
+ *    happens before anything is enqueued: a call that returns an error leaves
+ *    every output buffer untouched.
+ *  - A 1-D signal is a 2-D one with height 1 (ndim = 1 requires H = 1, filter
+ *    heights fh = 1 and pool heights kh = 1).
+ *  - Filters use cross-correlation order, as deep-learning frameworks do:
+ *    weight[o][i][t_h][t_w] multiplies input sample (y + t_h, x + t_w).  The
+ *    paper writes the same operation with a flipped filter (Sect. 3.3); the two
+ *    differ only in how the taps are numbered.
+ */
+#ifndef DSS_H
+#define DSS_H
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum dss_status {
+    DSS_OK = 0,
+    DSS_E_INVALID = 1,      /* bad argument: NULL pointer, bad descriptor, channel mismatch */
+    DSS_E_SHAPE = 2,        /* extents do not fit: signal smaller than the receptive field,
+                               fragment extents not divisible by the pool size, too small workspace */
+    DSS_E_UNSUPPORTED = 3,  /* valid request outside what this build implements */
+    DSS_E_NOMEM = 4,        /* device allocation failed */
+    DSS_E_HIP = 5           /* a HIP runtime call or kernel launch failed */
+} dss_status;
+
+typedef enum dss_dtype {
+    DSS_F32 = 0,            /* IEEE binary32 */
+    DSS_BF16 = 1            /* bfloat16: storage type; arithmetic accumulates in binary32 */
+} dss_dtype;
+
+typedef enum dss_act {
+    DSS_ACT_NONE = 0,
+    DSS_ACT_RELU = 1,
+    DSS_ACT_TANH = 2
+} dss_act;
+
+typedef enum dss_kind {
+    DSS_LAYER_CONV = 0,
+    DSS_LAYER_MAXPOOL = 1
+} dss_kind;
+
+/* One layer of the network as the ordinary (strided, patch-based) CNN sees it.
+ *  conv:    multi-channel valid convolution with a filter of fh x fw samples
+ *           (Sect. 3.3), then + bias, then the activation.  Fully-connected layers
+ *           are convolutions whose filter covers the whole remaining extent.
+ *  maxpool: channel-wise maximum over non-overlapping kh x kw blocks starting at
+ *           the first sample (Definition "strided function", Sect. 4).
+ * A conv directly followed by a maxpool forms one layer of the processing chain;
+ * a conv without a pool has k = 1, a pool without a conv before it has the
+ * identity transformation (bypass layers, end of Sect. 4.2). */
+typedef struct dss_layer {
+    int32_t kind;           /* dss_kind */
+    int32_t cin, cout;      /* conv: input / output channels */
+    int32_t fh, fw;         /* conv: filter extent per axis, >= 1 */
+    int32_t act;            /* conv: dss_act */
+    int32_t kh, kw;         /* maxpool: block extent per axis, >= 1 */
+    const float* weight;    /* conv, host: [cout][cin][fh][fw] binary32 */
+    const float* bias;      /* conv, host: [cout] binary32, or NULL for zero bias */
+} dss_layer;
+
+/* Geometry of a network applied to an H x W signal (Lemma "processing chain"
+ * (a)-(c), Sect. 4.2; stuffing count of Theorem "processing chain", Sect. 4.3). */
+typedef struct dss_geometry {
+    int32_t ndim;           /* 1 or 2 */
+    int32_t in_c, out_c;    /* input channels, output channels of the last layer */
+    int32_t n_chain;        /* L: number of processing-chain layers */
+    int32_t B_h, B_w;       /* receptive field per axis */
+    int32_t K_h, K_w;       /* final stride product k*_L per axis */
+    int32_t r_h, r_w;       /* dummy samples stuffed at the end of each axis */
+    int32_t D_h, D_w;       /* stuffed extents H + r_h, W + r_w */
+    int32_t out_h, out_w;   /* dense output extents H - B_h + 1, W - B_w + 1 */
+    int32_t dtype;          /* dss_dtype of the plan (geometry queries: the dtype passed) */
+    int32_t reserved;
+    int64_t workspace_bytes;/* device scratch that dss_eval_dense / dss_eval_slide need */
+    double conv_flops;      /* algorithmic convolution flops of one dense evaluation
+                               (2 per multiply-add, only the samples the method needs) */
+    double pool_bytes;      /* algorithmic bytes of the sliding max-pool + Frag steps
+                               (each tensor read once, written once, at its stored width) */
+    double total_bytes;     /* algorithmic bytes of every step (stuff, convs, pools, defrag) */
+} dss_geometry;
+
+/* Per-layer geometry for chain layer j (1-based, 1..L), or j = 0 for the stuffed input. */
+typedef struct dss_layer_geometry {
+    int32_t c_h, c_w;       /* dimensionality reduction constant of T_j per axis (1 for identity) */
+    int32_t k_h, k_w;       /* pool size k_j per axis (1 when the layer has no pool) */
+    int32_t kstar_h, kstar_w;/* stride products k*_j */
+    int32_t u_h, u_w;       /* strided extent u_j (Lemma (a)) */
+    int32_t U_h, U_w;       /* fragment extent U_j^row per axis (Lemma (b)) */
+    int32_t F;              /* number of fragments k*_j,h * k*_j,w (U_j^col for both axes) */
+    int32_t channels;       /* feature maps after layer j */
+    int32_t has_conv, has_pool;
+} dss_layer_geometry;
+
+typedef struct dss_plan* dss_plan_t;
+
+/* ---------------------------------------------------------------- geometry (host only) */
+
+/* Geometry of `layers` on an H x W signal with `in_channels` channels, without a
+ * plan and without touching the GPU.  `dtype` only affects workspace_bytes and
+ * the byte counts.  DSS_E_SHAPE if H < B_h or W < B_w (the transformation is
+ * defined only for signals at least as large as the receptive field). */
+dss_status dss_chain_geometry(const dss_layer* layers, int32_t n_layers, int32_t ndim,
+                              int32_t in_channels, dss_dtype dtype, int32_t H, int32_t W,
+                              dss_geometry* out);
+
+/* Same for chain layer j (0..L). */
+dss_status dss_chain_layer_geometry(const dss_layer* layers, int32_t n_layers, int32_t ndim,
+                                    int32_t in_channels, int32_t H, int32_t W, int32_t j,
+                                    dss_layer_geometry* out);
+
+/* ---------------------------------------------------------------- plans */
+
+/* Validates the layer list, derives the processing chain (receptive field B and
+ * stride products, Lemma (a)), and copies the weights to the current device in
+ * the layouts the kernels read (binary32, or bfloat16 rounded to nearest-even for
+ * DSS_BF16 plans; biases stay binary32).  The caller may free `layers` and its
+ * weight arrays right after the call.  The plan belongs to the device that was
+ * current at creation.  Errors: DSS_E_INVALID (descriptor), DSS_E_UNSUPPORTED
+ * (ndim, dtype), DSS_E_NOMEM, DSS_E_HIP. */
+dss_status dss_plan_create(const dss_layer* layers, int32_t n_layers, int32_t ndim,
+                           int32_t in_channels, dss_dtype dtype, dss_plan_t* out_plan);
+
+/* Releases the plan's device memory.  NULL is ignored.  Must not race with an
+ * evaluation that is still running on the plan. */
+void dss_plan_destroy(dss_plan_t plan);
+
+dss_status dss_plan_geometry(dss_plan_t plan, int32_t H, int32_t W, dss_geometry* out);
+dss_status dss_plan_layer_geometry(dss_plan_t plan, int32_t H, int32_t W, int32_t j,
+                                   dss_layer_geometry* out);
+
+/* ---------------------------------------------------------------- evaluation */
+
+/* Dense evaluation T(signal) = Trim(Defrag_{k*_L}(EvalSlide_L(Stuff(signal))))
+ * (Theorem "processing chain", Sect. 4.3), which equals the strided network
+ * applied to every window (Slide_{EvalStride_L}).
+ *   signal     device, [in_c][H][W] in the plan's dtype (binary32 or bfloat16)
+ *   out        device, binary32 [out_c][H - B_h + 1][W - B_w + 1];
+ *              out[c][i][j] is channel c of the network's output on the window
+ *              whose top-left sample is (i, j)
+ *   workspace  device scratch of at least dss_geometry.workspace_bytes bytes
+ *              (256-byte aligned), owned by the caller and not read afterwards
+ *   stream     HIP stream for every launch
+ * Concurrent evaluations of one plan are allowed if each uses its own workspace.
+ * Errors: DSS_E_INVALID (NULL pointers), DSS_E_SHAPE (signal smaller than the
+ * receptive field, workspace too small), DSS_E_HIP (launch failure). */
+dss_status dss_eval_dense(dss_plan_t plan, const void* signal, int32_t H, int32_t W, float* out,
+                          void* workspace, int64_t workspace_bytes, hipStream_t stream);
+
+/* The intermediate representation EvalSlide_j(Stuff(signal)) after chain layer j
+ * (0 <= j <= L; j = 0 gives the stuffed signal), as binary32 in the fragment
+ * layout [F_j][C_j][U_j,h][U_j,w] (fragment index linearised as for dss_frag).
+ * By Lemma "processing chain" (d), sample (y, x) of fragment
+ * (i mod k*_j,h) * k*_j,w + (w mod k*_j,w) holds, for y = i div k*_j,h + mu_h and
+ * x = w div k*_j,w + mu_w, sample (mu_h, mu_w) of the strided network's
+ * layer-j output on the window at (i, w).  Same arguments and errors as
+ * dss_eval_dense; `out` must hold F_j * C_j * U_h * U_w floats. */
+dss_status dss_eval_slide(dss_plan_t plan, const void* signal, int32_t H, int32_t W, int32_t j,
+                          float* out, void* workspace, int64_t workspace_bytes, hipStream_t stream);
+
+/* ---------------------------------------------------------------- Frag / Defrag */
+
+/* Fragmentation Frag_k per axis (Definition "fragmentation" and Lemma
+ * "frag-ops", Sect. 4.1) on a planar fragment tensor:
+ *   in   device, [S_h*S_w][C][H][W]       (S_h x S_w fragments, row-major)
+ *   out  device, [(k_h*S_h)*(k_w*S_w)][C][H/k_h][W/k_w]
+ *   out[(a_h*S_h + b_h)*(k_w*S_w) + a_w*S_w + b_w][c][m][n]
+ *        = in[b_h*S_w + b_w][c][m*k_h + a_h][n*k_w + a_w]
+ * i.e. per axis, sample m*k + a of input fragment b goes to sample m of output
+ * fragment a*S + b.  A pure permutation: bit-exact for either element width.
+ * DSS_E_SHAPE unless k_h divides H and k_w divides W.  in and out must not overlap. */
+dss_status dss_frag(int32_t k_h, int32_t k_w, int32_t S_h, int32_t S_w, int32_t C, int32_t H,
+                    int32_t W, dss_dtype dtype, const void* in, void* out, hipStream_t stream);
+
+/* Defragmentation Defrag_k per axis, the inverse of dss_frag (Lemma
+ * "defrag-ops", Sect. 4.1, and its simplified form in the appendix):
+ *   in   device, [(k_h*S_h)*(k_w*S_w)][C][H][W]
+ *   out  device, [S_h*S_w][C][H*k_h][W*k_w]
+ *   out[b_h*S_w + b_w][c][y][x]
+ *        = in[((y mod k_h)*S_h + b_h)*(k_w*S_w) + (x mod k_w)*S_w + b_w][c][y div k_h][x div k_w] */
+dss_status dss_defrag(int32_t k_h, int32_t k_w, int32_t S_h, int32_t S_w, int32_t C, int32_t H,
+                      int32_t W, dss_dtype dtype, const void* in, void* out, hipStream_t stream);
+
+/* ---------------------------------------------------------------- telemetry */
+
+/* Per-launch record of an evaluation on a plan with timing enabled. */
+typedef struct dss_launch_record {
+    const char* kernel;     /* static string: kernel family and variant */
+    int32_t chain_layer;    /* 1..L, 0 for stuffing, L+1 for defragmentation */
+    int32_t reserved;
+    double ms;              /* device time between HIP events around the launch */
+    double flops;           /* algorithmic flops of the launch (0 for data movement) */
+    double bytes;           /* algorithmic bytes of the launch (each tensor once) */
+} dss_launch_record;
+
+/* Enables (1) or disables (0) HIP-event timing of every launch of later
+ * evaluations of this plan, and discards the records collected so far (after
+ * waiting for their events).  Timing adds two event records per launch on the
+ * evaluation stream and is off by default.  Records accumulate over all timed
+ * evaluations until the next call of this function. */
+dss_status dss_plan_set_timing(dss_plan_t plan, int32_t enable);
+
+/* Waits for the events of the collected records and copies up to `cap` of
+ * them, oldest first; *count receives the number collected.  Not safe to call
+ * concurrently with an evaluation of the same plan. */
+dss_status dss_plan_timings(dss_plan_t plan, dss_launch_record* records, int32_t cap, int32_t* count);
+
+/* ---------------------------------------------------------------- misc */
+
+const char* dss_status_string(dss_status s);
+/* Reason for the calling thread's last failure ("" if none).  Valid until the
+ * thread's next failing call. */
+const char* dss_last_error(void);
+/* Library version as "major.minor.patch". */
+const char* dss_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* DSS_H */

@@ -1,0 +1,191 @@
+// Processing chain and per-signal geometry (host only, integer arithmetic).
+//
+//  * Grouping of the layer list into processing-chain layers: a convolution and
+//    the max-pool that directly follows it form one layer; a convolution without
+//    a pool gets k = 1 and a pool without a convolution gets the identity
+//    transformation c = 1 (bypass layers, end of Sect. 4.2).
+//  * Receptive field and stride products (Definition "processing chain" and
+//    Lemma "processing chain" (a), Sect. 4.2): starting from u_L = 1 the strided
+//    extents satisfy u_{j-1} - c_j + 1 = k_j u_j (Sect. 5.1), so
+//    B = u_0 and k*_j = k_1 ... k_j.
+//  * Stuffing count r = 0 if k*_L divides N - B + 1, else k*_L - rem(N - B + 1, k*_L)
+//    (Theorem "processing chain", Sect. 4.3), per axis.
+//  * Fragment extents of the sliding evaluation: U_0 = D = N + r, after T_j the
+//    extent is U_{j-1} - c_j + 1, after Slide_g it is one sample shorter per
+//    extra pooled sample, and Frag_k divides it by k (Lemma (b)); the fragment
+//    count per axis is k*_j.
+#include <cstring>
+
+#include "dss_internal.h"
+
+namespace dss {
+
+size_t dtype_size(dss_dtype dt) { return dt == DSS_BF16 ? 2 : 4; }
+
+dss_status build_chain(const dss_layer* layers, int n, int ndim, int in_c, Chain* out) {
+    if (!layers || n <= 0) return fail(DSS_E_INVALID, "empty layer list");
+    if (ndim != 1 && ndim != 2) return fail(DSS_E_UNSUPPORTED, "ndim must be 1 or 2 (got %d)", ndim);
+    if (in_c <= 0) return fail(DSS_E_INVALID, "in_channels must be positive (got %d)", in_c);
+    Chain ch;
+    ch.ndim = ndim;
+    ch.in_c = in_c;
+    int cur_c = in_c;
+    int t = 0;
+    while (t < n) {
+        const dss_layer& l = layers[t];
+        ChainLayer cl;
+        if (l.kind == DSS_LAYER_CONV) {
+            if (l.cin != cur_c)
+                return fail(DSS_E_INVALID, "layer %d: cin=%d but the previous layer gives %d channels", t, l.cin, cur_c);
+            if (l.cout <= 0 || l.fh <= 0 || l.fw <= 0)
+                return fail(DSS_E_INVALID, "layer %d: non-positive conv size", t);
+            if (ndim == 1 && l.fh != 1) return fail(DSS_E_INVALID, "layer %d: 1-D networks need fh = 1", t);
+            if (l.act < DSS_ACT_NONE || l.act > DSS_ACT_TANH)
+                return fail(DSS_E_INVALID, "layer %d: unknown activation %d", t, l.act);
+            if (!l.weight) return fail(DSS_E_INVALID, "layer %d: NULL weight", t);
+            cl.has_conv = true;
+            cl.c_h = l.fh;
+            cl.c_w = l.fw;
+            cl.cin = l.cin;
+            cl.cout = l.cout;
+            cl.act = l.act;
+            cl.desc = t;
+            cur_c = l.cout;
+            ++t;
+            if (t < n && layers[t].kind == DSS_LAYER_MAXPOOL) {
+                const dss_layer& p = layers[t];
+                if (p.kh <= 0 || p.kw <= 0) return fail(DSS_E_INVALID, "layer %d: non-positive pool size", t);
+                if (ndim == 1 && p.kh != 1) return fail(DSS_E_INVALID, "layer %d: 1-D networks need kh = 1", t);
+                cl.has_pool = true;
+                cl.k_h = p.kh;
+                cl.k_w = p.kw;
+                ++t;
+            }
+        } else if (l.kind == DSS_LAYER_MAXPOOL) {
+            if (l.kh <= 0 || l.kw <= 0) return fail(DSS_E_INVALID, "layer %d: non-positive pool size", t);
+            if (ndim == 1 && l.kh != 1) return fail(DSS_E_INVALID, "layer %d: 1-D networks need kh = 1", t);
+            cl.has_pool = true;
+            cl.k_h = l.kh;
+            cl.k_w = l.kw;
+            cl.cin = cl.cout = cur_c;
+            ++t;
+        } else {
+            return fail(DSS_E_INVALID, "layer %d: unknown kind %d", t, l.kind);
+        }
+        ch.layers.push_back(cl);
+    }
+    const int L = ch.L();
+    ch.kstar_h.assign(L + 1, 1);
+    ch.kstar_w.assign(L + 1, 1);
+    for (int j = 1; j <= L; ++j) {
+        const int64_t kh = (int64_t)ch.kstar_h[j - 1] * ch.layers[j - 1].k_h;
+        const int64_t kw = (int64_t)ch.kstar_w[j - 1] * ch.layers[j - 1].k_w;
+        if (kh > (1 << 20) || kw > (1 << 20)) return fail(DSS_E_UNSUPPORTED, "stride product too large");
+        ch.kstar_h[j] = (int)kh;
+        ch.kstar_w[j] = (int)kw;
+    }
+    ch.u_h.assign(L + 1, 1);
+    ch.u_w.assign(L + 1, 1);
+    for (int j = L; j >= 1; --j) {
+        const ChainLayer& c = ch.layers[j - 1];
+        const int64_t uh = (int64_t)c.k_h * ch.u_h[j] + c.c_h - 1;
+        const int64_t uw = (int64_t)c.k_w * ch.u_w[j] + c.c_w - 1;
+        if (uh > (1 << 28) || uw > (1 << 28)) return fail(DSS_E_UNSUPPORTED, "receptive field too large");
+        ch.u_h[j - 1] = (int)uh;
+        ch.u_w[j - 1] = (int)uw;
+    }
+    ch.B_h = ch.u_h[0];
+    ch.B_w = ch.u_w[0];
+    *out = std::move(ch);
+    return DSS_OK;
+}
+
+static int stuffing(int N, int B, int K) {
+    const int rem = (N - B + 1) % K;
+    return rem == 0 ? 0 : K - rem;
+}
+
+dss_status compute_geometry(const Chain& ch, dss_dtype dt, int H, int W, Geom* g) {
+    if (ch.ndim == 1 && H != 1) return fail(DSS_E_SHAPE, "1-D plan needs H = 1 (got %d)", H);
+    if (H < ch.B_h || W < ch.B_w)
+        return fail(DSS_E_SHAPE, "signal %dx%d is smaller than the receptive field %dx%d", H, W, ch.B_h, ch.B_w);
+    Geom G;
+    G.H = H;
+    G.W = W;
+    G.r_h = stuffing(H, ch.B_h, ch.K_h());
+    G.r_w = stuffing(W, ch.B_w, ch.K_w());
+    G.D_h = H + G.r_h;
+    G.D_w = W + G.r_w;
+    G.out_h = H - ch.B_h + 1;
+    G.out_w = W - ch.B_w + 1;
+    const double es = (double)dtype_size(dt);
+    const int L = ch.L();
+
+    int Uh = G.D_h, Uw = G.D_w;
+    int cur_c = ch.in_c;
+    int64_t maxbuf = (int64_t)G.D_h * G.D_w * ch.in_c * (int64_t)es;
+    G.total_bytes = (double)ch.in_c * H * W * es + (double)ch.in_c * G.D_h * G.D_w * es;
+    for (int j = 1; j <= L; ++j) {
+        const ChainLayer& c = ch.layers[j - 1];
+        LayerGeom lg;
+        lg.Uin_h = Uh;
+        lg.Uin_w = Uw;
+        lg.Fin_h = ch.kstar_h[j - 1];
+        lg.Fin_w = ch.kstar_w[j - 1];
+        lg.Fout_h = ch.kstar_h[j];
+        lg.Fout_w = ch.kstar_w[j];
+        const int64_t Fin = (int64_t)lg.Fin_h * lg.Fin_w;
+        lg.E_h = Uh - c.c_h + 1;
+        lg.E_w = Uw - c.c_w + 1;
+        if (lg.E_h < c.k_h || lg.E_w < c.k_w) return fail(DSS_E_SHAPE, "layer %d: extent underflow", j);
+        const int Ph = lg.E_h - c.k_h + 1, Pw = lg.E_w - c.k_w + 1;
+        if (Ph % c.k_h != 0 || Pw % c.k_w != 0)
+            return fail(DSS_E_SHAPE, "layer %d: sliding-pool extent %dx%d not divisible by %dx%d", j, Ph, Pw,
+                        c.k_h, c.k_w);
+        lg.U_h = Ph / c.k_h;
+        lg.U_w = Pw / c.k_w;
+        // the final conv of a bfloat16 plan stores binary32
+        const bool last_op = (j == L) && !c.has_pool;
+        if (c.has_conv) {
+            const double es_out = (dt == DSS_BF16 && last_op) ? 4.0 : es;
+            const double macs = (double)Fin * lg.E_h * lg.E_w * c.cout * (double)c.cin * c.c_h * c.c_w;
+            G.conv_flops += 2.0 * macs;
+            const int64_t out_b = Fin * lg.E_h * lg.E_w * c.cout * (int64_t)es_out;
+            maxbuf = std::max(maxbuf, out_b);
+            G.total_bytes += (double)Fin * Uh * Uw * c.cin * es + (double)out_b +
+                             (double)c.cout * c.cin * c.c_h * c.c_w * (dt == DSS_BF16 ? 2.0 : 4.0);
+        }
+        if (c.has_pool) {
+            const int64_t Fout = (int64_t)lg.Fout_h * lg.Fout_w;
+            const double pb = (double)Fin * lg.E_h * lg.E_w * c.cout * es + (double)Fout * lg.U_h * lg.U_w * c.cout * es;
+            G.pool_bytes += pb;
+            G.total_bytes += pb;
+            maxbuf = std::max(maxbuf, Fout * lg.U_h * lg.U_w * c.cout * (int64_t)es);
+        }
+        // Lemma (b): U_j = (D - k*_j + 1 - sum_{mu<=j} k*_{mu-1}(c_mu - 1)) / k*_j
+        int64_t sh = 0, sw = 0;
+        for (int mu = 1; mu <= j; ++mu) {
+            sh += (int64_t)ch.kstar_h[mu - 1] * (ch.layers[mu - 1].c_h - 1);
+            sw += (int64_t)ch.kstar_w[mu - 1] * (ch.layers[mu - 1].c_w - 1);
+        }
+        if ((G.D_h - ch.kstar_h[j] + 1 - sh) != (int64_t)lg.U_h * ch.kstar_h[j] ||
+            (G.D_w - ch.kstar_w[j] + 1 - sw) != (int64_t)lg.U_w * ch.kstar_w[j])
+            return fail(DSS_E_SHAPE, "layer %d: fragment extent disagrees with Lemma (b)", j);
+        G.L.push_back(lg);
+        Uh = lg.U_h;
+        Uw = lg.U_w;
+        cur_c = c.cout;
+    }
+    // Lemma (c) with u_L = 1: each of the k*_L fragments holds (D - B + 1)/k*_L outputs
+    if ((int64_t)Uh * ch.K_h() != (int64_t)G.D_h - ch.B_h + 1 || (int64_t)Uw * ch.K_w() != (int64_t)G.D_w - ch.B_w + 1)
+        return fail(DSS_E_SHAPE, "final fragment extent disagrees with Lemma (c)");
+    const bool last_f32 = dt == DSS_BF16 && !ch.layers.back().has_pool && ch.layers.back().has_conv;
+    const double es_last = last_f32 ? 4.0 : es;
+    G.total_bytes += (double)ch.K_h() * ch.K_w() * Uh * Uw * cur_c * es_last + (double)G.out_h * G.out_w * cur_c * 4.0;
+    G.buf_bytes = (maxbuf + 255) / 256 * 256;
+    G.ws_bytes = 2 * G.buf_bytes;
+    *g = std::move(G);
+    return DSS_OK;
+}
+
+}  // namespace dss

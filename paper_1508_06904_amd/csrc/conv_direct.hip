@@ -1,0 +1,94 @@
+// Direct (VALU) convolution over the fragment batch, fused bias + activation.
+//
+// The multi-channel convolution of Sect. 3.3 applied to every fragment
+// independently (Definition "fragmentwise evaluation", Sect. 4.2):
+//   out[f][y][x][o] = act( bias[o] + sum_{t_h, t_w, i} w[t_h][t_w][i][o] * in[f][y+t_h][x+t_w][i] )
+// for y < Hin - fh + 1, x < Win - fw + 1 (valid convolution, cross-correlation
+// tap order).  Used for the layers that do not suit the MFMA implicit GEMM: the
+// first layer (few input channels) and the final projections (few output
+// channels).  One thread computes COB consecutive output channels of one output
+// sample; the weight reads are uniform across the wavefront and go through the
+// scalar cache.  Accumulation is binary32 (bfloat16 activations are widened).
+#include "dev_common.h"
+#include "dss_internal.h"
+
+namespace dss {
+
+template <typename Tin, typename Tout, int COB, int VEC>
+__global__ __launch_bounds__(256) void conv_direct_kernel(const Tin* __restrict__ in, int Hin, int Win, int Cin,
+                                                         const float* __restrict__ w, const float* __restrict__ bias,
+                                                         int fh, int fw, int Cout, int CoutP, int act,
+                                                         Tout* __restrict__ out, int Hout, int Wout, int64_t npix) {
+    const int64_t p = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (p >= npix) return;
+    const int og = blockIdx.y * COB;
+    const int x = (int)(p % Wout);
+    const int64_t t = p / Wout;
+    const int y = (int)(t % Hout);
+    const int64_t f = t / Hout;
+    const Tin* base = in + ((f * Hin + y) * Win + x) * Cin;
+    float acc[COB];
+#pragma unroll
+    for (int o = 0; o < COB; ++o) acc[o] = bias[og + o];
+    for (int th = 0; th < fh; ++th) {
+        for (int tw = 0; tw < fw; ++tw) {
+            const Tin* px = base + ((int64_t)th * Win + tw) * Cin;
+            const float* wr = w + (int64_t)((th * fw + tw) * Cin) * CoutP + og;
+            for (int i = 0; i < Cin; i += VEC) {
+                float v[VEC];
+                VecIO<Tin, VEC>::load(px + i, v);
+#pragma unroll
+                for (int e = 0; e < VEC; ++e) {
+#pragma unroll
+                    for (int o = 0; o < COB; ++o) acc[o] = fmaf(v[e], wr[(int64_t)(i + e) * CoutP + o], acc[o]);
+                }
+            }
+        }
+    }
+    Tout* op = out + p * Cout + og;
+#pragma unroll
+    for (int o = 0; o < COB; ++o)
+        if (og + o < Cout) store_elem(op + o, activate(act, acc[o]));
+}
+
+template <typename Tin, typename Tout, int COB>
+static void run_direct(const void* in, int F, int Hin, int Win, int Cin, const PlanConv& pc, void* out,
+                       hipStream_t s) {
+    const int Hout = Hin - pc.fh + 1, Wout = Win - pc.fw + 1;
+    const int64_t npix = (int64_t)F * Hout * Wout;
+    const dim3 grid((unsigned)ceil_div64(npix, 256), (unsigned)(pc.cout_pad / COB));
+    const int vec_ok = (Cin % 4 == 0);
+    if (vec_ok)
+        conv_direct_kernel<Tin, Tout, COB, 4><<<grid, 256, 0, s>>>((const Tin*)in, Hin, Win, Cin, (const float*)pc.w,
+                                                                   pc.b, pc.fh, pc.fw, pc.cout, pc.cout_pad, pc.act,
+                                                                   (Tout*)out, Hout, Wout, npix);
+    else
+        conv_direct_kernel<Tin, Tout, COB, 1><<<grid, 256, 0, s>>>((const Tin*)in, Hin, Win, Cin, (const float*)pc.w,
+                                                                   pc.b, pc.fh, pc.fw, pc.cout, pc.cout_pad, pc.act,
+                                                                   (Tout*)out, Hout, Wout, npix);
+}
+
+template <typename Tin, typename Tout>
+static void dispatch_cob(const void* in, int F, int Hin, int Win, int Cin, const PlanConv& pc, void* out,
+                         hipStream_t s) {
+    switch (pc.cob) {
+        case 16: run_direct<Tin, Tout, 16>(in, F, Hin, Win, Cin, pc, out, s); break;
+        case 8: run_direct<Tin, Tout, 8>(in, F, Hin, Win, Cin, pc, out, s); break;
+        case 4: run_direct<Tin, Tout, 4>(in, F, Hin, Win, Cin, pc, out, s); break;
+        case 2: run_direct<Tin, Tout, 2>(in, F, Hin, Win, Cin, pc, out, s); break;
+        default: run_direct<Tin, Tout, 1>(in, F, Hin, Win, Cin, pc, out, s); break;
+    }
+}
+
+hipError_t launch_conv_direct(dss_dtype tin, dss_dtype tout, const void* in, int F, int Hin, int Win, int Cin,
+                              const PlanConv& pc, void* out, hipStream_t s) {
+    if (tin == DSS_F32)
+        dispatch_cob<float, float>(in, F, Hin, Win, Cin, pc, out, s);
+    else if (tout == DSS_F32)
+        dispatch_cob<uint16_t, float>(in, F, Hin, Win, Cin, pc, out, s);
+    else
+        dispatch_cob<uint16_t, uint16_t>(in, F, Hin, Win, Cin, pc, out, s);
+    return hipGetLastError();
+}
+
+}  // namespace dss

@@ -1,0 +1,340 @@
+// Convolution over the fragment batch as an MFMA implicit GEMM (gfx950).
+//
+// Every fragment is an independent signal (Definition "fragmentwise
+// evaluation", Sect. 4.2), so all fragments of a layer form one batch of
+// ordinary valid convolutions (Sect. 3.3 and its 2-D form in Sect. 6.1):
+//   out[f][y][x][o] = act( bias[o] + sum_{t_h,t_w,i} W[o][i][t_h][t_w] * in[f][y+t_h][x+t_w][i] )
+// As a GEMM: M = output samples (a TH x TW spatial tile of one fragment per
+// workgroup), N = output channels, K = fh * fw * Cin.
+//
+// Workgroup = 4 wavefronts of 64 lanes; each wave owns a 64 x (32*NT) block of
+// the output tile, computed with 32x32 MFMA tiles:
+//   binary32:  v_mfma_f32_32x32x2_f32   (K = 2 per issue)
+//   bfloat16:  v_mfma_f32_32x32x16_bf16 (K = 16 per issue), binary32 accumulation
+// K loop: input channels in chunks of 64 bytes per sample (16 binary32 or 32
+// bfloat16 channels) x filter taps.  For each chunk the input halo tile
+// (TH + fh - 1) x (TW + fw - 1) x chunk is staged in LDS once and reused by all
+// fh * fw taps; the weight slice of one (chunk, tap) pair, BN x chunk, is
+// double-buffered in LDS while the previous slice feeds the MFMAs.  Sample and
+// weight rows use an 80-byte LDS pitch so that the 32-byte operand reads of a
+// wavefront spread over all banks.
+//
+// K-index assignment inside one MFMA issue: lane half h (lanes 32h..32h+31)
+// holds input channels h*8 + s (binary32, issue s of 8) or h*16 + 8s .. +7
+// (bfloat16, issue s of 2) of the chunk; A and B use the same assignment, so
+// every product pairs an input sample with its own weight.
+//
+// Epilogue: + bias, activation, masked store (edge tiles, padded channels) in
+// the channels-last output layout; binary32 or bfloat16 (round to nearest even).
+#include "dev_common.h"
+#include "dss_internal.h"
+
+namespace dss {
+
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+
+constexpr int kPitchBytes = 80;     // LDS bytes per staged sample / weight row
+constexpr int kChunkBytes = 64;     // bytes of one channel chunk per sample
+constexpr int kMaxLds = 64 * 1024;
+
+template <bool BF16, int WGM, int WGN, int NT>
+struct MfmaCfg {
+    static constexpr int ES = BF16 ? 2 : 4;
+    static constexpr int CC = kChunkBytes / ES;        // channels per chunk
+    static constexpr int BM = 64 * WGM;                 // output samples per workgroup
+    static constexpr int BN = 32 * NT * WGN;            // output channels per workgroup
+    static constexpr int THREADS = 64 * WGM * WGN;
+    static constexpr int WSLICE_UNITS = BN * (kChunkBytes / 16);  // 16-byte units per weight slice
+};
+
+__device__ __forceinline__ floatx16 mfma_step_f32(const float* a, const float* b, int s, floatx16 acc) {
+    return __builtin_amdgcn_mfma_f32_32x32x2f32(a[s], b[s], acc, 0, 0, 0);
+}
+
+__device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8, v); }
+
+template <bool BF16, typename Tout, int WGM, int WGN, int NT>
+__global__ __launch_bounds__(256) void conv_mfma_kernel(
+    const char* __restrict__ in,       // [F][Hin][Win][Cin] of BF16 ? bfloat16 : binary32
+    int Hin, int Win, int Cin,
+    const char* __restrict__ wp,       // packed [nb][chunk][th][tw][BN][chunk channels]
+    const float* __restrict__ bias,    // [Cout_pad]
+    int fh, int fw, int Cout, int act, int nchunks,
+    Tout* __restrict__ out,            // [F][Hout][Wout][Cout]
+    int Hout, int Wout, int TH, int TW, int tilesY, int tilesX) {
+    using Cfg = MfmaCfg<BF16, WGM, WGN, NT>;
+    extern __shared__ __attribute__((aligned(16))) char lds[];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int wm = wave % WGM;           // wave position along M
+    const int wn = wave / WGM;           // wave position along N
+    const int half = lane >> 5;          // lane half: K slot of the MFMA operands
+    const int l32 = lane & 31;
+
+    // workgroup -> (fragment, tile row, tile column), N block
+    const int tiles = tilesY * tilesX;
+    const int f = blockIdx.x / tiles;
+    const int trem = blockIdx.x % tiles;
+    const int ty0 = (trem / tilesX) * TH;
+    const int tx0 = (trem % tilesX) * TW;
+    const int nb = blockIdx.y;
+
+    const int HH = TH + fh - 1, HW = TW + fw - 1;   // halo extents
+    const int halo_px = HH * HW;
+    char* halo = lds;
+    char* wbuf0 = lds + ((halo_px * kPitchBytes + 127) / 128) * 128;
+    char* wbuf1 = wbuf0 + Cfg::BN * kPitchBytes;
+
+    // per-lane operand offsets (bytes) inside the halo / weight slice
+    int a_off[2];
+#pragma unroll
+    for (int mt = 0; mt < 2; ++mt) {
+        const int m = wm * 64 + mt * 32 + l32;
+        a_off[mt] = ((m / TW) * HW + (m % TW)) * kPitchBytes + half * 32;
+    }
+    int b_off[NT];
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) b_off[nt] = (wn * 32 * NT + nt * 32 + l32) * kPitchBytes + half * 32;
+
+    floatx16 acc[2][NT];
+#pragma unroll
+    for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) acc[mt][nt][v] = 0.f;
+
+    const int taps = fh * fw;
+    const int steps = nchunks * taps;
+    const size_t row_bytes = (size_t)Cin * Cfg::ES;
+    const char* in_f = in + (size_t)f * Hin * Win * row_bytes;
+    const char* w_nb = wp + (size_t)nb * steps * (Cfg::BN * kChunkBytes);
+
+    // -- staging helpers
+    auto load_halo = [&](int cc) {
+        const int units = halo_px * 4;
+        for (int u = tid; u < units; u += Cfg::THREADS) {
+            const int px = u >> 2, q = u & 3;
+            const int y = ty0 + px / HW, x = tx0 + px % HW;
+            const int c0 = cc * Cfg::CC + q * (16 / Cfg::ES);
+            uint4 v = make_uint4(0, 0, 0, 0);
+            if (y < Hin && x < Win && c0 < Cin)
+                v = *reinterpret_cast<const uint4*>(in_f + ((size_t)y * Win + x) * row_bytes + (size_t)c0 * Cfg::ES);
+            *reinterpret_cast<uint4*>(halo + px * kPitchBytes + q * 16) = v;
+        }
+    };
+    constexpr int WU = Cfg::WSLICE_UNITS;
+    constexpr int WPER = (WU + Cfg::THREADS - 1) / Cfg::THREADS;
+    uint4 wreg[WPER];
+    auto load_w = [&](int step) {
+        const char* src = w_nb + (size_t)step * (Cfg::BN * kChunkBytes);
+#pragma unroll
+        for (int r = 0; r < WPER; ++r) {
+            const int u = tid + r * Cfg::THREADS;
+            if (WU % Cfg::THREADS == 0 || u < WU) wreg[r] = *reinterpret_cast<const uint4*>(src + (size_t)u * 16);
+        }
+    };
+    auto store_w = [&](char* dst) {
+#pragma unroll
+        for (int r = 0; r < WPER; ++r) {
+            const int u = tid + r * Cfg::THREADS;
+            if (WU % Cfg::THREADS == 0 || u < WU)
+                *reinterpret_cast<uint4*>(dst + (u >> 2) * kPitchBytes + (u & 3) * 16) = wreg[r];
+        }
+    };
+
+    // -- prologue
+    load_halo(0);
+    load_w(0);
+    store_w(wbuf0);
+    __syncthreads();
+
+    for (int step = 0; step < steps; ++step) {
+        const int next = step + 1;
+        if (next < steps) load_w(next);
+
+        const int tap = step % taps;
+        const int th = tap / fw, tw = tap % fw;
+        const int tap_off = (th * HW + tw) * kPitchBytes;
+        const char* wcur = (step & 1) ? wbuf1 : wbuf0;
+
+        uint4 a[2][2], b[NT][2];
+#pragma unroll
+        for (int mt = 0; mt < 2; ++mt) {
+            a[mt][0] = *reinterpret_cast<const uint4*>(halo + a_off[mt] + tap_off);
+            a[mt][1] = *reinterpret_cast<const uint4*>(halo + a_off[mt] + tap_off + 16);
+        }
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+            b[nt][0] = *reinterpret_cast<const uint4*>(wcur + b_off[nt]);
+            b[nt][1] = *reinterpret_cast<const uint4*>(wcur + b_off[nt] + 16);
+        }
+        if constexpr (BF16) {
+#pragma unroll
+            for (int s = 0; s < 2; ++s)
+#pragma unroll
+                for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+                    for (int nt = 0; nt < NT; ++nt)
+                        acc[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a[mt][s]), as_bf16x8(b[nt][s]),
+                                                                              acc[mt][nt], 0, 0, 0);
+        } else {
+            float af[2][8], bf[NT][8];
+#pragma unroll
+            for (int mt = 0; mt < 2; ++mt) {
+                const uint32_t w8[8] = {a[mt][0].x, a[mt][0].y, a[mt][0].z, a[mt][0].w,
+                                        a[mt][1].x, a[mt][1].y, a[mt][1].z, a[mt][1].w};
+#pragma unroll
+                for (int s = 0; s < 8; ++s) af[mt][s] = __uint_as_float(w8[s]);
+            }
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt) {
+                const uint32_t w8[8] = {b[nt][0].x, b[nt][0].y, b[nt][0].z, b[nt][0].w,
+                                        b[nt][1].x, b[nt][1].y, b[nt][1].z, b[nt][1].w};
+#pragma unroll
+                for (int s = 0; s < 8; ++s) bf[nt][s] = __uint_as_float(w8[s]);
+            }
+#pragma unroll
+            for (int s = 0; s < 8; ++s)
+#pragma unroll
+                for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+                    for (int nt = 0; nt < NT; ++nt) acc[mt][nt] = mfma_step_f32(af[mt], bf[nt], s, acc[mt][nt]);
+        }
+
+        if (next < steps) {
+            store_w((next & 1) ? wbuf1 : wbuf0);
+            if (next % taps == 0) {
+                __syncthreads();          // every wave is done with the current halo
+                load_halo(next / taps);
+            }
+        }
+        __syncthreads();
+    }
+
+    // -- epilogue: D[i][j] of a 32x32 tile sits in lane j + 32*((i/4)%2), register (i/8)*4 + i%4
+    const int n_base = nb * Cfg::BN + wn * 32 * NT;
+    const size_t f_off = (size_t)f * Hout * Wout;
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+        const int n = n_base + nt * 32 + l32;
+        if (n >= Cout) continue;
+        const float bn = bias[n];
+#pragma unroll
+        for (int mt = 0; mt < 2; ++mt) {
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const int i = (v >> 2) * 8 + half * 4 + (v & 3);
+                const int m = wm * 64 + mt * 32 + i;
+                const int y = ty0 + m / TW, x = tx0 + m % TW;
+                if (y < Hout && x < Wout)
+                    store_elem(out + (f_off + (size_t)y * Wout + x) * Cout + n, activate(act, acc[mt][nt][v] + bn));
+            }
+        }
+    }
+}
+
+// ------------------------------------------------------------------ host side
+
+int mfma_f32_pick_bn(int cout) { return cout >= 128 ? 128 : cout >= 64 ? 64 : 32; }
+int mfma_bf16_pick_bn(int cout) { return cout >= 128 ? 128 : cout >= 64 ? 64 : 32; }
+
+static size_t packed_elems(const PlanConv& pc, int cc) {
+    return (size_t)(pc.cout_pad / pc.bn) * (pc.cin_pad / cc) * pc.fh * pc.fw * pc.bn * cc;
+}
+size_t mfma_f32_packed_floats(const PlanConv& pc) { return packed_elems(pc, 16); }
+size_t mfma_bf16_packed_elems(const PlanConv& pc) { return packed_elems(pc, 32); }
+
+// Packed weight layout: [nb][chunk][th][tw][n in BN][c in chunk], so that the
+// slice of one (chunk, tap) pair is one contiguous BN x 64-byte block.
+template <typename E, typename Conv>
+static void pack_weights(const PlanConv& pc, int cc, const float* w, E* dst, Conv conv) {
+    const int nbs = pc.cout_pad / pc.bn, nch = pc.cin_pad / cc;
+    size_t idx = 0;
+    for (int nb = 0; nb < nbs; ++nb)
+        for (int ch = 0; ch < nch; ++ch)
+            for (int th = 0; th < pc.fh; ++th)
+                for (int tw = 0; tw < pc.fw; ++tw)
+                    for (int nl = 0; nl < pc.bn; ++nl)
+                        for (int cl = 0; cl < cc; ++cl, ++idx) {
+                            const int o = nb * pc.bn + nl, i = ch * cc + cl;
+                            float v = 0.f;
+                            if (o < pc.cout && i < pc.cin) v = w[(((size_t)o * pc.cin + i) * pc.fh + th) * pc.fw + tw];
+                            dst[idx] = conv(v);
+                        }
+}
+
+void mfma_f32_pack(const PlanConv& pc, const float* w, float* dst) {
+    pack_weights(pc, 16, w, dst, [](float v) { return v; });
+}
+void mfma_bf16_pack(const PlanConv& pc, const float* w, uint16_t* dst) {
+    pack_weights(pc, 32, w, dst, [](float v) { return host_f32_to_bf16(v); });
+}
+
+struct Tile {
+    int TH, TW;
+    size_t lds;
+};
+
+// Spatial tile TH x TW = BM output samples: the shape that wastes the fewest
+// masked samples on this layer's fragment extent, then the smallest halo.
+static Tile pick_tile(int BM, int BN, int Hout, int Wout, int fh, int fw) {
+    Tile best{0, 0, 0};
+    int64_t best_work = -1, best_halo = -1;
+    for (int TW = 8; TW <= BM; TW *= 2) {
+        const int TH = BM / TW;
+        const int64_t halo_px = (int64_t)(TH + fh - 1) * (TW + fw - 1);
+        const size_t lds = (size_t)((halo_px * kPitchBytes + 127) / 128) * 128 + 2 * (size_t)BN * kPitchBytes;
+        if (lds > (size_t)kMaxLds) continue;
+        const int64_t work = ceil_div64(Hout, TH) * TH * ceil_div64(Wout, TW) * TW;
+        if (best_work < 0 || work < best_work || (work == best_work && halo_px < best_halo)) {
+            best = Tile{TH, TW, lds};
+            best_work = work;
+            best_halo = halo_px;
+        }
+    }
+    return best;
+}
+
+template <bool BF16, typename Tout, int WGM, int WGN, int NT>
+static hipError_t run_mfma(const void* in, int F, int Hin, int Win, const PlanConv& pc, void* out, hipStream_t s) {
+    using Cfg = MfmaCfg<BF16, WGM, WGN, NT>;
+    const int Hout = Hin - pc.fh + 1, Wout = Win - pc.fw + 1;
+    const Tile t = pick_tile(Cfg::BM, Cfg::BN, Hout, Wout, pc.fh, pc.fw);
+    if (t.TH == 0) return hipErrorInvalidConfiguration;
+    const int tilesY = (int)ceil_div64(Hout, t.TH), tilesX = (int)ceil_div64(Wout, t.TW);
+    const int64_t nblocks = (int64_t)F * tilesY * tilesX;
+    if (nblocks >= (1ll << 31)) return hipErrorInvalidConfiguration;
+    const dim3 grid((unsigned)nblocks, (unsigned)(pc.cout_pad / Cfg::BN));
+    const int nchunks = pc.cin_pad / Cfg::CC;
+    conv_mfma_kernel<BF16, Tout, WGM, WGN, NT><<<grid, Cfg::THREADS, t.lds, s>>>(
+        (const char*)in, Hin, Win, pc.cin, (const char*)pc.w, pc.b, pc.fh, pc.fw, pc.cout, pc.act, nchunks,
+        (Tout*)out, Hout, Wout, t.TH, t.TW, tilesY, tilesX);
+    return hipGetLastError();
+}
+
+template <bool BF16, typename Tout>
+static hipError_t dispatch_bn(const void* in, int F, int Hin, int Win, const PlanConv& pc, void* out, hipStream_t s) {
+    switch (pc.bn) {
+        case 128: return run_mfma<BF16, Tout, 2, 2, 2>(in, F, Hin, Win, pc, out, s);
+        case 64: return run_mfma<BF16, Tout, 4, 1, 2>(in, F, Hin, Win, pc, out, s);
+        case 32: return run_mfma<BF16, Tout, 4, 1, 1>(in, F, Hin, Win, pc, out, s);
+    }
+    return hipErrorInvalidValue;
+}
+
+hipError_t launch_conv_mfma_f32(const float* in, int F, int Hin, int Win, const PlanConv& pc, float* out,
+                                hipStream_t s) {
+    return dispatch_bn<false, float>(in, F, Hin, Win, pc, out, s);
+}
+
+hipError_t launch_conv_mfma_bf16(dss_dtype tout, const uint16_t* in, int F, int Hin, int Win, const PlanConv& pc,
+                                 void* out, hipStream_t s) {
+    if (tout == DSS_F32) return dispatch_bn<true, float>(in, F, Hin, Win, pc, out, s);
+    return dispatch_bn<true, uint16_t>(in, F, Hin, Win, pc, out, s);
+}
+
+}  // namespace dss

@@ -1,0 +1,131 @@
+// Internal declarations of the dense-signal-scanning library: the processing
+// chain built from the layer list, the per-signal geometry, the plan, and the
+// kernel launchers.  Host code only sees these; kernels live in the .hip files.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "../../include/dss.h"
+
+namespace dss {
+
+// ------------------------------------------------------------------ errors
+void set_error(const char* fmt, ...);
+dss_status fail(dss_status s, const char* fmt, ...);
+dss_status hip_fail(hipError_t e, const char* what);
+
+// ------------------------------------------------------------------ chain
+// One layer of the processing chain (Definition "processing chain", Sect. 4.2):
+// a subsignal compatible transformation T_j (a convolution + bias + activation,
+// or the identity) followed by a pooling kernel g_j with block size k_j
+// (k_j = 1: bypass, end of Sect. 4.2).
+struct ChainLayer {
+    bool has_conv = false, has_pool = false;
+    int c_h = 1, c_w = 1;       // dimensionality reduction constant of T_j
+    int k_h = 1, k_w = 1;       // pool block size
+    int cin = 0, cout = 0;      // channels entering / leaving the layer
+    int act = DSS_ACT_NONE;
+    int desc = -1;              // index of the conv descriptor in the caller's list
+};
+
+struct Chain {
+    int ndim = 2, in_c = 0;
+    std::vector<ChainLayer> layers;          // L entries
+    int B_h = 1, B_w = 1;                    // receptive field
+    std::vector<int> kstar_h, kstar_w;       // k*_0..k*_L
+    std::vector<int> u_h, u_w;               // u_0..u_L (Lemma (a))
+    int K_h() const { return kstar_h.back(); }
+    int K_w() const { return kstar_w.back(); }
+    int L() const { return (int)layers.size(); }
+    int out_c() const { return layers.empty() ? in_c : layers.back().cout; }
+};
+
+dss_status build_chain(const dss_layer* layers, int n, int ndim, int in_c, Chain* out);
+
+// Geometry of one chain layer for a given stuffed signal.
+struct LayerGeom {
+    int Uin_h, Uin_w;   // fragment extent entering the layer (U_{j-1})
+    int E_h, E_w;       // extent after T_j (U_{j-1} - c_j + 1)
+    int U_h, U_w;       // extent after Slide_g + Frag (U_j)
+    int Fin_h, Fin_w;   // fragments entering (k*_{j-1})
+    int Fout_h, Fout_w; // fragments leaving (k*_j)
+};
+
+struct Geom {
+    int H = 0, W = 0, r_h = 0, r_w = 0, D_h = 0, D_w = 0, out_h = 0, out_w = 0;
+    std::vector<LayerGeom> L;
+    int64_t buf_bytes = 0;      // one ping-pong buffer
+    int64_t ws_bytes = 0;       // both buffers
+    double conv_flops = 0, pool_bytes = 0, total_bytes = 0;
+};
+
+size_t dtype_size(dss_dtype dt);
+dss_status compute_geometry(const Chain& ch, dss_dtype dt, int H, int W, Geom* g);
+
+// ------------------------------------------------------------------ plan
+enum ConvImpl { CONV_DIRECT = 0, CONV_MFMA_F32 = 1, CONV_MFMA_BF16 = 2 };
+
+struct PlanConv {
+    ConvImpl impl = CONV_DIRECT;
+    int cin = 0, cout = 0, fh = 1, fw = 1, act = 0;
+    int cob = 1, cout_pad = 0;  // direct kernel: outputs per thread, padded Cout
+    int bn = 0, cin_pad = 0;    // MFMA kernels: N tile, padded Cin
+    void* w = nullptr;          // device weights in the kernel's layout
+    float* b = nullptr;         // device bias [cout_pad], zero padded
+};
+
+struct LaunchRec {
+    const char* name;
+    int layer;
+    double flops, bytes;
+    int ev0, ev1;
+};
+
+}  // namespace dss
+
+struct dss_plan {
+    dss::Chain chain;
+    dss_dtype dtype = DSS_F32;
+    int device = 0;
+    std::vector<dss::PlanConv> convs;     // one per chain layer (impl unused if no conv)
+    bool timing = false;
+    std::vector<hipEvent_t> events;
+    std::vector<dss::LaunchRec> recs;
+};
+
+namespace dss {
+
+// ------------------------------------------------------------------ kernel launchers
+// Element types: binary32 activations are float, bfloat16 activations uint16_t bits.
+hipError_t launch_stuff_pack(dss_dtype dt, const void* in, int C, int H, int W, void* out, int D_h,
+                             int D_w, hipStream_t s);
+hipError_t launch_conv_direct(dss_dtype tin, dss_dtype tout, const void* in, int F, int Hin, int Win,
+                              int Cin, const PlanConv& pc, void* out, hipStream_t s);
+hipError_t launch_conv_mfma_f32(const float* in, int F, int Hin, int Win, const PlanConv& pc,
+                                float* out, hipStream_t s);
+hipError_t launch_conv_mfma_bf16(dss_dtype tout, const uint16_t* in, int F, int Hin, int Win,
+                                 const PlanConv& pc, void* out, hipStream_t s);
+hipError_t launch_pool_frag(dss_dtype dt, const void* in, int S_h, int S_w, int E_h, int E_w, int C,
+                            int k_h, int k_w, void* out, hipStream_t s);
+hipError_t launch_defrag_trim(dss_dtype dt, const void* in, int K_h, int K_w, int U_h, int U_w, int C,
+                              float* out, int O_h, int O_w, hipStream_t s);
+hipError_t launch_to_planar(dss_dtype dt, const void* in, int F, int h, int w, int C, float* out,
+                            hipStream_t s);
+hipError_t launch_frag_planar(int elem_bytes, bool inverse, const void* in, int k_h, int k_w, int S_h,
+                              int S_w, int C, int H, int W, void* out, hipStream_t s);
+
+// host-side weight packing for the MFMA kernels (conv_mfma_*.hip)
+int mfma_f32_pick_bn(int cout);
+int mfma_bf16_pick_bn(int cout);
+size_t mfma_f32_packed_floats(const PlanConv& pc);
+void mfma_f32_pack(const PlanConv& pc, const float* w_oihw, float* dst);
+size_t mfma_bf16_packed_elems(const PlanConv& pc);
+void mfma_bf16_pack(const PlanConv& pc, const float* w_oihw, uint16_t* dst);
+
+uint16_t host_f32_to_bf16(float f);
+
+}  // namespace dss

@@ -1,0 +1,218 @@
+// Data-movement kernels of the dense evaluation.  All are HBM-bound streaming
+// kernels: no arithmetic besides the channel-wise maximum of the pool.
+//
+//  stuff_pack   Stuff_r per axis (Definition "stuff-trim", Sect. 4.3): copy the
+//               planar [C][H][W] signal into the channels-last [D_h][D_w][C]
+//               working layout and append r dummy samples (zeta = +0) at the end
+//               of each axis.
+//  pool_frag    Slide_{g_max} followed by Frag_k (Definition "processing chain",
+//               Sect. 4.2): the k_h x k_w maximum at every position of every
+//               fragment (stride 1), written straight to its fragment after
+//               fragmentation.  Per axis, sliding-pool sample m*k + a of input
+//               fragment b lands at sample m of output fragment a*S + b
+//               (Lemma "frag-ops", Sect. 4.1).
+//  defrag_trim  Defrag_{k*_L} and Trim_r (appendix lemma on the simplified
+//               defragmentation; Definition "stuff-trim"): dense output sample
+//               (i, j) is sample (i div K_h, j div K_w) of fragment
+//               (i mod K_h) * K_w + (j mod K_w); only i < H - B_h + 1,
+//               j < W - B_w + 1 are written.  Output is planar binary32.
+//  to_planar    channels-last fragments -> planar binary32 [F][C][h][w].
+//  frag_planar  dss_frag / dss_defrag on planar tensors (pure permutations of
+//               2- or 4-byte elements).
+#include "dev_common.h"
+#include "dss_internal.h"
+
+namespace dss {
+
+constexpr int kThreads = 256;
+
+// ------------------------------------------------------------------ stuff_pack
+template <typename E>
+__global__ __launch_bounds__(kThreads) void stuff_pack_kernel(const E* __restrict__ in, int C, int H, int W,
+                                                             E* __restrict__ out, int D_h, int D_w) {
+    const int64_t p = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (p >= (int64_t)D_h * D_w) return;
+    const int y = (int)(p / D_w), x = (int)(p % D_w);
+    E* o = out + p * C;
+    if (y < H && x < W) {
+        for (int c = 0; c < C; ++c) o[c] = in[((int64_t)c * H + y) * W + x];
+    } else {
+        for (int c = 0; c < C; ++c) o[c] = E(0);
+    }
+}
+
+hipError_t launch_stuff_pack(dss_dtype dt, const void* in, int C, int H, int W, void* out, int D_h, int D_w,
+                             hipStream_t s) {
+    const int64_t n = (int64_t)D_h * D_w;
+    const dim3 grid((unsigned)ceil_div64(n, kThreads));
+    if (dt == DSS_BF16)
+        stuff_pack_kernel<uint16_t><<<grid, kThreads, 0, s>>>((const uint16_t*)in, C, H, W, (uint16_t*)out, D_h, D_w);
+    else
+        stuff_pack_kernel<uint32_t><<<grid, kThreads, 0, s>>>((const uint32_t*)in, C, H, W, (uint32_t*)out, D_h, D_w);
+    return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ pool_frag
+// One thread per (input fragment, sliding-pool position, group of V channels).
+template <typename T, int V>
+__global__ __launch_bounds__(kThreads) void pool_frag_kernel(const T* __restrict__ in, int S_h, int S_w, int E_h,
+                                                            int E_w, int C, int k_h, int k_w, T* __restrict__ out,
+                                                            int U_h, int U_w) {
+    const int CV = C / V;
+    const int P_h = k_h * U_h, P_w = k_w * U_w;   // sliding-pool extents
+    const int64_t total = (int64_t)S_h * S_w * P_h * P_w * CV;
+    const int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (idx >= total) return;
+    const int cv = (int)(idx % CV);
+    int64_t t = idx / CV;
+    const int x = (int)(t % P_w);
+    t /= P_w;
+    const int y = (int)(t % P_h);
+    const int s = (int)(t / P_h);
+    const int b_h = s / S_w, b_w = s % S_w;
+
+    const T* src = in + (((int64_t)s * E_h + y) * E_w + x) * C + cv * V;
+    float m[V];
+    VecIO<T, V>::load(src, m);
+    for (int dy = 0; dy < k_h; ++dy) {
+        for (int dx = 0; dx < k_w; ++dx) {
+            if ((dy | dx) == 0) continue;
+            float v[V];
+            VecIO<T, V>::load(src + ((int64_t)dy * E_w + dx) * C, v);
+#pragma unroll
+            for (int e = 0; e < V; ++e) m[e] = fmaxf(m[e], v[e]);
+        }
+    }
+    const int a_h = y % k_h, a_w = x % k_w;
+    const int f_new = (a_h * S_h + b_h) * (k_w * S_w) + (a_w * S_w + b_w);
+    T* dst = out + (((int64_t)f_new * U_h + y / k_h) * U_w + x / k_w) * C + cv * V;
+    VecIO<T, V>::store(dst, m);
+}
+
+template <typename T, int V>
+static void run_pool(const void* in, int S_h, int S_w, int E_h, int E_w, int C, int k_h, int k_w, void* out,
+                     hipStream_t s) {
+    const int U_h = (E_h - k_h + 1) / k_h, U_w = (E_w - k_w + 1) / k_w;
+    const int64_t total = (int64_t)S_h * S_w * (k_h * U_h) * (k_w * U_w) * (C / V);
+    pool_frag_kernel<T, V><<<dim3((unsigned)ceil_div64(total, kThreads)), kThreads, 0, s>>>(
+        (const T*)in, S_h, S_w, E_h, E_w, C, k_h, k_w, (T*)out, U_h, U_w);
+}
+
+hipError_t launch_pool_frag(dss_dtype dt, const void* in, int S_h, int S_w, int E_h, int E_w, int C, int k_h,
+                            int k_w, void* out, hipStream_t s) {
+    if (dt == DSS_BF16) {
+        if (C % 8 == 0) run_pool<uint16_t, 8>(in, S_h, S_w, E_h, E_w, C, k_h, k_w, out, s);
+        else if (C % 4 == 0) run_pool<uint16_t, 4>(in, S_h, S_w, E_h, E_w, C, k_h, k_w, out, s);
+        else run_pool<uint16_t, 1>(in, S_h, S_w, E_h, E_w, C, k_h, k_w, out, s);
+    } else {
+        if (C % 4 == 0) run_pool<float, 4>(in, S_h, S_w, E_h, E_w, C, k_h, k_w, out, s);
+        else run_pool<float, 1>(in, S_h, S_w, E_h, E_w, C, k_h, k_w, out, s);
+    }
+    return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ defrag_trim
+template <typename T>
+__global__ __launch_bounds__(kThreads) void defrag_trim_kernel(const T* __restrict__ in, int K_h, int K_w, int U_h,
+                                                              int U_w, int C, float* __restrict__ out, int O_h,
+                                                              int O_w) {
+    const int64_t p = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (p >= (int64_t)O_h * O_w) return;
+    const int i = (int)(p / O_w), j = (int)(p % O_w);
+    const int f = (i % K_h) * K_w + (j % K_w);
+    const T* src = in + (((int64_t)f * U_h + i / K_h) * U_w + j / K_w) * C;
+    for (int c = 0; c < C; ++c) out[(int64_t)c * O_h * O_w + p] = to_f32(src[c]);
+}
+
+hipError_t launch_defrag_trim(dss_dtype dt, const void* in, int K_h, int K_w, int U_h, int U_w, int C, float* out,
+                              int O_h, int O_w, hipStream_t s) {
+    const dim3 grid((unsigned)ceil_div64((int64_t)O_h * O_w, kThreads));
+    if (dt == DSS_BF16)
+        defrag_trim_kernel<uint16_t><<<grid, kThreads, 0, s>>>((const uint16_t*)in, K_h, K_w, U_h, U_w, C, out, O_h, O_w);
+    else
+        defrag_trim_kernel<float><<<grid, kThreads, 0, s>>>((const float*)in, K_h, K_w, U_h, U_w, C, out, O_h, O_w);
+    return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ to_planar
+template <typename T>
+__global__ __launch_bounds__(kThreads) void to_planar_kernel(const T* __restrict__ in, int F, int h, int w, int C,
+                                                            float* __restrict__ out) {
+    const int64_t p = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    const int64_t hw = (int64_t)h * w;
+    if (p >= (int64_t)F * hw) return;
+    const int64_t f = p / hw, q = p % hw;
+    const T* src = in + p * C;
+    for (int c = 0; c < C; ++c) out[(f * C + c) * hw + q] = to_f32(src[c]);
+}
+
+hipError_t launch_to_planar(dss_dtype dt, const void* in, int F, int h, int w, int C, float* out, hipStream_t s) {
+    const dim3 grid((unsigned)ceil_div64((int64_t)F * h * w, kThreads));
+    if (dt == DSS_BF16)
+        to_planar_kernel<uint16_t><<<grid, kThreads, 0, s>>>((const uint16_t*)in, F, h, w, C, out);
+    else
+        to_planar_kernel<float><<<grid, kThreads, 0, s>>>((const float*)in, F, h, w, C, out);
+    return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ frag / defrag (planar)
+// One thread per output element; consecutive threads write consecutive
+// samples of one output row.
+template <typename E>
+__global__ __launch_bounds__(kThreads) void frag_planar_kernel(const E* __restrict__ in, int k_h, int k_w, int S_h,
+                                                              int S_w, int C, int H, int W, E* __restrict__ out) {
+    const int Ho = H / k_h, Wo = W / k_w;
+    const int64_t total = (int64_t)k_h * S_h * k_w * S_w * C * Ho * Wo;
+    const int64_t p = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (p >= total) return;
+    const int n = (int)(p % Wo);
+    int64_t t = p / Wo;
+    const int m = (int)(t % Ho);
+    t /= Ho;
+    const int c = (int)(t % C);
+    const int fo = (int)(t / C);
+    const int Fw = k_w * S_w;
+    const int fh = fo / Fw, fw = fo % Fw;
+    const int a_h = fh / S_h, b_h = fh % S_h, a_w = fw / S_w, b_w = fw % S_w;
+    out[p] = in[(((int64_t)(b_h * S_w + b_w) * C + c) * H + (int64_t)m * k_h + a_h) * W + (int64_t)n * k_w + a_w];
+}
+
+template <typename E>
+__global__ __launch_bounds__(kThreads) void defrag_planar_kernel(const E* __restrict__ in, int k_h, int k_w, int S_h,
+                                                                int S_w, int C, int H, int W, E* __restrict__ out) {
+    const int Y = H * k_h, X = W * k_w;
+    const int64_t total = (int64_t)S_h * S_w * C * Y * X;
+    const int64_t p = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (p >= total) return;
+    const int x = (int)(p % X);
+    int64_t t = p / X;
+    const int y = (int)(t % Y);
+    t /= Y;
+    const int c = (int)(t % C);
+    const int s = (int)(t / C);
+    const int b_h = s / S_w, b_w = s % S_w;
+    const int fo = ((y % k_h) * S_h + b_h) * (k_w * S_w) + (x % k_w) * S_w + b_w;
+    out[p] = in[(((int64_t)fo * C + c) * H + y / k_h) * W + x / k_w];
+}
+
+hipError_t launch_frag_planar(int elem_bytes, bool inverse, const void* in, int k_h, int k_w, int S_h, int S_w, int C,
+                              int H, int W, void* out, hipStream_t s) {
+    const int64_t total = inverse ? (int64_t)S_h * S_w * C * H * k_h * W * k_w
+                                  : (int64_t)k_h * S_h * k_w * S_w * C * (H / k_h) * (W / k_w);
+    if (total == 0) return hipSuccess;
+    const dim3 grid((unsigned)ceil_div64(total, kThreads));
+    if (elem_bytes == 2) {
+        if (inverse)
+            defrag_planar_kernel<uint16_t><<<grid, kThreads, 0, s>>>((const uint16_t*)in, k_h, k_w, S_h, S_w, C, H, W, (uint16_t*)out);
+        else
+            frag_planar_kernel<uint16_t><<<grid, kThreads, 0, s>>>((const uint16_t*)in, k_h, k_w, S_h, S_w, C, H, W, (uint16_t*)out);
+    } else {
+        if (inverse)
+            defrag_planar_kernel<uint32_t><<<grid, kThreads, 0, s>>>((const uint32_t*)in, k_h, k_w, S_h, S_w, C, H, W, (uint32_t*)out);
+        else
+            frag_planar_kernel<uint32_t><<<grid, kThreads, 0, s>>>((const uint32_t*)in, k_h, k_w, S_h, S_w, C, H, W, (uint32_t*)out);
+    }
+    return hipGetLastError();
+}
+
+}  // namespace dss

@@ -1,0 +1,277 @@
+"""Python binding of libdss.so (include/dss.h): argument marshalling only.
+
+Every step of the dense evaluation runs in the library's HIP kernels; torch is
+used here for device memory (tensors whose data pointers are handed to the C
+ABI) and for the current HIP stream.  There is no fallback: if libdss.so is
+missing or a call fails, a `DssError` is raised.
+
+Layers are the dicts produced by `workloads`:
+  {"kind": "conv", "cin", "cout", "fh", "fw", "act", "weight": [cout][cin][fh][fw], "bias": [cout]}
+  {"kind": "maxpool", "kh", "kw"}
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libdss.so")
+
+DSS_F32, DSS_BF16 = 0, 1
+DTYPES = {"f32": DSS_F32, "bf16": DSS_BF16}
+ACTS = {"none": 0, "relu": 1, "tanh": 2}
+
+
+class DssError(RuntimeError):
+    def __init__(self, status, what, detail):
+        super().__init__("%s failed with status %d (%s): %s" % (what, status, _STATUS.get(status, "?"), detail))
+        self.status = status
+
+
+_STATUS = {0: "ok", 1: "invalid", 2: "shape", 3: "unsupported", 4: "nomem", 5: "hip"}
+
+
+class Layer(ctypes.Structure):
+    _fields_ = [("kind", ctypes.c_int32), ("cin", ctypes.c_int32), ("cout", ctypes.c_int32),
+                ("fh", ctypes.c_int32), ("fw", ctypes.c_int32), ("act", ctypes.c_int32),
+                ("kh", ctypes.c_int32), ("kw", ctypes.c_int32),
+                ("weight", ctypes.POINTER(ctypes.c_float)), ("bias", ctypes.POINTER(ctypes.c_float))]
+
+
+class Geometry(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in
+                ("ndim", "in_c", "out_c", "n_chain", "B_h", "B_w", "K_h", "K_w", "r_h", "r_w",
+                 "D_h", "D_w", "out_h", "out_w", "dtype", "reserved")] + \
+               [("workspace_bytes", ctypes.c_int64), ("conv_flops", ctypes.c_double),
+                ("pool_bytes", ctypes.c_double), ("total_bytes", ctypes.c_double)]
+
+    def as_dict(self):
+        return {n: getattr(self, n) for n, _ in self._fields_ if n != "reserved"}
+
+
+class LayerGeometry(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in
+                ("c_h", "c_w", "k_h", "k_w", "kstar_h", "kstar_w", "u_h", "u_w", "U_h", "U_w", "F",
+                 "channels", "has_conv", "has_pool")]
+
+    def as_dict(self):
+        return {n: getattr(self, n) for n, _ in self._fields_}
+
+
+class LaunchRecord(ctypes.Structure):
+    _fields_ = [("kernel", ctypes.c_char_p), ("chain_layer", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("ms", ctypes.c_double), ("flops", ctypes.c_double), ("bytes", ctypes.c_double)]
+
+
+EXPORTS = ("dss_chain_geometry", "dss_chain_layer_geometry", "dss_plan_create", "dss_plan_destroy",
+           "dss_plan_geometry", "dss_plan_layer_geometry", "dss_eval_dense", "dss_eval_slide", "dss_frag",
+           "dss_defrag", "dss_plan_set_timing", "dss_plan_timings", "dss_status_string", "dss_last_error",
+           "dss_version")
+
+_lib = None
+
+
+def lib():
+    """Load libdss.so; raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise DssError(-1, "loading libdss.so", "%s does not exist; run __graft_entry__.build()" % LIB_PATH)
+        L = ctypes.CDLL(LIB_PATH)
+        P, I32, I64, VP = ctypes.POINTER, ctypes.c_int32, ctypes.c_int64, ctypes.c_void_p
+        L.dss_chain_geometry.argtypes = [P(Layer), I32, I32, I32, I32, I32, I32, P(Geometry)]
+        L.dss_chain_layer_geometry.argtypes = [P(Layer), I32, I32, I32, I32, I32, I32, P(LayerGeometry)]
+        L.dss_plan_create.argtypes = [P(Layer), I32, I32, I32, I32, P(VP)]
+        L.dss_plan_destroy.argtypes = [VP]
+        L.dss_plan_destroy.restype = None
+        L.dss_plan_geometry.argtypes = [VP, I32, I32, P(Geometry)]
+        L.dss_plan_layer_geometry.argtypes = [VP, I32, I32, I32, P(LayerGeometry)]
+        L.dss_eval_dense.argtypes = [VP, VP, I32, I32, VP, VP, I64, VP]
+        L.dss_eval_slide.argtypes = [VP, VP, I32, I32, I32, VP, VP, I64, VP]
+        L.dss_frag.argtypes = [I32, I32, I32, I32, I32, I32, I32, I32, VP, VP, VP]
+        L.dss_defrag.argtypes = [I32, I32, I32, I32, I32, I32, I32, I32, VP, VP, VP]
+        L.dss_plan_set_timing.argtypes = [VP, I32]
+        L.dss_plan_timings.argtypes = [VP, P(LaunchRecord), I32, P(I32)]
+        L.dss_status_string.argtypes = [I32]
+        L.dss_status_string.restype = ctypes.c_char_p
+        L.dss_last_error.argtypes = []
+        L.dss_last_error.restype = ctypes.c_char_p
+        L.dss_version.argtypes = []
+        L.dss_version.restype = ctypes.c_char_p
+        for name in ("dss_chain_geometry", "dss_chain_layer_geometry", "dss_plan_create", "dss_plan_geometry",
+                     "dss_plan_layer_geometry", "dss_eval_dense", "dss_eval_slide", "dss_frag", "dss_defrag",
+                     "dss_plan_set_timing", "dss_plan_timings"):
+            getattr(L, name).restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def _check(status, what):
+    if status != 0:
+        raise DssError(status, what, lib().dss_last_error().decode())
+
+
+class _LayerArray:
+    """ctypes dss_layer array plus the binary32 weight copies it points into."""
+
+    def __init__(self, layers):
+        self.keep = []
+        self.arr = (Layer * max(1, len(layers)))()
+        for t, l in enumerate(layers):
+            if l["kind"] == "conv":
+                w = np.ascontiguousarray(l["weight"], dtype=np.float32)
+                assert w.shape == (l["cout"], l["cin"], l["fh"], l["fw"])
+                b = None if l.get("bias") is None else np.ascontiguousarray(l["bias"], dtype=np.float32)
+                self.keep += [w, b]
+                self.arr[t] = Layer(0, l["cin"], l["cout"], l["fh"], l["fw"], ACTS[l["act"]], 1, 1,
+                                    w.ctypes.data_as(ctypes.POINTER(ctypes.c_float)),
+                                    b.ctypes.data_as(ctypes.POINTER(ctypes.c_float)) if b is not None
+                                    else ctypes.POINTER(ctypes.c_float)())
+            else:
+                self.arr[t] = Layer(1, 0, 0, 1, 1, 0, l["kh"], l["kw"], ctypes.POINTER(ctypes.c_float)(),
+                                    ctypes.POINTER(ctypes.c_float)())
+        self.n = len(layers)
+
+
+def chain_geometry(layers, ndim, in_channels, H, W, dtype="f32"):
+    la = _LayerArray(layers)
+    g = Geometry()
+    _check(lib().dss_chain_geometry(la.arr, la.n, ndim, in_channels, DTYPES[dtype], H, W, ctypes.byref(g)),
+           "dss_chain_geometry")
+    return g.as_dict()
+
+
+def chain_layer_geometry(layers, ndim, in_channels, H, W, j):
+    la = _LayerArray(layers)
+    g = LayerGeometry()
+    _check(lib().dss_chain_layer_geometry(la.arr, la.n, ndim, in_channels, H, W, j, ctypes.byref(g)),
+           "dss_chain_layer_geometry")
+    return g.as_dict()
+
+
+def _stream(stream):
+    import torch
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _ptr(t):
+    return ctypes.c_void_p(t.data_ptr())
+
+
+class Plan:
+    """A dss plan on the current device."""
+
+    def __init__(self, layers, ndim, in_channels, dtype="f32"):
+        self.layers = layers
+        self.ndim = ndim
+        self.in_channels = in_channels
+        self.dtype = dtype
+        la = _LayerArray(layers)
+        h = ctypes.c_void_p()
+        _check(lib().dss_plan_create(la.arr, la.n, ndim, in_channels, DTYPES[dtype], ctypes.byref(h)),
+               "dss_plan_create")
+        self.handle = h
+        self._ws = None
+
+    @classmethod
+    def from_workload(cls, wl):
+        return cls(wl.layers, wl.ndim, wl.x.shape[0], wl.dtype)
+
+    def close(self):
+        if getattr(self, "handle", None):
+            lib().dss_plan_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def geometry(self, H, W):
+        g = Geometry()
+        _check(lib().dss_plan_geometry(self.handle, H, W, ctypes.byref(g)), "dss_plan_geometry")
+        return g.as_dict()
+
+    def layer_geometry(self, H, W, j):
+        g = LayerGeometry()
+        _check(lib().dss_plan_layer_geometry(self.handle, H, W, j, ctypes.byref(g)), "dss_plan_layer_geometry")
+        return g.as_dict()
+
+    def workspace(self, H, W, device=None):
+        """A device workspace (uint8 tensor) large enough for an H x W signal; reused across calls."""
+        import torch
+        need = self.geometry(H, W)["workspace_bytes"]
+        if self._ws is None or self._ws.numel() < need:
+            self._ws = None
+            self._ws = torch.empty(max(need, 256), dtype=torch.uint8, device=device or "cuda")
+        return self._ws
+
+    def _check_signal(self, signal):
+        import torch
+        want = torch.float32 if self.dtype == "f32" else torch.bfloat16
+        if not signal.is_cuda or signal.dtype != want or not signal.is_contiguous() or signal.dim() != 3:
+            raise ValueError("signal must be a contiguous CUDA %s tensor [C][H][W]" % want)
+        if signal.shape[0] != self.in_channels:
+            raise ValueError("signal has %d channels, plan expects %d" % (signal.shape[0], self.in_channels))
+
+    def eval_dense(self, signal, out=None, workspace=None, stream=None):
+        import torch
+        self._check_signal(signal)
+        _, H, W = signal.shape
+        g = self.geometry(H, W)
+        if out is None:
+            out = torch.empty((g["out_c"], g["out_h"], g["out_w"]), dtype=torch.float32, device=signal.device)
+        ws = workspace if workspace is not None else self.workspace(H, W, signal.device)
+        _check(lib().dss_eval_dense(self.handle, _ptr(signal), H, W, _ptr(out), _ptr(ws), ws.numel(),
+                                    _stream(stream)), "dss_eval_dense")
+        return out
+
+    def eval_slide(self, signal, j, out=None, workspace=None, stream=None):
+        import torch
+        self._check_signal(signal)
+        _, H, W = signal.shape
+        lg = self.layer_geometry(H, W, j)
+        if out is None:
+            out = torch.empty((lg["F"], lg["channels"], lg["U_h"], lg["U_w"]), dtype=torch.float32,
+                              device=signal.device)
+        ws = workspace if workspace is not None else self.workspace(H, W, signal.device)
+        _check(lib().dss_eval_slide(self.handle, _ptr(signal), H, W, j, _ptr(out), _ptr(ws), ws.numel(),
+                                    _stream(stream)), "dss_eval_slide")
+        return out
+
+    def set_timing(self, on=True):
+        _check(lib().dss_plan_set_timing(self.handle, 1 if on else 0), "dss_plan_set_timing")
+
+    def timings(self):
+        n = ctypes.c_int32()
+        _check(lib().dss_plan_timings(self.handle, None, 0, ctypes.byref(n)), "dss_plan_timings")
+        recs = (LaunchRecord * max(1, n.value))()
+        _check(lib().dss_plan_timings(self.handle, recs, n.value, ctypes.byref(n)), "dss_plan_timings")
+        return [{"kernel": r.kernel.decode(), "layer": r.chain_layer, "ms": r.ms, "flops": r.flops,
+                 "bytes": r.bytes} for r in recs[: n.value]]
+
+
+def frag(x, k_h, k_w, S_h, S_w, out=None, stream=None):
+    """dss_frag on a CUDA tensor [S_h*S_w][C][H][W] of 4- or 2-byte elements."""
+    import torch
+    S, C, H, W = x.shape
+    dt = DSS_BF16 if x.element_size() == 2 else DSS_F32
+    if out is None:
+        out = torch.empty((k_h * S_h * k_w * S_w, C, H // k_h, W // k_w), dtype=x.dtype, device=x.device)
+    _check(lib().dss_frag(k_h, k_w, S_h, S_w, C, H, W, dt, _ptr(x), _ptr(out), _stream(stream)), "dss_frag")
+    return out
+
+
+def defrag(x, k_h, k_w, S_h, S_w, out=None, stream=None):
+    """dss_defrag on a CUDA tensor [(k_h*S_h)*(k_w*S_w)][C][H][W]."""
+    import torch
+    F, C, H, W = x.shape
+    dt = DSS_BF16 if x.element_size() == 2 else DSS_F32
+    if out is None:
+        out = torch.empty((S_h * S_w, C, H * k_h, W * k_w), dtype=x.dtype, device=x.device)
+    _check(lib().dss_defrag(k_h, k_w, S_h, S_w, C, H, W, dt, _ptr(x), _ptr(out), _stream(stream)), "dss_defrag")
+    return out

@@ -1,0 +1,173 @@
+"""Host-side checks of the C-ABI library (no GPU): it loads, exports every
+function the header declares, and its host-only geometry agrees with the
+oracle's brute-force receptive field and with the paper's closed forms."""
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_1508_06904_amd import dss, workloads as wl
+from tests.test_oracle import chain_layers, lemma_a_u
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def header_functions():
+    src = open(os.path.join(ROOT, "include", "dss.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(dss_[a-z_]+)\s*\(", src)))
+
+
+def test_library_exports_every_declared_function():
+    L = dss.lib()
+    names = header_functions()
+    assert len(names) >= 15
+    for n in names:
+        assert hasattr(L, n), n
+    assert set(names) == set(dss.EXPORTS)
+    assert L.dss_version().decode().count(".") == 2
+
+
+def test_status_strings():
+    L = dss.lib()
+    for s in range(6):
+        assert L.dss_status_string(s)
+
+
+NAMED = {
+    # name: (arch, C, H, W, ndim, B, K, r)
+    "c1": (wl.arch_c1(), 1, 64, 64, 2, (28, 28), (4, 4), (3, 3)),
+    "c2": (wl.arch_c2(), 1, 1, 1 << 20, 1, (1, 120), (1, 8), (0, 7)),
+    "c3": (wl.arch_c3(), 3, 512, 512, 2, (68, 68), (8, 8), (3, 3)),
+    "c4": (wl.arch_c4(), 3, 1080, 1920, 2, (68, 68), (8, 8), (3, 3)),
+    "c5": (wl.arch_c5(), 3, 2160, 3840, 2, (156, 156), (16, 16), (11, 11)),
+}
+
+
+def theorem_r(N, B, K):
+    """Stuffing count of Theorem 'processing chain' (Sect. 4.3)."""
+    return 0 if (N - B + 1) % K == 0 else K - (N - B + 1) % K
+
+
+@pytest.mark.parametrize("name", list(NAMED))
+def test_named_geometry(name):
+    arch, C, H, W, nd, B, K, r = NAMED[name]
+    layers = wl.init_layers(arch, np.random.default_rng(0))
+    g = dss.chain_geometry(layers, nd, C, H, W)
+    assert (g["B_h"], g["B_w"]) == B == tuple(oracle.receptive_field(layers))
+    assert (g["K_h"], g["K_w"]) == K
+    assert (g["r_h"], g["r_w"]) == r == (theorem_r(H, B[0], K[0]), theorem_r(W, B[1], K[1]))
+    assert (g["out_h"], g["out_w"]) == (H - B[0] + 1, W - B[1] + 1)
+    assert (g["D_h"], g["D_w"]) == (H + r[0], W + r[1])
+    assert g["out_c"] == [l for l in layers if l["kind"] == "conv"][-1]["cout"]
+    # per-layer extents against Lemma 'processing chain' (a)-(c)
+    ch = chain_layers(layers)
+    D = (g["D_h"], g["D_w"])
+    for axis, key in ((0, "h"), (1, "w")):
+        u, kstar = lemma_a_u(ch, B[axis], axis)
+        for j in range(len(ch) + 1):
+            lg = dss.chain_layer_geometry(layers, nd, C, H, W, j)
+            assert lg["u_" + key] == u[j]
+            assert lg["kstar_" + key] == kstar[j]
+            s = sum(kstar[mu - 1] * (ch[mu - 1][0][axis] - 1) for mu in range(1, j + 1))
+            assert (D[axis] - kstar[j] + 1 - s) % kstar[j] == 0
+            assert lg["U_" + key] == (D[axis] - kstar[j] + 1 - s) // kstar[j]          # Lemma (b)
+            assert lg["U_" + key] - u[j] + 1 == (D[axis] - B[axis] + 1) // kstar[j]    # Lemma (c)
+    last = dss.chain_layer_geometry(layers, nd, C, H, W, len(ch))
+    assert last["F"] == K[0] * K[1] and last["u_h"] == last["u_w"] == 1
+
+
+def direct_conv_flops(layers, nd, C, H, W):
+    """Convolution flops of the sliding evaluation, counted per layer from the
+    evaluation counts of Sect. 5.1: U^col_{j-1} (U^row_{j-1} - c_j + 1) evaluations
+    of f_j per axis, each Cin * c_h * c_w multiply-adds per output channel."""
+    ch = chain_layers(layers)
+    convs = [l for l in layers if l["kind"] == "conv"]
+    total, ci = 0.0, 0
+    for j, (c, k) in enumerate(ch, start=1):
+        prev = dss.chain_layer_geometry(layers, nd, C, H, W, j - 1)
+        has_conv = dss.chain_layer_geometry(layers, nd, C, H, W, j)["has_conv"]
+        if not has_conv:
+            continue
+        l = convs[ci]
+        ci += 1
+        n_eval = prev["F"] * (prev["U_h"] - c[0] + 1) * (prev["U_w"] - c[1] + 1)
+        total += 2.0 * n_eval * l["cout"] * l["cin"] * c[0] * c[1]
+    return total
+
+
+@pytest.mark.parametrize("name", list(NAMED))
+def test_conv_flop_accounting(name):
+    arch, C, H, W, nd, *_ = NAMED[name]
+    layers = wl.init_layers(arch, np.random.default_rng(0))
+    g = dss.chain_geometry(layers, nd, C, H, W)
+    assert g["conv_flops"] == pytest.approx(direct_conv_flops(layers, nd, C, H, W), rel=1e-12)
+
+
+def test_hd_frame_flops_and_speedup_shape():
+    """The HD configuration: about 19.8 TFLOP of convolution per frame for the
+    sliding evaluation, against EvalStride's (N-B+1)^2 * per-window cost."""
+    layers = wl.init_layers(wl.arch_c4(), np.random.default_rng(0))
+    g = dss.chain_geometry(layers, 2, 3, 1080, 1920)
+    assert 19.7e12 < g["conv_flops"] < 20.0e12
+    assert g["workspace_bytes"] > 0 and g["workspace_bytes"] % 256 == 0
+
+
+def test_every_stuffing_amount():
+    """Signal extents B .. B+K cover every stuffing amount r in [0, K-1]."""
+    layers = wl.init_layers([("conv", 1, 2, 3, 3, "relu"), ("pool", 2, 2), ("conv", 2, 2, 2, 2, "relu"),
+                             ("pool", 3, 3), ("conv", 2, 1, 2, 2, "none")], np.random.default_rng(0))
+    B = oracle.receptive_field(layers)
+    seen = set()
+    for n in range(B[0], B[0] + 7):
+        g = dss.chain_geometry(layers, 2, 1, n, n + 1)
+        assert g["r_h"] == theorem_r(n, B[0], 6)
+        assert (g["D_h"] - g["B_h"] + 1) % g["K_h"] == 0
+        seen.add(g["r_h"])
+    assert seen == set(range(6))
+
+
+def test_paper_sweep_fragment_count():
+    for L in (3, 4, 12, 15):
+        layers = wl.init_layers(wl.arch_paper_sweep(L, maps=4), np.random.default_rng(0))
+        B = oracle.receptive_field(layers)
+        g = dss.chain_geometry(layers, 2, 1, 240, 320)
+        assert (g["B_h"], g["B_w"]) == B
+        if L == 12:
+            assert g["K_h"] * g["K_w"] == 64
+
+
+@pytest.mark.parametrize("bad", ["cin_mismatch", "zero_filter", "empty", "ndim", "1d_fh", "small_signal", "act"])
+def test_validation_errors(bad):
+    layers = wl.init_layers(wl.arch_c1(), np.random.default_rng(0))
+    nd, C, H, W = 2, 1, 64, 64
+    want = 1
+    if bad == "cin_mismatch":
+        layers[2]["cin"] = 5
+        layers[2]["weight"] = np.zeros((8, 5, 5, 5), np.float32)
+    elif bad == "zero_filter":
+        layers[0]["fh"] = 0
+        layers[0]["weight"] = np.zeros((4, 1, 0, 5), np.float32)
+    elif bad == "empty":
+        layers = []
+    elif bad == "ndim":
+        nd, want = 3, 3
+    elif bad == "1d_fh":
+        nd = 1
+    elif bad == "small_signal":
+        H, want = 27, 2
+    elif bad == "act":
+        layers[0]["act"] = "none"
+        dss_layers = layers
+    with pytest.raises(dss.DssError) as e:
+        if bad == "act":
+            la = dss._LayerArray(layers)
+            la.arr[0].act = 7
+            g = dss.Geometry()
+            dss._check(dss.lib().dss_chain_geometry(la.arr, la.n, nd, C, 0, H, W, dss.ctypes.byref(g)), "geom")
+        else:
+            dss.chain_geometry(layers, nd, C, H, W)
+    assert e.value.status == want
+    assert dss.lib().dss_last_error().decode() != ""

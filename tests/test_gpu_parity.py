@@ -1,0 +1,327 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle on the
+same seeded inputs.  Bit-exact for permutations and integer-valued data;
+binary32 within 1e-4 * max|oracle|, bfloat16 within 2e-2 * max|oracle|."""
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+from oracle import fragment as fr
+from paper_1508_06904_amd import dss, workloads as wl
+from tests.gpu_helpers import (assert_close, gpu_dense, kstar, log, oracle_layers, oracle_windows, sampled_windows,
+                               to_device)
+from tests.test_oracle import HAND, _layers_from_json, chain_layers
+
+pytestmark = pytest.mark.gpu
+
+F32_TOL = 1e-4
+BF16_TOL = 2e-2
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    dss.lib()
+    yield
+    torch.cuda.synchronize()
+
+
+@pytest.fixture
+def direct_conv(monkeypatch):
+    """Plans created inside the test use the VALU convolution for every layer."""
+    monkeypatch.setenv("DSS_CONV_KERNEL", "direct")
+
+
+def chain_ends(layers):
+    """Number of layer descriptors consumed after each processing-chain layer."""
+    ends, t = [], 0
+    while t < len(layers):
+        t += 1
+        if layers[t - 1]["kind"] == "conv" and t < len(layers) and layers[t]["kind"] == "maxpool":
+            t += 1
+        ends.append(t)
+    return ends
+
+
+# ----------------------------------------------------------------------------- Frag / Defrag
+
+
+@pytest.mark.parametrize("kh,kw,Sh,Sw,C,H,W", [(2, 2, 1, 1, 3, 8, 10), (2, 3, 2, 1, 5, 6, 9), (1, 2, 1, 4, 1, 1, 16),
+                                               (3, 2, 2, 2, 2, 9, 4), (4, 4, 2, 2, 7, 12, 20), (2, 2, 4, 4, 64, 34, 66)])
+@pytest.mark.parametrize("elem", [4, 2])
+def test_frag_defrag_bit_exact(kh, kw, Sh, Sw, C, H, W, elem):
+    import torch
+    log("frag/defrag k=%dx%d S=%dx%d C=%d H=%d W=%d elem=%d" % (kh, kw, Sh, Sw, C, H, W, elem))
+    rng = np.random.default_rng(kh * 7 + kw + Sh + C)
+    npdt, tdt = (np.int32, torch.int32) if elem == 4 else (np.int16, torch.int16)
+    info = np.iinfo(npdt)
+    x = rng.integers(info.min, info.max, size=(Sh * Sw, C, H, W), dtype=npdt)
+    xd = torch.from_numpy(x).cuda()
+    y = dss.frag(xd, kh, kw, Sh, Sw)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(y.cpu().numpy(), fr.frag_tensor(x, kh, kw, Sh, Sw))
+    z = dss.defrag(y, kh, kw, Sh, Sw)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(z.cpu().numpy(), x)
+    np.testing.assert_array_equal(z.cpu().numpy(), fr.defrag_tensor(fr.frag_tensor(x, kh, kw, Sh, Sw), kh, kw, Sh, Sw))
+
+
+def test_frag_rejects_bad_shape():
+    import torch
+    x = torch.zeros((1, 1, 5, 4), dtype=torch.float32, device="cuda")
+    with pytest.raises(dss.DssError) as e:
+        dss.frag(x, 2, 2, 1, 1)
+    assert e.value.status == 2
+
+
+# ----------------------------------------------------------------------------- hand-derived cases
+
+
+@pytest.mark.parametrize("case", HAND, ids=[c["name"] for c in HAND])
+def test_hand_chain_gpu(case):
+    layers = _layers_from_json(case["layers"])
+    x = np.array(case["x"], dtype=np.float32)
+    nd = 1 if x.shape[1] == 1 and all(l.get("fh", 1) == 1 and l.get("kh", 1) == 1 for l in layers) else 2
+    out, plan = gpu_dense(layers, x, nd)
+    g = plan.geometry(x.shape[1], x.shape[2])
+    assert [g["B_h"], g["B_w"]] == case["B"] and [g["K_h"], g["K_w"]] == case["K"]
+    assert [g["r_h"], g["r_w"]] == case["r"]
+    np.testing.assert_array_equal(out, np.array(case["expected"], dtype=np.float64))
+
+
+# ----------------------------------------------------------------------------- exact integer arithmetic
+
+EXACT_ARCH = [("conv", 16, 32, 3, 3, "relu"), ("pool", 2, 2), ("conv", 32, 48, 3, 2, "relu"), ("pool", 2, 2),
+              ("conv", 48, 136, 2, 3, "relu"), ("conv", 136, 3, 1, 1, "none")]
+
+
+@pytest.mark.parametrize("kernel", ["mfma", "direct"])
+def test_exact_integer_chain_bit_identical(kernel, monkeypatch):
+    """Integer inputs, weights in {-1,0,1}, integer biases: every partial sum is an
+    exactly representable integer, so any summation order must reproduce the
+    oracle bit for bit.  Pins Stuff, Frag, Defrag, Trim and the output placement."""
+    if kernel == "direct":
+        monkeypatch.setenv("DSS_CONV_KERNEL", "direct")
+    w = wl.custom(EXACT_ARCH, 16, 41, 47, seed=3, weight_kind="int", value_kind="int")
+    log("exact chain %s on %s" % (kernel, w.x.shape))
+    out, plan = gpu_dense(w.layers, w.x, 2)
+    ref = oracle.eval_stride(w.layers, w.x)
+    assert np.abs(ref).max() < 2 ** 23
+    np.testing.assert_array_equal(out, ref)
+
+
+def test_exact_integer_bf16_conv_bit_identical():
+    """bfloat16 MFMA path on integer data: one conv layer whose binary32 output is exact."""
+    arch = [("conv", 32, 48, 3, 3, "none")]
+    w = wl.custom(arch, 32, 19, 70, seed=5, weight_kind="int", value_kind="int", dtype="bf16")
+    out, _ = gpu_dense(w.layers, w.x, 2, "bf16")
+    ref = oracle.eval_stride(w.layers, w.x)
+    np.testing.assert_array_equal(out, ref)
+
+
+# ----------------------------------------------------------------------------- random chains
+
+CHAINS = {
+    "2d_small_direct": ([("conv", 3, 5, 3, 2, "relu"), ("pool", 2, 1), ("conv", 5, 6, 2, 3, "tanh"), ("pool", 1, 2),
+                         ("conv", 6, 2, 2, 2, "none")], 3, 2),
+    "2d_mfma_mixed": ([("conv", 3, 16, 5, 5, "relu"), ("pool", 2, 2), ("conv", 16, 40, 3, 3, "relu"), ("pool", 2, 2),
+                       ("conv", 40, 72, 3, 3, "tanh"), ("pool", 2, 2), ("conv", 72, 130, 4, 4, "relu"),
+                       ("conv", 130, 2, 1, 1, "none")], 3, 2),
+    "2d_pool_first": ([("pool", 2, 2), ("conv", 2, 20, 2, 2, "relu"), ("pool", 3, 3), ("conv", 20, 32, 2, 2, "relu"),
+                       ("conv", 32, 1, 1, 1, "none")], 2, 2),
+    "2d_pool_pool": ([("conv", 4, 24, 3, 3, "relu"), ("pool", 2, 2), ("pool", 2, 2), ("conv", 24, 20, 3, 3, "relu"),
+                      ("conv", 20, 4, 1, 1, "none")], 4, 2),
+    "1d_c2_like": ([("conv", 1, 16, 1, 9, "relu"), ("pool", 1, 2), ("conv", 16, 32, 1, 9, "relu"), ("pool", 1, 2),
+                    ("conv", 32, 64, 1, 9, "relu"), ("pool", 1, 2), ("conv", 64, 2, 1, 8, "none")], 1, 1),
+    "2d_ragged_cin": ([("conv", 20, 36, 3, 3, "relu"), ("pool", 2, 2), ("conv", 36, 20, 2, 2, "none")], 20, 2),
+}
+
+
+@pytest.mark.parametrize("name", list(CHAINS))
+def test_random_chain_f32(name):
+    arch, C, nd = CHAINS[name]
+    w0 = wl.custom(arch, C, 1, 1, seed=1)
+    B = oracle.receptive_field(w0.layers)
+    K = kstar(arch)
+    H = 1 if nd == 1 else B[0] + 3 * K[0] + 1
+    W = B[1] + 5 * K[1] + 3 if nd == 1 else B[1] + 4 * K[1] + 2
+    if nd == 1:
+        W = B[1] + 300
+    w = wl.custom(arch, C, H, W, seed=2, value_kind="normal")
+    log("chain %s on %s, B=%s" % (name, w.x.shape, B))
+    out, _ = gpu_dense(w.layers, w.x, nd)
+    ref = oracle.eval_stride(w.layers, w.x)
+    assert_close(out, ref, F32_TOL, name)
+
+
+@pytest.mark.parametrize("name", ["2d_mfma_mixed", "2d_pool_pool", "2d_ragged_cin"])
+def test_random_chain_bf16(name):
+    arch, C, nd = CHAINS[name]
+    w0 = wl.custom(arch, C, 1, 1, seed=1)
+    B = oracle.receptive_field(w0.layers)
+    K = kstar(arch)
+    w = wl.custom(arch, C, B[0] + 2 * K[0] + 1, B[1] + 3 * K[1] + 2, seed=4, dtype="bf16")
+    log("bf16 chain %s on %s" % (name, w.x.shape))
+    out, _ = gpu_dense(w.layers, w.x, nd, "bf16")
+    ref = oracle.eval_stride(oracle_layers(w.layers, "bf16"), w.x)
+    assert_close(out, ref, BF16_TOL, name)
+
+
+def test_direct_and_mfma_agree(direct_conv):
+    """Both convolution kernels on the same chain agree to rounding."""
+    arch, C, nd = CHAINS["2d_mfma_mixed"]
+    w = wl.custom(arch, C, 60, 57, seed=7)
+    d, _ = gpu_dense(w.layers, w.x, nd)
+    os.environ.pop("DSS_CONV_KERNEL")
+    m, _ = gpu_dense(w.layers, w.x, nd)
+    assert_close(m, d, 1e-5, "mfma vs direct")
+
+
+# ----------------------------------------------------------------------------- geometry edge cases
+
+
+def test_every_stuffing_amount_gpu():
+    arch = [("conv", 2, 16, 3, 3, "relu"), ("pool", 2, 2), ("conv", 16, 16, 2, 2, "relu"), ("pool", 3, 3),
+            ("conv", 16, 2, 2, 2, "none")]
+    w0 = wl.custom(arch, 2, 1, 1, seed=0)
+    B = oracle.receptive_field(w0.layers)
+    plan = dss.Plan(w0.layers, 2, 2)
+    seen = set()
+    for n in range(B[0], B[0] + 7):
+        w = wl.custom(arch, 2, n, B[1] + 6 - (n - B[0]), seed=n)
+        w.layers = w0.layers
+        out, _ = gpu_dense(w.layers, w.x, 2, plan=plan)
+        ref = oracle.eval_stride(w.layers, w.x)
+        assert_close(out, ref, F32_TOL, "n=%d" % n)
+        seen.add(plan.geometry(n, w.x.shape[2])["r_h"])
+    assert seen == set(range(6))
+
+
+def test_signal_equal_to_receptive_field():
+    w = wl.make("c1_64x64", H=28, W=28)
+    out, _ = gpu_dense(w.layers, w.x, 2)
+    assert out.shape == (1, 1, 1)
+    assert_close(out, oracle.eval_stride(w.layers, w.x), F32_TOL)
+
+
+def test_eval_slide_lemma_d():
+    """Per-layer check of Lemma 'processing chain' (d): the strided network's
+    layer-j output on window (i, w) sits in fragment (i mod k*_h) k*_w + (w mod k*_w)
+    of the sliding evaluation, at offset (i div k*_h, w div k*_w)."""
+    import torch
+    arch = [("conv", 3, 16, 3, 3, "relu"), ("pool", 2, 2), ("conv", 16, 24, 2, 3, "relu"), ("pool", 2, 3),
+            ("conv", 24, 20, 3, 2, "relu"), ("conv", 20, 2, 1, 1, "none")]
+    w = wl.custom(arch, 3, 40, 45, seed=9)
+    plan = dss.Plan(w.layers, 2, 3)
+    B = plan.geometry(40, 45)
+    ch = chain_layers(w.layers)
+    xd = to_device(w.x, "f32")
+    ends = chain_ends(w.layers)
+    rng = np.random.default_rng(0)
+    for j in range(1, len(ch) + 1):
+        lg = plan.layer_geometry(40, 45, j)
+        slide = plan.eval_slide(xd, j)
+        torch.cuda.synchronize()
+        slide = slide.cpu().numpy().astype(np.float64)
+        wi = rng.integers(0, B["out_h"], size=12)
+        wj = rng.integers(0, B["out_w"], size=12)
+        ref = oracle.eval_stride(w.layers, w.x, windows=(wi, wj), upto=ends[j - 1])
+        C, uh, uw = lg["channels"], lg["u_h"], lg["u_w"]
+        ref = ref.reshape(len(wi), C, uh, uw)
+        for q in range(len(wi)):
+            f = (wi[q] % lg["kstar_h"]) * lg["kstar_w"] + (wj[q] % lg["kstar_w"])
+            y0, x0 = wi[q] // lg["kstar_h"], wj[q] // lg["kstar_w"]
+            got = slide[f, :, y0:y0 + uh, x0:x0 + uw]
+            assert_close(got, ref[q], F32_TOL, "layer %d window (%d,%d)" % (j, wi[q], wj[q]))
+
+
+def test_translation_equivariance_gpu():
+    arch, C, nd = CHAINS["2d_mfma_mixed"]
+    w = wl.custom(arch, C, 90, 85, seed=12)
+    full, plan = gpu_dense(w.layers, w.x, 2)
+    g = plan.geometry(90, 85)
+    a, b, h, ww = 5, 3, g["B_h"] + 9, g["B_w"] + 11
+    crop, _ = gpu_dense(w.layers, np.ascontiguousarray(w.x[:, a:a + h, b:b + ww]), 2, plan=plan)
+    assert_close(crop, full[:, a:a + h - g["B_h"] + 1, b:b + ww - g["B_w"] + 1], 1e-6, "crop")
+
+
+# ----------------------------------------------------------------------------- named workloads
+
+
+def test_c1_full_dense():
+    w = wl.make("c1_64x64")
+    out, plan = gpu_dense(w.layers, w.x, 2)
+    assert out.shape == (1, 37, 37)
+    assert_close(out, oracle.eval_stride(w.layers, w.x), F32_TOL, "c1")
+
+
+@pytest.mark.parametrize("name,H,W,widths", [("c2_1d_1m", 1, 20000, None), ("c3_512", 100, 118, (16, 32, 48, 64)),
+                                             ("c4_hd", 90, 97, (16, 32, 64, 128)),
+                                             ("c5_4k", 170, 181, (16, 16, 32, 32))])
+def test_named_reduced_full_oracle(name, H, W, widths):
+    """The named layer patterns at reduced extents and widths, every window checked."""
+    w = wl.make(name, H=H, W=W, widths=widths)
+    log("%s reduced %s widths=%s" % (name, w.x.shape, widths))
+    out, _ = gpu_dense(w.layers, w.x, w.ndim, w.dtype)
+    ref = oracle.eval_stride(oracle_layers(w.layers, w.dtype), w.x)
+    assert_close(out, ref, BF16_TOL if w.dtype == "bf16" else F32_TOL, name)
+
+
+@pytest.mark.parametrize("name,max_phases", [("c2_1d_1m", None), ("c3_512", None), ("c4_hd", None), ("c5_4k", 64)])
+def test_named_full_size_sampled(name, max_phases):
+    """Full-size workloads in the benchmark's launch configuration; the oracle
+    checks a seeded sample covering the corners, edge midpoints and fragment phases."""
+    w = wl.make(name)
+    log("%s full size %s" % (name, w.x.shape))
+    out, plan = gpu_dense(w.layers, w.x, w.ndim, w.dtype)
+    g = plan.geometry(w.x.shape[1], w.x.shape[2])
+    assert out.shape == (g["out_c"], g["out_h"], g["out_w"])
+    assert np.all(np.isfinite(out))
+    i, j = sampled_windows(g["out_h"], g["out_w"], g["K_h"], g["K_w"], per_phase=1, max_phases=max_phases)
+    log("  checking %d windows" % len(i))
+    ref = oracle_windows(oracle_layers(w.layers, w.dtype), w.x, i, j)
+    assert_close(out[:, i, j].T, ref, BF16_TOL if w.dtype == "bf16" else F32_TOL, name)
+
+
+# ----------------------------------------------------------------------------- robustness
+
+
+def test_errors_leave_output_untouched():
+    import torch
+    w = wl.make("c1_64x64")
+    plan = dss.Plan.from_workload(w)
+    out = torch.full((1, 37, 37), 123.0, device="cuda")
+    small = to_device(w.x[:, :27, :], "f32")
+    with pytest.raises(dss.DssError) as e:
+        plan.eval_dense(small, out=torch.empty((1, 1, 1), device="cuda"))
+    assert e.value.status == 2
+    ws = torch.empty(16 * 1024, dtype=torch.uint8, device="cuda")
+    with pytest.raises(dss.DssError) as e:
+        plan.eval_dense(to_device(w.x, "f32"), out=out, workspace=ws)
+    assert e.value.status == 2
+    torch.cuda.synchronize()
+    assert torch.all(out == 123.0)
+
+
+def test_run_twice_bit_identical():
+    arch, C, nd = CHAINS["2d_mfma_mixed"]
+    w = wl.custom(arch, C, 70, 66, seed=13)
+    a, plan = gpu_dense(w.layers, w.x, nd)
+    b, _ = gpu_dense(w.layers, w.x, nd, plan=plan)
+    np.testing.assert_array_equal(a, b)
+
+
+def test_timing_records():
+    w = wl.make("c3_512", H=120, W=130, widths=(16, 32, 64, 128))
+    plan = dss.Plan.from_workload(w)
+    plan.set_timing(True)
+    gpu_dense(w.layers, w.x, 2, plan=plan)
+    recs = plan.timings()
+    names = [r["kernel"] for r in recs]
+    assert names[0] == "stuff_pack" and names[-1] == "defrag_trim"
+    assert "conv_mfma_f32" in names and "pool_frag" in names
+    g = plan.geometry(120, 130)
+    assert sum(r["flops"] for r in recs) == pytest.approx(g["conv_flops"], rel=1e-9)
+    assert all(r["ms"] >= 0 for r in recs)
