@@ -68,7 +68,11 @@ def main():
     ap.add_argument("--config", default="c4_hd", choices=sorted(WORKLOAD_TEXT))
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target length of the oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="only run plain 1 GiB device-to-device copies (scales the HBM byte counters of a profiler)")
     args = ap.parse_args()
+    if args.calibrate_copy:
+        return calibrate_copy()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -162,6 +166,20 @@ def main():
     if not args.no_cpu_baseline:
         record["cpu_baseline"], record["parity_spot_check"] = cpu_baseline(w, g, out, args.cpu_seconds)
     print(json.dumps(record), flush=True)
+
+
+def calibrate_copy(n=4, nbytes=1 << 30):
+    """n plain copies of an nbytes buffer: a kernel whose true HBM traffic is known
+    (nbytes read + nbytes written per launch)."""
+    import torch
+    src = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(n):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"calibration": "device copy", "bytes_read_per_launch": nbytes,
+                      "bytes_written_per_launch": nbytes, "launches": n}), flush=True)
 
 
 def cpu_baseline(w, g, out, target_s):

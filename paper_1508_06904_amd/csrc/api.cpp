@@ -52,16 +52,20 @@ uint16_t host_f32_to_bf16(float f) {
 }
 
 // Kernel choice per convolution.  The MFMA implicit GEMM wants a contraction
-// deep enough to fill its K loop and enough output channels to fill an N tile;
-// the first layers (few input channels) and the final projections (few output
-// channels) go to the direct VALU kernel.
+// deep enough to fill its K loop (at least 16 input channels, channel rows of
+// whole 16-byte units); the first layers with few input channels go to the
+// direct VALU kernel.  Narrow outputs (the final projections) still use MFMA
+// with the 32-channel N tile: the padded output channels cost MFMA cycles the
+// layer has to spare, while the direct kernel would be limited by its
+// uncoalesced reads of the wide input rows.
 static ConvImpl choose_impl(const ChainLayer& c, dss_dtype dt) {
     // Tuning / cross-check override: DSS_CONV_KERNEL=direct selects the VALU
     // kernel for every convolution of plans created afterwards.
     const char* force = getenv("DSS_CONV_KERNEL");
     if (force && std::strcmp(force, "direct") == 0) return CONV_DIRECT;
-    if (dt == DSS_F32 && c.cin % 4 == 0 && c.cin >= 16 && c.cout >= 16) return CONV_MFMA_F32;
-    if (dt == DSS_BF16 && c.cin % 8 == 0 && c.cin >= 16 && c.cout >= 16) return CONV_MFMA_BF16;
+    if (c.cin < 16) return CONV_DIRECT;
+    if (dt == DSS_F32 && c.cin % 4 == 0 && mfma_supports(false, c.cout, c.c_h, c.c_w)) return CONV_MFMA_F32;
+    if (dt == DSS_BF16 && c.cin % 8 == 0 && mfma_supports(true, c.cout, c.c_h, c.c_w)) return CONV_MFMA_BF16;
     return CONV_DIRECT;
 }
 
@@ -364,11 +368,19 @@ struct Timer {
     }
 };
 
+// Telemetry name of a convolution launch: one name per kernel instantiation, so
+// that per-name averages match a profiler's per-symbol statistics.
 const char* conv_name(const PlanConv& pc, dss_dtype tout) {
     switch (pc.impl) {
-        case CONV_MFMA_F32: return "conv_mfma_f32";
-        case CONV_MFMA_BF16: return tout == DSS_F32 ? "conv_mfma_bf16_f32out" : "conv_mfma_bf16";
-        default: return "conv_direct";
+        case CONV_MFMA_F32:
+            return pc.bn == 128 ? "conv_mfma_f32_n128" : pc.bn == 64 ? "conv_mfma_f32_n64" : "conv_mfma_f32_n32";
+        case CONV_MFMA_BF16:
+            if (tout == DSS_F32)
+                return pc.bn == 128 ? "conv_mfma_bf16_n128_f32out" : pc.bn == 64 ? "conv_mfma_bf16_n64_f32out"
+                                                                   : "conv_mfma_bf16_n32_f32out";
+            return pc.bn == 128 ? "conv_mfma_bf16_n128" : pc.bn == 64 ? "conv_mfma_bf16_n64" : "conv_mfma_bf16_n32";
+        default:
+            return "conv_direct";
     }
 }
 

@@ -33,6 +33,7 @@ namespace dss {
 
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));   // one 16-byte unit
 
 constexpr int kPitchBytes = 80;     // LDS bytes per staged sample / weight row
 constexpr int kChunkBytes = 64;     // bytes of one channel chunk per sample
@@ -46,13 +47,12 @@ struct MfmaCfg {
     static constexpr int BN = 32 * NT * WGN;            // output channels per workgroup
     static constexpr int THREADS = 64 * WGM * WGN;
     static constexpr int WSLICE_UNITS = BN * (kChunkBytes / 16);  // 16-byte units per weight slice
+    static constexpr int WPER = (WSLICE_UNITS + THREADS - 1) / THREADS;
+    // 16-byte halo units each thread stages per chunk (bounds the halo extent)
+    static constexpr int HU = BM <= 128 ? 6 : 10;
 };
 
-__device__ __forceinline__ floatx16 mfma_step_f32(const float* a, const float* b, int s, floatx16 acc) {
-    return __builtin_amdgcn_mfma_f32_32x32x2f32(a[s], b[s], acc, 0, 0, 0);
-}
-
-__device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8, v); }
+__device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
 
 template <bool BF16, typename Tout, int WGM, int WGN, int NT>
 __global__ __launch_bounds__(256) void conv_mfma_kernel(
@@ -64,6 +64,10 @@ __global__ __launch_bounds__(256) void conv_mfma_kernel(
     Tout* __restrict__ out,            // [F][Hout][Wout][Cout]
     int Hout, int Wout, int TH, int TW, int tilesY, int tilesX) {
     using Cfg = MfmaCfg<BF16, WGM, WGN, NT>;
+    constexpr int THREADS = Cfg::THREADS;
+    constexpr int HU = Cfg::HU;
+    constexpr int WPER = Cfg::WPER;
+    constexpr int WU = Cfg::WSLICE_UNITS;
     extern __shared__ __attribute__((aligned(16))) char lds[];
 
     const int tid = threadIdx.x;
@@ -82,8 +86,8 @@ __global__ __launch_bounds__(256) void conv_mfma_kernel(
     const int tx0 = (trem % tilesX) * TW;
     const int nb = blockIdx.y;
 
-    const int HH = TH + fh - 1, HW = TW + fw - 1;   // halo extents
-    const int halo_px = HH * HW;
+    const int HW = TW + fw - 1;          // halo width
+    const int halo_px = (TH + fh - 1) * HW;
     char* halo = lds;
     char* wbuf0 = lds + ((halo_px * kPitchBytes + 127) / 128) * 128;
     char* wbuf1 = wbuf0 + Cfg::BN * kPitchBytes;
@@ -99,6 +103,26 @@ __global__ __launch_bounds__(256) void conv_mfma_kernel(
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) b_off[nt] = (wn * 32 * NT + nt * 32 + l32) * kPitchBytes + half * 32;
 
+    // per-thread halo units.  Unit u = tid + r*THREADS is 16-byte quad q = u & 3 (the
+    // same for every r) of halo sample u >> 2.  Sources are 32-bit byte offsets from
+    // the tile's top-left input sample (-1 outside the fragment); only the chunk
+    // offset changes between chunks.
+    const size_t row_bytes = (size_t)Cin * Cfg::ES;
+    const char* in_tile = in + (((size_t)f * Hin + ty0) * Win + tx0) * row_bytes;
+    const int hq = tid & 3;
+    const int h_c0 = hq * (16 / Cfg::ES);          // first channel of this thread's quad
+    const int h_px0 = tid >> 2;
+    constexpr int PX_STEP = THREADS / 4;
+    int h_src[HU];
+#pragma unroll
+    for (int r = 0; r < HU; ++r) {
+        const int px = h_px0 + r * PX_STEP;
+        const int dy = px / HW, dx = px % HW;
+        h_src[r] = (px < halo_px && ty0 + dy < Hin && tx0 + dx < Win) ? (dy * Win + dx) * (int)row_bytes + hq * 16 : -1;
+    }
+    u32x4 hreg[HU];
+    u32x4 wreg[WPER];
+
     floatx16 acc[2][NT];
 #pragma unroll
     for (int mt = 0; mt < 2; ++mt)
@@ -109,111 +133,109 @@ __global__ __launch_bounds__(256) void conv_mfma_kernel(
 
     const int taps = fh * fw;
     const int steps = nchunks * taps;
-    const size_t row_bytes = (size_t)Cin * Cfg::ES;
-    const char* in_f = in + (size_t)f * Hin * Win * row_bytes;
     const char* w_nb = wp + (size_t)nb * steps * (Cfg::BN * kChunkBytes);
 
-    // -- staging helpers
-    auto load_halo = [&](int cc) {
-        const int units = halo_px * 4;
-        for (int u = tid; u < units; u += Cfg::THREADS) {
-            const int px = u >> 2, q = u & 3;
-            const int y = ty0 + px / HW, x = tx0 + px % HW;
-            const int c0 = cc * Cfg::CC + q * (16 / Cfg::ES);
-            uint4 v = make_uint4(0, 0, 0, 0);
-            if (y < Hin && x < Win && c0 < Cin)
-                v = *reinterpret_cast<const uint4*>(in_f + ((size_t)y * Win + x) * row_bytes + (size_t)c0 * Cfg::ES);
-            *reinterpret_cast<uint4*>(halo + px * kPitchBytes + q * 16) = v;
-        }
-    };
-    constexpr int WU = Cfg::WSLICE_UNITS;
-    constexpr int WPER = (WU + Cfg::THREADS - 1) / Cfg::THREADS;
-    uint4 wreg[WPER];
-    auto load_w = [&](int step) {
-        const char* src = w_nb + (size_t)step * (Cfg::BN * kChunkBytes);
-#pragma unroll
-        for (int r = 0; r < WPER; ++r) {
-            const int u = tid + r * Cfg::THREADS;
-            if (WU % Cfg::THREADS == 0 || u < WU) wreg[r] = *reinterpret_cast<const uint4*>(src + (size_t)u * 16);
-        }
-    };
-    auto store_w = [&](char* dst) {
-#pragma unroll
-        for (int r = 0; r < WPER; ++r) {
-            const int u = tid + r * Cfg::THREADS;
-            if (WU % Cfg::THREADS == 0 || u < WU)
-                *reinterpret_cast<uint4*>(dst + (u >> 2) * kPitchBytes + (u & 3) * 16) = wreg[r];
-        }
-    };
+#define DSS_HALO_FETCH(cc)                                                                       \
+    {                                                                                            \
+        const bool chan_ok = (cc) * Cfg::CC + h_c0 < Cin;                                        \
+        const char* src_c = in_tile + (size_t)(cc) * kChunkBytes;                                \
+        _Pragma("unroll") for (int r = 0; r < HU; ++r) {                                         \
+            u32x4 v = {0u, 0u, 0u, 0u};                                                          \
+            if (chan_ok && h_src[r] >= 0) v = *reinterpret_cast<const u32x4*>(src_c + h_src[r]); \
+            hreg[r] = v;                                                                         \
+        }                                                                                        \
+    }
+#define DSS_HALO_STORE()                                                                         \
+    _Pragma("unroll") for (int r = 0; r < HU; ++r) {                                             \
+        if (h_px0 + r * PX_STEP < halo_px)                                                       \
+            *reinterpret_cast<u32x4*>(halo + (h_px0 + r * PX_STEP) * kPitchBytes + hq * 16) = hreg[r]; \
+    }
+#define DSS_W_FETCH(st)                                                                          \
+    _Pragma("unroll") for (int r = 0; r < WPER; ++r) {                                           \
+        const int u = tid + r * THREADS;                                                         \
+        if (WU % THREADS == 0 || u < WU)                                                         \
+            wreg[r] = *reinterpret_cast<const u32x4*>(w_nb + (size_t)(st) * (Cfg::BN * kChunkBytes) + (size_t)u * 16); \
+    }
+#define DSS_W_STORE(dst)                                                                         \
+    _Pragma("unroll") for (int r = 0; r < WPER; ++r) {                                           \
+        const int u = tid + r * THREADS;                                                         \
+        if (WU % THREADS == 0 || u < WU)                                                         \
+            *reinterpret_cast<u32x4*>((dst) + (u >> 2) * kPitchBytes + (u & 3) * 16) = wreg[r];  \
+    }
 
-    // -- prologue
-    load_halo(0);
-    load_w(0);
-    store_w(wbuf0);
+    // -- prologue: chunk 0 halo and the first weight slice
+    DSS_HALO_FETCH(0);
+    DSS_W_FETCH(0);
+    DSS_HALO_STORE();
+    DSS_W_STORE(wbuf0);
     __syncthreads();
 
-    for (int step = 0; step < steps; ++step) {
-        const int next = step + 1;
-        if (next < steps) load_w(next);
-
-        const int tap = step % taps;
-        const int th = tap / fw, tw = tap % fw;
-        const int tap_off = (th * HW + tw) * kPitchBytes;
-        const char* wcur = (step & 1) ? wbuf1 : wbuf0;
-
-        uint4 a[2][2], b[NT][2];
+    int step = 0;
+    for (int cc = 0; cc < nchunks; ++cc) {
+        for (int th = 0; th < fh; ++th) {
+            for (int tw = 0; tw < fw; ++tw, ++step) {
+                const bool has_next = step + 1 < steps;
+                const bool last_tap = (th == fh - 1) && (tw == fw - 1);
+                // prefetch the next weight slice (and the next chunk's halo) into registers;
+                // the loads complete while the MFMAs below run
+                if (has_next) {
+                    DSS_W_FETCH(step + 1);
+                    if (last_tap) {
+                        DSS_HALO_FETCH(cc + 1);
+                    }
+                }
+                const int tap_off = (th * HW + tw) * kPitchBytes;
+                const char* wcur = (step & 1) ? wbuf1 : wbuf0;
+                u32x4 a[2][2], b[NT][2];
 #pragma unroll
-        for (int mt = 0; mt < 2; ++mt) {
-            a[mt][0] = *reinterpret_cast<const uint4*>(halo + a_off[mt] + tap_off);
-            a[mt][1] = *reinterpret_cast<const uint4*>(halo + a_off[mt] + tap_off + 16);
-        }
+                for (int mt = 0; mt < 2; ++mt) {
+                    a[mt][0] = *reinterpret_cast<const u32x4*>(halo + a_off[mt] + tap_off);
+                    a[mt][1] = *reinterpret_cast<const u32x4*>(halo + a_off[mt] + tap_off + 16);
+                }
 #pragma unroll
-        for (int nt = 0; nt < NT; ++nt) {
-            b[nt][0] = *reinterpret_cast<const uint4*>(wcur + b_off[nt]);
-            b[nt][1] = *reinterpret_cast<const uint4*>(wcur + b_off[nt] + 16);
-        }
-        if constexpr (BF16) {
+                for (int nt = 0; nt < NT; ++nt) {
+                    b[nt][0] = *reinterpret_cast<const u32x4*>(wcur + b_off[nt]);
+                    b[nt][1] = *reinterpret_cast<const u32x4*>(wcur + b_off[nt] + 16);
+                }
+                if constexpr (BF16) {
 #pragma unroll
-            for (int s = 0; s < 2; ++s)
+                    for (int s = 0; s < 2; ++s)
 #pragma unroll
-                for (int mt = 0; mt < 2; ++mt)
+                        for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
-                    for (int nt = 0; nt < NT; ++nt)
-                        acc[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a[mt][s]), as_bf16x8(b[nt][s]),
-                                                                              acc[mt][nt], 0, 0, 0);
-        } else {
-            float af[2][8], bf[NT][8];
+                            for (int nt = 0; nt < NT; ++nt)
+                                acc[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                                    as_bf16x8(a[mt][s]), as_bf16x8(b[nt][s]), acc[mt][nt], 0, 0, 0);
+                } else {
 #pragma unroll
-            for (int mt = 0; mt < 2; ++mt) {
-                const uint32_t w8[8] = {a[mt][0].x, a[mt][0].y, a[mt][0].z, a[mt][0].w,
-                                        a[mt][1].x, a[mt][1].y, a[mt][1].z, a[mt][1].w};
+                    for (int s = 0; s < 8; ++s) {
 #pragma unroll
-                for (int s = 0; s < 8; ++s) af[mt][s] = __uint_as_float(w8[s]);
+                        for (int mt = 0; mt < 2; ++mt) {
+                            const uint32_t aw = a[mt][s >> 2][s & 3];
+#pragma unroll
+                            for (int nt = 0; nt < NT; ++nt) {
+                                const uint32_t bw = b[nt][s >> 2][s & 3];
+                                acc[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(aw), __uint_as_float(bw),
+                                                                                  acc[mt][nt], 0, 0, 0);
+                            }
+                        }
+                    }
+                }
+                if (has_next) {
+                    if (last_tap) {
+                        __syncthreads();          // every wave is done with this chunk's halo
+                        DSS_HALO_STORE();
+                    }
+                    DSS_W_STORE((step & 1) ? wbuf0 : wbuf1);
+                }
+                __syncthreads();
             }
-#pragma unroll
-            for (int nt = 0; nt < NT; ++nt) {
-                const uint32_t w8[8] = {b[nt][0].x, b[nt][0].y, b[nt][0].z, b[nt][0].w,
-                                        b[nt][1].x, b[nt][1].y, b[nt][1].z, b[nt][1].w};
-#pragma unroll
-                for (int s = 0; s < 8; ++s) bf[nt][s] = __uint_as_float(w8[s]);
-            }
-#pragma unroll
-            for (int s = 0; s < 8; ++s)
-#pragma unroll
-                for (int mt = 0; mt < 2; ++mt)
-#pragma unroll
-                    for (int nt = 0; nt < NT; ++nt) acc[mt][nt] = mfma_step_f32(af[mt], bf[nt], s, acc[mt][nt]);
         }
-
-        if (next < steps) {
-            store_w((next & 1) ? wbuf1 : wbuf0);
-            if (next % taps == 0) {
-                __syncthreads();          // every wave is done with the current halo
-                load_halo(next / taps);
-            }
-        }
-        __syncthreads();
     }
+#undef DSS_HALO_FETCH
+#undef DSS_HALO_STORE
+#undef DSS_W_FETCH
+#undef DSS_W_STORE
 
     // -- epilogue: D[i][j] of a 32x32 tile sits in lane j + 32*((i/4)%2), register (i/8)*4 + i%4
     const int n_base = nb * Cfg::BN + wn * 32 * NT;
@@ -281,14 +303,14 @@ struct Tile {
 
 // Spatial tile TH x TW = BM output samples: the shape that wastes the fewest
 // masked samples on this layer's fragment extent, then the smallest halo.
-static Tile pick_tile(int BM, int BN, int Hout, int Wout, int fh, int fw) {
+static Tile pick_tile(int BM, int BN, int HU, int threads, int Hout, int Wout, int fh, int fw) {
     Tile best{0, 0, 0};
     int64_t best_work = -1, best_halo = -1;
     for (int TW = 8; TW <= BM; TW *= 2) {
         const int TH = BM / TW;
         const int64_t halo_px = (int64_t)(TH + fh - 1) * (TW + fw - 1);
         const size_t lds = (size_t)((halo_px * kPitchBytes + 127) / 128) * 128 + 2 * (size_t)BN * kPitchBytes;
-        if (lds > (size_t)kMaxLds) continue;
+        if (lds > (size_t)kMaxLds || halo_px * 4 > (int64_t)HU * threads) continue;
         const int64_t work = ceil_div64(Hout, TH) * TH * ceil_div64(Wout, TW) * TW;
         if (best_work < 0 || work < best_work || (work == best_work && halo_px < best_halo)) {
             best = Tile{TH, TW, lds};
@@ -299,11 +321,20 @@ static Tile pick_tile(int BM, int BN, int Hout, int Wout, int fh, int fw) {
     return best;
 }
 
+// Whether some spatial tile of the variant chosen for `cout` keeps the halo of an
+// fh x fw filter within the staging bounds.
+bool mfma_supports(bool bf16, int cout, int fh, int fw) {
+    const int bn = bf16 ? mfma_bf16_pick_bn(cout) : mfma_f32_pick_bn(cout);
+    const int bm = bn == 128 ? 128 : 256;
+    const int hu = bm <= 128 ? 6 : 10;
+    return pick_tile(bm, bn, hu, 256, 1, 1, fh, fw).TH > 0 && pick_tile(bm, bn, hu, 256, 64, 64, fh, fw).TH > 0;
+}
+
 template <bool BF16, typename Tout, int WGM, int WGN, int NT>
 static hipError_t run_mfma(const void* in, int F, int Hin, int Win, const PlanConv& pc, void* out, hipStream_t s) {
     using Cfg = MfmaCfg<BF16, WGM, WGN, NT>;
     const int Hout = Hin - pc.fh + 1, Wout = Win - pc.fw + 1;
-    const Tile t = pick_tile(Cfg::BM, Cfg::BN, Hout, Wout, pc.fh, pc.fw);
+    const Tile t = pick_tile(Cfg::BM, Cfg::BN, Cfg::HU, Cfg::THREADS, Hout, Wout, pc.fh, pc.fw);
     if (t.TH == 0) return hipErrorInvalidConfiguration;
     const int tilesY = (int)ceil_div64(Hout, t.TH), tilesX = (int)ceil_div64(Wout, t.TW);
     const int64_t nblocks = (int64_t)F * tilesY * tilesX;

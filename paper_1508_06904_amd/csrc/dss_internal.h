@@ -118,7 +118,8 @@ hipError_t launch_to_planar(dss_dtype dt, const void* in, int F, int h, int w, i
 hipError_t launch_frag_planar(int elem_bytes, bool inverse, const void* in, int k_h, int k_w, int S_h,
                               int S_w, int C, int H, int W, void* out, hipStream_t s);
 
-// host-side weight packing for the MFMA kernels (conv_mfma_*.hip)
+// host-side weight packing for the MFMA kernels (conv_mfma.hip)
+bool mfma_supports(bool bf16, int cout, int fh, int fw);
 int mfma_f32_pick_bn(int cout);
 int mfma_bf16_pick_bn(int cout);
 size_t mfma_f32_packed_floats(const PlanConv& pc);

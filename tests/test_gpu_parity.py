@@ -321,7 +321,7 @@ def test_timing_records():
     recs = plan.timings()
     names = [r["kernel"] for r in recs]
     assert names[0] == "stuff_pack" and names[-1] == "defrag_trim"
-    assert "conv_mfma_f32" in names and "pool_frag" in names
+    assert "conv_mfma_f32_n128" in names and "conv_mfma_f32_n32" in names and "pool_frag" in names
     g = plan.geometry(120, 130)
     assert sum(r["flops"] for r in recs) == pytest.approx(g["conv_flops"], rel=1e-9)
     assert all(r["ms"] >= 0 for r in recs)
