@@ -38,6 +38,8 @@ typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));   // one 16-byte
 constexpr int kPitchBytes = 80;     // LDS bytes per staged sample / weight row
 constexpr int kChunkBytes = 64;     // bytes of one channel chunk per sample
 constexpr int kMaxLds = 64 * 1024;
+constexpr int kXcds = 8;            // accelerator complex dies of an MI355X
+constexpr int kGroup = 16;          // neighbouring tiles scheduled together
 
 template <bool BF16, int WGM, int WGN, int NT>
 struct MfmaCfg {
@@ -62,7 +64,7 @@ __global__ __launch_bounds__(256) void conv_mfma_kernel(
     const float* __restrict__ bias,    // [Cout_pad]
     int fh, int fw, int Cout, int act, int nchunks,
     Tout* __restrict__ out,            // [F][Hout][Wout][Cout]
-    int Hout, int Wout, int TH, int TW, int tilesY, int tilesX) {
+    int Hout, int Wout, int TH, int TW, int tilesY, int tilesX, int nbs) {
     using Cfg = MfmaCfg<BF16, WGM, WGN, NT>;
     constexpr int THREADS = Cfg::THREADS;
     constexpr int HU = Cfg::HU;
@@ -78,13 +80,27 @@ __global__ __launch_bounds__(256) void conv_mfma_kernel(
     const int half = lane >> 5;          // lane half: K slot of the MFMA operands
     const int l32 = lane & 31;
 
-    // workgroup -> (fragment, tile row, tile column), N block
+    // workgroup -> (fragment, tile row, tile column, N block).  Workgroups are
+    // handed to the 8 XCDs round-robin by id; the remap gives every XCD one
+    // contiguous range of work items.  Items are ordered in groups of kGroup
+    // neighbouring tiles (which share halo samples); inside a group the N block
+    // is the outer index, so the workgroups that run together on an XCD read the
+    // same weight slices and the same input tiles from its L2.
+    const int total = gridDim.x;
+    const int xcd = blockIdx.x % kXcds, slot = blockIdx.x / kXcds;
+    const int q8 = total / kXcds, r8 = total % kXcds;
+    const int item = xcd < r8 ? xcd * (q8 + 1) + slot : r8 * (q8 + 1) + (xcd - r8) * q8 + slot;
+    const int ntiles = total / nbs;
+    const int g = item / (kGroup * nbs);
+    const int gsize = min(kGroup, ntiles - g * kGroup);
+    const int grem = item - g * kGroup * nbs;
+    const int nb = grem / gsize;
+    const int tile = g * kGroup + grem % gsize;
     const int tiles = tilesY * tilesX;
-    const int f = blockIdx.x / tiles;
-    const int trem = blockIdx.x % tiles;
+    const int f = tile / tiles;
+    const int trem = tile % tiles;
     const int ty0 = (trem / tilesX) * TH;
     const int tx0 = (trem % tilesX) * TW;
-    const int nb = blockIdx.y;
 
     const int HW = TW + fw - 1;          // halo width
     const int halo_px = (TH + fh - 1) * HW;
@@ -337,13 +353,13 @@ static hipError_t run_mfma(const void* in, int F, int Hin, int Win, const PlanCo
     const Tile t = pick_tile(Cfg::BM, Cfg::BN, Cfg::HU, Cfg::THREADS, Hout, Wout, pc.fh, pc.fw);
     if (t.TH == 0) return hipErrorInvalidConfiguration;
     const int tilesY = (int)ceil_div64(Hout, t.TH), tilesX = (int)ceil_div64(Wout, t.TW);
-    const int64_t nblocks = (int64_t)F * tilesY * tilesX;
+    const int nbs = pc.cout_pad / Cfg::BN;
+    const int64_t nblocks = (int64_t)F * tilesY * tilesX * nbs;
     if (nblocks >= (1ll << 31)) return hipErrorInvalidConfiguration;
-    const dim3 grid((unsigned)nblocks, (unsigned)(pc.cout_pad / Cfg::BN));
     const int nchunks = pc.cin_pad / Cfg::CC;
-    conv_mfma_kernel<BF16, Tout, WGM, WGN, NT><<<grid, Cfg::THREADS, t.lds, s>>>(
+    conv_mfma_kernel<BF16, Tout, WGM, WGN, NT><<<dim3((unsigned)nblocks), Cfg::THREADS, t.lds, s>>>(
         (const char*)in, Hin, Win, pc.cin, (const char*)pc.w, pc.b, pc.fh, pc.fw, pc.cout, pc.act, nchunks,
-        (Tout*)out, Hout, Wout, t.TH, t.TW, tilesY, tilesX);
+        (Tout*)out, Hout, Wout, t.TH, t.TW, tilesY, tilesX, nbs);
     return hipGetLastError();
 }
 

@@ -8,7 +8,9 @@
 //  pool_frag    Slide_{g_max} followed by Frag_k (Definition "processing chain",
 //               Sect. 4.2): the k_h x k_w maximum at every position of every
 //               fragment (stride 1), written straight to its fragment after
-//               fragmentation.  Per axis, sliding-pool sample m*k + a of input
+//               fragmentation.  Pools up to 4 rows high use the separable strip
+//               kernel (each input row read once per column); taller pools the
+//               direct one.  Per axis, sliding-pool sample m*k + a of input
 //               fragment b lands at sample m of output fragment a*S + b
 //               (Lemma "frag-ops", Sect. 4.1).
 //  defrag_trim  Defrag_{k*_L} and Trim_r (appendix lemma on the simplified
@@ -89,10 +91,81 @@ __global__ __launch_bounds__(kThreads) void pool_frag_kernel(const T* __restrict
     VecIO<T, V>::store(dst, m);
 }
 
+// Separable form for small pool heights: one thread per (input fragment, strip
+// of NY sliding-pool rows, column, group of V channels).  The thread walks the
+// KH + NY - 1 input rows of its strip once, keeps the horizontal maxima of the
+// last KH rows in registers, and emits one output row per input row.
+template <typename T, int V, int KH, int NY>
+__global__ __launch_bounds__(kThreads) void pool_frag_strip_kernel(const T* __restrict__ in, int S_h, int S_w,
+                                                                  int E_h, int E_w, int C, int k_w,
+                                                                  T* __restrict__ out, int U_h, int U_w) {
+    const int CV = C / V;
+    const int P_h = KH * U_h, P_w = k_w * U_w;
+    const int strips = (P_h + NY - 1) / NY;
+    const int64_t total = (int64_t)S_h * S_w * strips * P_w * CV;
+    const int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (idx >= total) return;
+    const int cv = (int)(idx % CV);
+    int64_t t = idx / CV;
+    const int x = (int)(t % P_w);
+    t /= P_w;
+    const int strip = (int)(t % strips);
+    const int s = (int)(t / strips);
+    const int b_h = s / S_w, b_w = s % S_w;
+    const int y0 = strip * NY;
+    const int y1 = min(y0 + NY, P_h);
+
+    const T* src = in + (((int64_t)s * E_h + y0) * E_w + x) * C + cv * V;
+    const int a_w = x % k_w;
+    const int Fw = k_w * S_w;
+    const int64_t row_stride = (int64_t)E_w * C;
+    float ring[KH][V];
+    for (int yy = y0; yy < y1 + KH - 1; ++yy, src += row_stride) {
+        float h[V];
+        VecIO<T, V>::load(src, h);
+        for (int dx = 1; dx < k_w; ++dx) {
+            float v[V];
+            VecIO<T, V>::load(src + (int64_t)dx * C, v);
+#pragma unroll
+            for (int e = 0; e < V; ++e) h[e] = fmaxf(h[e], v[e]);
+        }
+#pragma unroll
+        for (int r = 0; r + 1 < KH; ++r)
+#pragma unroll
+            for (int e = 0; e < V; ++e) ring[r][e] = ring[r + 1][e];
+#pragma unroll
+        for (int e = 0; e < V; ++e) ring[KH - 1][e] = h[e];
+        if (yy >= y0 + KH - 1) {
+            const int y = yy - (KH - 1);
+            float m[V];
+#pragma unroll
+            for (int e = 0; e < V; ++e) {
+                m[e] = ring[0][e];
+#pragma unroll
+                for (int r = 1; r < KH; ++r) m[e] = fmaxf(m[e], ring[r][e]);
+            }
+            const int f_new = ((y % KH) * S_h + b_h) * Fw + (a_w * S_w + b_w);
+            VecIO<T, V>::store(out + (((int64_t)f_new * U_h + y / KH) * U_w + x / k_w) * C + cv * V, m);
+        }
+    }
+}
+
 template <typename T, int V>
 static void run_pool(const void* in, int S_h, int S_w, int E_h, int E_w, int C, int k_h, int k_w, void* out,
                      hipStream_t s) {
     const int U_h = (E_h - k_h + 1) / k_h, U_w = (E_w - k_w + 1) / k_w;
+    constexpr int NY = 16;
+    if (k_h >= 1 && k_h <= 4) {
+        const int64_t total = (int64_t)S_h * S_w * ((k_h * U_h + NY - 1) / NY) * (k_w * U_w) * (C / V);
+        const dim3 grid((unsigned)ceil_div64(total, kThreads));
+        switch (k_h) {
+            case 1: pool_frag_strip_kernel<T, V, 1, NY><<<grid, kThreads, 0, s>>>((const T*)in, S_h, S_w, E_h, E_w, C, k_w, (T*)out, U_h, U_w); break;
+            case 2: pool_frag_strip_kernel<T, V, 2, NY><<<grid, kThreads, 0, s>>>((const T*)in, S_h, S_w, E_h, E_w, C, k_w, (T*)out, U_h, U_w); break;
+            case 3: pool_frag_strip_kernel<T, V, 3, NY><<<grid, kThreads, 0, s>>>((const T*)in, S_h, S_w, E_h, E_w, C, k_w, (T*)out, U_h, U_w); break;
+            default: pool_frag_strip_kernel<T, V, 4, NY><<<grid, kThreads, 0, s>>>((const T*)in, S_h, S_w, E_h, E_w, C, k_w, (T*)out, U_h, U_w); break;
+        }
+        return;
+    }
     const int64_t total = (int64_t)S_h * S_w * (k_h * U_h) * (k_w * U_w) * (C / V);
     pool_frag_kernel<T, V><<<dim3((unsigned)ceil_div64(total, kThreads)), kThreads, 0, s>>>(
         (const T*)in, S_h, S_w, E_h, E_w, C, k_h, k_w, (T*)out, U_h, U_w);
