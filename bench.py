@@ -40,6 +40,24 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
+def profiled_traffic(kernel, config):
+    """HBM bytes per launch of `kernel` on `config` from the committed rocprofv3
+    counter summaries (FETCH_SIZE + WRITE_SIZE, scaled by a plain copy), or None
+    when no summary covers it or the kernel source changed since it was taken."""
+    import glob
+    import hashlib
+    src = b"".join(open(os.path.join(ROOT, "paper_1508_06904_amd", "csrc", f), "rb").read()
+                   for f in ("conv_mfma.hip", "dev_common.h"))
+    h = hashlib.sha256(src).hexdigest()[:16]
+    for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "*.md"))):
+        for line in open(path):
+            if line.startswith("traffic-json:"):
+                d = json.loads(line.split(":", 1)[1])
+                if d["kernel"] == kernel and d["workload"] == config and d["source_sha256_16"] == h:
+                    return d["traffic_bytes_per_launch"]
+    return None
+
+
 def summarize(recs, steps):
     by = {}
     for r in recs:
@@ -129,7 +147,8 @@ def main():
         ach = (domd["flops"] / domd["n"]) / (domd["ms"] / domd["n"]) / 1e9
         peak = PEAK_TFLOPS[w.dtype]
         roof = {"bound": "mfma", "kernel": dom["kernel"], "achieved": ach, "peak": peak, "unit": "TFLOP/s",
-                "frac": ach / peak, "traffic": None,
+                "frac": ach / peak, "traffic": profiled_traffic(dom["kernel"], args.config),
+                "traffic_unit": "bytes per launch (HBM, rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
                 "per_launch": {"flops": domd["flops"] / domd["n"], "avg_ms": domd["ms"] / domd["n"],
                                "launches_per_step": domd["n"] / args.steps}}
     else:
