@@ -7,8 +7,10 @@
 // As a GEMM: M = output samples (a TH x TW spatial tile of one fragment per
 // workgroup), N = output channels, K = fh * fw * Cin.
 //
-// Workgroup = 4 wavefronts of 64 lanes; each wave owns a 64 x (32*NT) block of
-// the output tile, computed with 32x32 MFMA tiles:
+// Workgroup = 4 wavefronts of 64 lanes; each wave owns a (32*MT) x (32*NT) block
+// of the output tile (128 x 64 for the wide layers: per MFMA K step a lane reads
+// 16 bytes of A per 32 rows and of B per 32 columns from LDS, so the wider the
+// wave tile the fewer LDS bytes per flop), computed with 32x32 MFMA tiles:
 //   binary32:  v_mfma_f32_32x32x2_f32   (K = 2 per issue)
 //   bfloat16:  v_mfma_f32_32x32x16_bf16 (K = 16 per issue), binary32 accumulation
 // K loop: input channels in chunks of 64 bytes per sample (16 binary32 or 32
@@ -26,6 +28,8 @@
 //
 // Epilogue: + bias, activation, masked store (edge tiles, padded channels) in
 // the channels-last output layout; binary32 or bfloat16 (round to nearest even).
+#include <algorithm>
+
 #include "dev_common.h"
 #include "dss_internal.h"
 
@@ -36,40 +40,48 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));   // one 16-byte unit
 
 constexpr int kPitchBytes = 80;     // LDS bytes per staged sample / weight row
+constexpr int kSlotsPerRow = kPitchBytes / 16;
 constexpr int kChunkBytes = 64;     // bytes of one channel chunk per sample
-constexpr int kMaxLds = 64 * 1024;
+constexpr int kMaxLds = 78 * 1024;  // two workgroups per CU (160 KB of LDS)
 constexpr int kXcds = 8;            // accelerator complex dies of an MI355X
 constexpr int kGroup = 16;          // neighbouring tiles scheduled together
 
-template <bool BF16, int WGM, int WGN, int NT>
+template <bool BF16, int WGM, int WGN, int MT, int NT>
 struct MfmaCfg {
     static constexpr int ES = BF16 ? 2 : 4;
     static constexpr int CC = kChunkBytes / ES;        // channels per chunk
-    static constexpr int BM = 64 * WGM;                 // output samples per workgroup
+    static constexpr int BM = 32 * MT * WGM;            // output samples per workgroup
     static constexpr int BN = 32 * NT * WGN;            // output channels per workgroup
     static constexpr int THREADS = 64 * WGM * WGN;
-    static constexpr int WSLICE_UNITS = BN * (kChunkBytes / 16);  // 16-byte units per weight slice
-    static constexpr int WPER = (WSLICE_UNITS + THREADS - 1) / THREADS;
-    // 16-byte halo units each thread stages per chunk (bounds the halo extent)
-    static constexpr int HU = BM <= 128 ? 6 : 10;
+    static constexpr int WSLOTS = BN * kSlotsPerRow;    // 16-byte LDS slots of one weight slice
 };
+
+// 16 zero bytes: the source of every staged unit that lies outside the fragment
+// or in the zero-padded channels of the last chunk.
+__device__ __attribute__((aligned(16))) const unsigned int g_zero16[4] = {0u, 0u, 0u, 0u};
 
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
 
-template <bool BF16, typename Tout, int WGM, int WGN, int NT>
-__global__ __launch_bounds__(256) void conv_mfma_kernel(
+typedef __attribute__((address_space(3))) void lds_void;
+
+// Direct global -> LDS copy of one 16-byte unit per active lane: the unit lands in
+// LDS at wave_dst + 16 * lane (gfx950 global_load_lds_dwordx4).
+__device__ __forceinline__ void dma16(const void* src, char* wave_dst) {
+    __builtin_amdgcn_global_load_lds(src, (lds_void*)wave_dst, 16, 0, 0);
+}
+
+template <bool BF16, typename Tout, int WGM, int WGN, int MT, int NT>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void conv_mfma_kernel(
     const char* __restrict__ in,       // [F][Hin][Win][Cin] of BF16 ? bfloat16 : binary32
     int Hin, int Win, int Cin,
     const char* __restrict__ wp,       // packed [nb][chunk][th][tw][BN][chunk channels]
     const float* __restrict__ bias,    // [Cout_pad]
     int fh, int fw, int Cout, int act, int nchunks,
     Tout* __restrict__ out,            // [F][Hout][Wout][Cout]
-    int Hout, int Wout, int TH, int TW, int tilesY, int tilesX, int nbs) {
-    using Cfg = MfmaCfg<BF16, WGM, WGN, NT>;
+    int Hout, int Wout, int TH, int TW, int tilesY, int tilesX, int nbs, int dbl_halo) {
+    using Cfg = MfmaCfg<BF16, WGM, WGN, MT, NT>;
     constexpr int THREADS = Cfg::THREADS;
-    constexpr int HU = Cfg::HU;
-    constexpr int WPER = Cfg::WPER;
-    constexpr int WU = Cfg::WSLICE_UNITS;
+    constexpr int WSLOTS = Cfg::WSLOTS;
     extern __shared__ __attribute__((aligned(16))) char lds[];
 
     const int tid = threadIdx.x;
@@ -104,107 +116,92 @@ __global__ __launch_bounds__(256) void conv_mfma_kernel(
 
     const int HW = TW + fw - 1;          // halo width
     const int halo_px = (TH + fh - 1) * HW;
-    char* halo = lds;
-    char* wbuf0 = lds + ((halo_px * kPitchBytes + 127) / 128) * 128;
+    const int halo_slots = halo_px * kSlotsPerRow;
+    const int halo_bytes = ((halo_px * kPitchBytes + 127) / 128) * 128;
+    char* halo0 = lds;
+    char* halo1 = dbl_halo ? lds + halo_bytes : lds;
+    char* wbuf0 = lds + (dbl_halo ? 2 : 1) * halo_bytes;
     char* wbuf1 = wbuf0 + Cfg::BN * kPitchBytes;
 
     // per-lane operand offsets (bytes) inside the halo / weight slice
-    int a_off[2];
+    int a_off[MT];
 #pragma unroll
-    for (int mt = 0; mt < 2; ++mt) {
-        const int m = wm * 64 + mt * 32 + l32;
+    for (int mt = 0; mt < MT; ++mt) {
+        const int m = wm * 32 * MT + mt * 32 + l32;
         a_off[mt] = ((m / TW) * HW + (m % TW)) * kPitchBytes + half * 32;
     }
     int b_off[NT];
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) b_off[nt] = (wn * 32 * NT + nt * 32 + l32) * kPitchBytes + half * 32;
 
-    // per-thread halo units.  Unit u = tid + r*THREADS is 16-byte quad q = u & 3 (the
-    // same for every r) of halo sample u >> 2.  Sources are 32-bit byte offsets from
-    // the tile's top-left input sample (-1 outside the fragment); only the chunk
-    // offset changes between chunks.
-    const size_t row_bytes = (size_t)Cin * Cfg::ES;
-    const char* in_tile = in + (((size_t)f * Hin + ty0) * Win + tx0) * row_bytes;
-    const int hq = tid & 3;
-    const int h_c0 = hq * (16 / Cfg::ES);          // first channel of this thread's quad
-    const int h_px0 = tid >> 2;
-    constexpr int PX_STEP = THREADS / 4;
-    int h_src[HU];
+    floatx16 acc[MT][NT];
 #pragma unroll
-    for (int r = 0; r < HU; ++r) {
-        const int px = h_px0 + r * PX_STEP;
-        const int dy = px / HW, dx = px % HW;
-        h_src[r] = (px < halo_px && ty0 + dy < Hin && tx0 + dx < Win) ? (dy * Win + dx) * (int)row_bytes + hq * 16 : -1;
-    }
-    u32x4 hreg[HU];
-    u32x4 wreg[WPER];
-
-    floatx16 acc[2][NT];
-#pragma unroll
-    for (int mt = 0; mt < 2; ++mt)
+    for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
             for (int v = 0; v < 16; ++v) acc[mt][nt][v] = 0.f;
 
+    const size_t row_bytes = (size_t)Cin * Cfg::ES;
+    const char* in_tile = in + (((size_t)f * Hin + ty0) * Win + tx0) * row_bytes;
     const int taps = fh * fw;
     const int steps = nchunks * taps;
     const char* w_nb = wp + (size_t)nb * steps * (Cfg::BN * kChunkBytes);
+    const char* zero = reinterpret_cast<const char*>(g_zero16);
 
-#define DSS_HALO_FETCH(cc)                                                                       \
-    {                                                                                            \
-        const bool chan_ok = (cc) * Cfg::CC + h_c0 < Cin;                                        \
-        const char* src_c = in_tile + (size_t)(cc) * kChunkBytes;                                \
-        _Pragma("unroll") for (int r = 0; r < HU; ++r) {                                         \
-            u32x4 v = {0u, 0u, 0u, 0u};                                                          \
-            if (chan_ok && h_src[r] >= 0) v = *reinterpret_cast<const u32x4*>(src_c + h_src[r]); \
-            hreg[r] = v;                                                                         \
-        }                                                                                        \
-    }
-#define DSS_HALO_STORE()                                                                         \
-    _Pragma("unroll") for (int r = 0; r < HU; ++r) {                                             \
-        if (h_px0 + r * PX_STEP < halo_px)                                                       \
-            *reinterpret_cast<u32x4*>(halo + (h_px0 + r * PX_STEP) * kPitchBytes + hq * 16) = hreg[r]; \
-    }
-#define DSS_W_FETCH(st)                                                                          \
-    _Pragma("unroll") for (int r = 0; r < WPER; ++r) {                                           \
-        const int u = tid + r * THREADS;                                                         \
-        if (WU % THREADS == 0 || u < WU)                                                         \
-            wreg[r] = *reinterpret_cast<const u32x4*>(w_nb + (size_t)(st) * (Cfg::BN * kChunkBytes) + (size_t)u * 16); \
-    }
-#define DSS_W_STORE(dst)                                                                         \
-    _Pragma("unroll") for (int r = 0; r < WPER; ++r) {                                           \
-        const int u = tid + r * THREADS;                                                         \
-        if (WU % THREADS == 0 || u < WU)                                                         \
-            *reinterpret_cast<u32x4*>((dst) + (u >> 2) * kPitchBytes + (u & 3) * 16) = wreg[r];  \
-    }
+    // Staging: LDS slot S (16 bytes) of the halo holds quad S % 5 of halo sample
+    // S / 5 (slot 4 of every sample is padding and is never written); lane l of
+    // wave w stages slot r * THREADS + w * 64 + l in round r.
+    auto stage_halo = [&](int cc, char* dst) {
+        const char* src_c = in_tile + (size_t)cc * kChunkBytes;
+        const int c_base = cc * Cfg::CC;
+        for (int r0 = 0; r0 < halo_slots; r0 += THREADS) {
+            const int S = r0 + tid;
+            const int px = S / kSlotsPerRow, q = S - px * kSlotsPerRow;
+            if (S < halo_slots && q < 4) {
+                const int dy = px / HW, dx = px - dy * HW;
+                const bool ok = ty0 + dy < Hin && tx0 + dx < Win && c_base + q * (16 / Cfg::ES) < Cin;
+                dma16(ok ? src_c + ((size_t)dy * Win + dx) * row_bytes + q * 16 : zero, dst + (r0 + wave * 64) * 16);
+            }
+        }
+    };
+    auto stage_w = [&](int st, char* dst) {
+        const char* src = w_nb + (size_t)st * (Cfg::BN * kChunkBytes);
+        for (int r0 = 0; r0 < WSLOTS; r0 += THREADS) {
+            const int S = r0 + tid;
+            const int n = S / kSlotsPerRow, q = S - n * kSlotsPerRow;
+            if (S < WSLOTS && q < 4) dma16(src + n * kChunkBytes + q * 16, dst + (r0 + wave * 64) * 16);
+        }
+    };
+    auto wait_staged = [] {
+        __builtin_amdgcn_s_waitcnt(0);   // this wave's copies have landed in LDS
+        __syncthreads();                 // ... and every other wave's
+    };
 
     // -- prologue: chunk 0 halo and the first weight slice
-    DSS_HALO_FETCH(0);
-    DSS_W_FETCH(0);
-    DSS_HALO_STORE();
-    DSS_W_STORE(wbuf0);
-    __syncthreads();
+    stage_halo(0, halo0);
+    stage_w(0, wbuf0);
+    wait_staged();
 
     int step = 0;
     for (int cc = 0; cc < nchunks; ++cc) {
+        const char* halo = (cc & 1) ? halo1 : halo0;
         for (int th = 0; th < fh; ++th) {
             for (int tw = 0; tw < fw; ++tw, ++step) {
                 const bool has_next = step + 1 < steps;
                 const bool last_tap = (th == fh - 1) && (tw == fw - 1);
-                // prefetch the next weight slice (and the next chunk's halo) into registers;
-                // the loads complete while the MFMAs below run
+                // stage the next weight slice (its buffer was last read in the
+                // previous step) and, with a double-buffered halo, the next chunk's
+                // halo; the copies run while the MFMAs below execute
                 if (has_next) {
-                    DSS_W_FETCH(step + 1);
-                    if (last_tap) {
-                        DSS_HALO_FETCH(cc + 1);
-                    }
+                    stage_w(step + 1, (step & 1) ? wbuf0 : wbuf1);
+                    if (last_tap && dbl_halo) stage_halo(cc + 1, (cc & 1) ? halo0 : halo1);
                 }
                 const int tap_off = (th * HW + tw) * kPitchBytes;
                 const char* wcur = (step & 1) ? wbuf1 : wbuf0;
-                u32x4 a[2][2], b[NT][2];
+                u32x4 a[MT][2], b[NT][2];
 #pragma unroll
-                for (int mt = 0; mt < 2; ++mt) {
+                for (int mt = 0; mt < MT; ++mt) {
                     a[mt][0] = *reinterpret_cast<const u32x4*>(halo + a_off[mt] + tap_off);
                     a[mt][1] = *reinterpret_cast<const u32x4*>(halo + a_off[mt] + tap_off + 16);
                 }
@@ -217,7 +214,7 @@ __global__ __launch_bounds__(256) void conv_mfma_kernel(
 #pragma unroll
                     for (int s = 0; s < 2; ++s)
 #pragma unroll
-                        for (int mt = 0; mt < 2; ++mt)
+                        for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
                             for (int nt = 0; nt < NT; ++nt)
                                 acc[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
@@ -226,7 +223,7 @@ __global__ __launch_bounds__(256) void conv_mfma_kernel(
 #pragma unroll
                     for (int s = 0; s < 8; ++s) {
 #pragma unroll
-                        for (int mt = 0; mt < 2; ++mt) {
+                        for (int mt = 0; mt < MT; ++mt) {
                             const uint32_t aw = a[mt][s >> 2][s & 3];
 #pragma unroll
                             for (int nt = 0; nt < NT; ++nt) {
@@ -237,21 +234,14 @@ __global__ __launch_bounds__(256) void conv_mfma_kernel(
                         }
                     }
                 }
-                if (has_next) {
-                    if (last_tap) {
-                        __syncthreads();          // every wave is done with this chunk's halo
-                        DSS_HALO_STORE();
-                    }
-                    DSS_W_STORE((step & 1) ? wbuf0 : wbuf1);
+                if (has_next && last_tap && !dbl_halo) {
+                    __syncthreads();                   // every wave is done with this chunk's halo
+                    stage_halo(cc + 1, halo0);
                 }
-                __syncthreads();
+                wait_staged();
             }
         }
     }
-#undef DSS_HALO_FETCH
-#undef DSS_HALO_STORE
-#undef DSS_W_FETCH
-#undef DSS_W_STORE
 
     // -- epilogue: D[i][j] of a 32x32 tile sits in lane j + 32*((i/4)%2), register (i/8)*4 + i%4
     const int n_base = nb * Cfg::BN + wn * 32 * NT;
@@ -262,11 +252,11 @@ __global__ __launch_bounds__(256) void conv_mfma_kernel(
         if (n >= Cout) continue;
         const float bn = bias[n];
 #pragma unroll
-        for (int mt = 0; mt < 2; ++mt) {
+        for (int mt = 0; mt < MT; ++mt) {
 #pragma unroll
             for (int v = 0; v < 16; ++v) {
                 const int i = (v >> 2) * 8 + half * 4 + (v & 3);
-                const int m = wm * 64 + mt * 32 + i;
+                const int m = wm * 32 * MT + mt * 32 + i;
                 const int y = ty0 + m / TW, x = tx0 + m % TW;
                 if (y < Hout && x < Wout)
                     store_elem(out + (f_off + (size_t)y * Wout + x) * Cout + n, activate(act, acc[mt][nt][v] + bn));
@@ -315,21 +305,45 @@ void mfma_bf16_pack(const PlanConv& pc, const float* w, uint16_t* dst) {
 struct Tile {
     int TH, TW;
     size_t lds;
+    int dbl;    // halo double-buffered
 };
 
+// Largest dynamic LDS allocation per workgroup on the current device.
+static size_t device_lds_limit() {
+    static int cached = -1;
+    if (cached < 0) {
+        int dev = 0, v = 0;
+        if (hipGetDevice(&dev) != hipSuccess ||
+            hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess)
+            v = 64 * 1024;
+        cached = v;
+    }
+    return (size_t)cached;
+}
+
 // Spatial tile TH x TW = BM output samples: the shape that wastes the fewest
-// masked samples on this layer's fragment extent, then the smallest halo.
-static Tile pick_tile(int BM, int BN, int HU, int threads, int Hout, int Wout, int fh, int fw) {
-    Tile best{0, 0, 0};
+// masked samples on this layer's fragment extent; among those, one whose halo can
+// be double-buffered within the LDS budget of two workgroups per CU, then the
+// smallest halo.
+static Tile pick_tile(int BM, int BN, int Hout, int Wout, int fh, int fw, size_t lds_max) {
+    Tile best{0, 0, 0, 0};
     int64_t best_work = -1, best_halo = -1;
     for (int TW = 8; TW <= BM; TW *= 2) {
         const int TH = BM / TW;
         const int64_t halo_px = (int64_t)(TH + fh - 1) * (TW + fw - 1);
-        const size_t lds = (size_t)((halo_px * kPitchBytes + 127) / 128) * 128 + 2 * (size_t)BN * kPitchBytes;
-        if (lds > (size_t)kMaxLds || halo_px * 4 > (int64_t)HU * threads) continue;
+        const size_t halo_b = (size_t)((halo_px * kPitchBytes + 127) / 128) * 128;
+        const size_t wb = 2 * (size_t)BN * kPitchBytes;
+        const size_t cap = std::min(lds_max, (size_t)kMaxLds);
+        int dbl;
+        size_t lds;
+        if (2 * halo_b + wb <= cap) { dbl = 1; lds = 2 * halo_b + wb; }
+        else if (halo_b + wb <= cap) { dbl = 0; lds = halo_b + wb; }
+        else continue;
         const int64_t work = ceil_div64(Hout, TH) * TH * ceil_div64(Wout, TW) * TW;
-        if (best_work < 0 || work < best_work || (work == best_work && halo_px < best_halo)) {
-            best = Tile{TH, TW, lds};
+        const bool better = best_work < 0 || work < best_work ||
+                            (work == best_work && (dbl > best.dbl || (dbl == best.dbl && halo_px < best_halo)));
+        if (better) {
+            best = Tile{TH, TW, lds, dbl};
             best_work = work;
             best_halo = halo_px;
         }
@@ -337,38 +351,45 @@ static Tile pick_tile(int BM, int BN, int HU, int threads, int Hout, int Wout, i
     return best;
 }
 
-// Whether some spatial tile of the variant chosen for `cout` keeps the halo of an
-// fh x fw filter within the staging bounds.
+// Whether some spatial tile of the variant chosen for `cout` fits an fh x fw
+// filter's halo into LDS (checked against the 64 KB every device offers).
 bool mfma_supports(bool bf16, int cout, int fh, int fw) {
     const int bn = bf16 ? mfma_bf16_pick_bn(cout) : mfma_f32_pick_bn(cout);
-    const int bm = bn == 128 ? 128 : 256;
-    const int hu = bm <= 128 ? 6 : 10;
-    return pick_tile(bm, bn, hu, 256, 1, 1, fh, fw).TH > 0 && pick_tile(bm, bn, hu, 256, 64, 64, fh, fw).TH > 0;
+    return pick_tile(256, bn, 1, 1, fh, fw, 64 * 1024).TH > 0 && pick_tile(256, bn, 64, 64, fh, fw, 64 * 1024).TH > 0;
 }
 
-template <bool BF16, typename Tout, int WGM, int WGN, int NT>
+template <bool BF16, typename Tout, int WGM, int WGN, int MT, int NT>
 static hipError_t run_mfma(const void* in, int F, int Hin, int Win, const PlanConv& pc, void* out, hipStream_t s) {
-    using Cfg = MfmaCfg<BF16, WGM, WGN, NT>;
+    using Cfg = MfmaCfg<BF16, WGM, WGN, MT, NT>;
     const int Hout = Hin - pc.fh + 1, Wout = Win - pc.fw + 1;
-    const Tile t = pick_tile(Cfg::BM, Cfg::BN, Cfg::HU, Cfg::THREADS, Hout, Wout, pc.fh, pc.fw);
+    const Tile t = pick_tile(Cfg::BM, Cfg::BN, Hout, Wout, pc.fh, pc.fw, device_lds_limit());
     if (t.TH == 0) return hipErrorInvalidConfiguration;
+    auto kern = conv_mfma_kernel<BF16, Tout, WGM, WGN, MT, NT>;
+    if (t.lds > 64 * 1024) {
+        static bool attr_set = false;   // per instantiation
+        if (!attr_set) {
+            hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kMaxLds);
+            if (e != hipSuccess) return e;
+            attr_set = true;
+        }
+    }
     const int tilesY = (int)ceil_div64(Hout, t.TH), tilesX = (int)ceil_div64(Wout, t.TW);
     const int nbs = pc.cout_pad / Cfg::BN;
     const int64_t nblocks = (int64_t)F * tilesY * tilesX * nbs;
     if (nblocks >= (1ll << 31)) return hipErrorInvalidConfiguration;
     const int nchunks = pc.cin_pad / Cfg::CC;
-    conv_mfma_kernel<BF16, Tout, WGM, WGN, NT><<<dim3((unsigned)nblocks), Cfg::THREADS, t.lds, s>>>(
+    kern<<<dim3((unsigned)nblocks), Cfg::THREADS, t.lds, s>>>(
         (const char*)in, Hin, Win, pc.cin, (const char*)pc.w, pc.b, pc.fh, pc.fw, pc.cout, pc.act, nchunks,
-        (Tout*)out, Hout, Wout, t.TH, t.TW, tilesY, tilesX, nbs);
+        (Tout*)out, Hout, Wout, t.TH, t.TW, tilesY, tilesX, nbs, t.dbl);
     return hipGetLastError();
 }
 
 template <bool BF16, typename Tout>
 static hipError_t dispatch_bn(const void* in, int F, int Hin, int Win, const PlanConv& pc, void* out, hipStream_t s) {
     switch (pc.bn) {
-        case 128: return run_mfma<BF16, Tout, 2, 2, 2>(in, F, Hin, Win, pc, out, s);
-        case 64: return run_mfma<BF16, Tout, 4, 1, 2>(in, F, Hin, Win, pc, out, s);
-        case 32: return run_mfma<BF16, Tout, 4, 1, 1>(in, F, Hin, Win, pc, out, s);
+        case 128: return run_mfma<BF16, Tout, 2, 2, 4, 2>(in, F, Hin, Win, pc, out, s);
+        case 64: return run_mfma<BF16, Tout, 4, 1, 2, 2>(in, F, Hin, Win, pc, out, s);
+        case 32: return run_mfma<BF16, Tout, 4, 1, 2, 1>(in, F, Hin, Win, pc, out, s);
     }
     return hipErrorInvalidValue;
 }
