@@ -151,7 +151,18 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
 
     // Staging: LDS slot S (16 bytes) of the halo holds quad S % 5 of halo sample
     // S / 5 (slot 4 of every sample is padding and is never written); lane l of
-    // wave w stages slot r * THREADS + w * 64 + l in round r.
+    // wave w stages slot r * THREADS + w * 64 + l in round r.  Weight slots map to
+    // the same source offsets in every step, so they are computed once (kPad: a
+    // padding slot, nothing to stage); the halo mapping is recomputed per chunk.
+    constexpr int kPad = -1;
+    constexpr int kWRounds = (WSLOTS + THREADS - 1) / THREADS;
+    int w_off[kWRounds];
+#pragma unroll
+    for (int r = 0; r < kWRounds; ++r) {
+        const int S = r * THREADS + tid;
+        const int n = S / kSlotsPerRow, q = S - n * kSlotsPerRow;
+        w_off[r] = (S >= WSLOTS || q == 4) ? kPad : n * kChunkBytes + q * 16;
+    }
     auto stage_halo = [&](int cc, char* dst) {
         const char* src_c = in_tile + (size_t)cc * kChunkBytes;
         const int c_base = cc * Cfg::CC;
@@ -167,11 +178,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
     };
     auto stage_w = [&](int st, char* dst) {
         const char* src = w_nb + (size_t)st * (Cfg::BN * kChunkBytes);
-        for (int r0 = 0; r0 < WSLOTS; r0 += THREADS) {
-            const int S = r0 + tid;
-            const int n = S / kSlotsPerRow, q = S - n * kSlotsPerRow;
-            if (S < WSLOTS && q < 4) dma16(src + n * kChunkBytes + q * 16, dst + (r0 + wave * 64) * 16);
-        }
+#pragma unroll
+        for (int r = 0; r < kWRounds; ++r)
+            if (w_off[r] != kPad) dma16(src + w_off[r], dst + (r * THREADS + wave * 64) * 16);
     };
     auto wait_staged = [] {
         __builtin_amdgcn_s_waitcnt(0);   // this wave's copies have landed in LDS
