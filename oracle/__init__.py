@@ -172,3 +172,6 @@ def eval_stride(layers, x, windows=None, upto=None, patch=None, threads=0, with_
     if with_counts:
         return res, counts[:upto].copy()
     return res
+
+
+from . import mixed  # noqa: E402,F401  (needs eval_stride above)
