@@ -11,6 +11,11 @@ Prints ONE JSON line with the throughput, a roofline object for the dominant
 kernel (per-launch HIP-event durations measured inside the timed region), a
 per-kernel breakdown, and the oracle's throughput on a bounded window sample of
 the same frame (CPU baseline, also used as a parity spot check).
+
+`--ell l` (l > 0) times the mixed evaluation instead (appendix, Theorem
+"evalrelaxslide"): the first l chain layers pool with stride, and the output is
+the dense output downsampled by k*_l per axis; the metric then counts those
+window outputs.
 """
 from __future__ import annotations
 
@@ -86,6 +91,8 @@ def main():
     ap.add_argument("--config", default="c4_hd", choices=sorted(WORKLOAD_TEXT))
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target length of the oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--ell", type=int, default=0,
+                    help="mixed level: chain layers 1..ell run relaxed (0 = dense evaluation)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run plain 1 GiB device-to-device copies (scales the HBM byte counters of a profiler)")
     args = ap.parse_args()
@@ -109,17 +116,24 @@ def main():
     log("workload %s %s generated in %.1fs" % (args.config, w.x.shape, time.time() - t0))
     plan = dss.Plan.from_workload(w)
     C, H, W = w.x.shape
-    g = plan.geometry(H, W)
+    ell = args.ell
+    g = plan.geometry(H, W, ell)
     x = torch.from_numpy(w.x).to("cuda")
     if w.dtype == "bf16":
         x = x.to(torch.bfloat16)
     x = x.contiguous()
     out = torch.empty((g["out_c"], g["out_h"], g["out_w"]), dtype=torch.float32, device="cuda")
-    ws = plan.workspace(H, W)
+    ws = plan.workspace(H, W, ell=ell)
     windows = g["out_h"] * g["out_w"]
 
+    def step():
+        if ell == 0:
+            plan.eval_dense(x, out=out, workspace=ws)
+        else:
+            plan.eval_mixed(x, ell, out=out, workspace=ws)
+
     for i in range(args.warmup):
-        plan.eval_dense(x, out=out, workspace=ws)
+        step()
         torch.cuda.synchronize()
         log("warmup %d done" % i)
 
@@ -130,7 +144,7 @@ def main():
     t_wall = time.perf_counter()
     start.record()
     for _ in range(args.steps):
-        plan.eval_dense(x, out=out, workspace=ws)
+        step()
     end.record()
     torch.cuda.synchronize()
     wall_s = time.perf_counter() - t_wall
@@ -147,7 +161,7 @@ def main():
         ach = (domd["flops"] / domd["n"]) / (domd["ms"] / domd["n"]) / 1e9
         peak = PEAK_TFLOPS[w.dtype]
         roof = {"bound": "mfma", "kernel": dom["kernel"], "achieved": ach, "peak": peak, "unit": "TFLOP/s",
-                "frac": ach / peak, "traffic": profiled_traffic(dom["kernel"], args.config),
+                "frac": ach / peak, "traffic": profiled_traffic(dom["kernel"], args.config if ell == 0 else "%s_ell%d" % (args.config, ell)),
                 "traffic_unit": "bytes per launch (HBM, rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
                 "per_launch": {"flops": domd["flops"] / domd["n"], "avg_ms": domd["ms"] / domd["n"],
                                "launches_per_step": domd["n"] / args.steps}}
@@ -159,8 +173,15 @@ def main():
     conv_ms = sum(d["ms"] for e, d in kernels if d["flops"] > 0) / args.steps
     conv_tflops = g["conv_flops"] / (conv_ms * 1e9) if conv_ms > 0 else None
 
+    config = {"workload": args.config + ": " + WORKLOAD_TEXT[args.config], "input": [C, H, W],
+              "windows_per_step": windows, "receptive_field": [g["B_h"], g["B_w"]],
+              "k_star": [g["K_h"], g["K_w"]], "conv_gflop_per_step": g["conv_flops"] / 1e9}
+    if ell:
+        config.update({"mixed_level": ell, "output_spacing": [g["step_h"], g["step_w"]],
+                       "trimmed": [g["trim_h"], g["trim_w"]], "stuffed": [g["r_h"], g["r_w"]]})
     record = {
-        "metric": "dense window outputs/sec at 1 MI355X",
+        "metric": "dense window outputs/sec at 1 MI355X" if ell == 0 else
+                  "mixed-fashion window outputs/sec at 1 MI355X (every k*_l-th window per axis)",
         "value": windows / (ms_per_step / 1e3),
         "unit": "windows/s",
         "n_gpus": 1,
@@ -172,9 +193,7 @@ def main():
         "vs_baseline": None,
         "dtype": w.dtype,
         "data": "synthetic (seeded), random He-init weights",
-        "config": {"workload": args.config + ": " + WORKLOAD_TEXT[args.config], "input": [C, H, W],
-                   "windows_per_step": windows, "receptive_field": [g["B_h"], g["B_w"]],
-                   "k_star": [g["K_h"], g["K_w"]], "conv_gflop_per_step": g["conv_flops"] / 1e9},
+        "config": config,
         "roofline": roof,
         "conv_aggregate": {"tflops": conv_tflops, "frac_of_peak": (conv_tflops / PEAK_TFLOPS[w.dtype]) if conv_tflops else None,
                            "ms_per_step": conv_ms},
@@ -215,20 +234,24 @@ def cpu_baseline(w, g, out, target_s):
         layers = [dict(l, weight=wl.to_bf16_representable(l["weight"])) if l["kind"] == "conv" else l
                   for l in w.layers]
     threads = oracle.threads()
-    si, sj = wl.sample_windows(g["out_h"], g["out_w"], g["K_h"], g["K_w"], per_phase=1, seed=1)
+    # output positions are sampled over the phases of the final defragmentation
+    # (k*_L / k*_l per axis); output (i, j) is the window at (k*_l,h i, k*_l,w j)
+    Gh, Gw = g["K_h"] // g["step_h"], g["K_w"] // g["step_w"]
+    sh, sw = g["step_h"], g["step_w"]
+    si, sj = wl.sample_windows(g["out_h"], g["out_w"], Gh, Gw, per_phase=1, seed=1)
     nprobe = min(len(si), threads)
     t = time.perf_counter()
-    oracle.eval_stride(layers, w.x, windows=(si[:nprobe], sj[:nprobe]))
+    oracle.eval_stride(layers, w.x, windows=(sh * si[:nprobe], sw * sj[:nprobe]))
     probe_s = time.perf_counter() - t
     n = int(max(nprobe, min(4096, target_s / max(probe_s, 1e-6) * nprobe)))
     if n > len(si):
         reps = -(-n // max(1, len(si))) + 1
-        si, sj = wl.sample_windows(g["out_h"], g["out_w"], g["K_h"], g["K_w"], per_phase=reps, seed=1)
+        si, sj = wl.sample_windows(g["out_h"], g["out_w"], Gh, Gw, per_phase=reps, seed=1)
     n = min(n, len(si))
     si, sj = si[:n], sj[:n]
     log("cpu baseline: %d windows on %d threads (probe %.2fs for %d)" % (n, threads, probe_s, nprobe))
     t = time.perf_counter()
-    ref = oracle.eval_stride(layers, w.x, windows=(si, sj))
+    ref = oracle.eval_stride(layers, w.x, windows=(sh * si, sw * sj))
     cpu_s = time.perf_counter() - t
     got = out[:, si, sj].T.cpu().numpy().astype(np.float64) if hasattr(out, "cpu") else out
     err = float(np.abs(got - ref).max() / max(np.abs(ref).max(), 1e-300))
@@ -236,7 +259,9 @@ def cpu_baseline(w, g, out, target_s):
     windows = g["out_h"] * g["out_w"]
     base = {"value": n / cpu_s, "unit": "windows/s", "cores": threads, "kind": "oracle",
             "sample": "%d seeded windows of the %dx%d frame covering every fragment phase (i mod %d, j mod %d) "
-                      "plus corners and edge midpoints; fp64 EvalStride per window" % (n, H, W, g["K_h"], g["K_w"]),
+                      "plus corners and edge midpoints%s; fp64 EvalStride per window"
+                      % (n, H, W, Gh, Gw, "" if sh == sw == 1 else
+                         " of the output grid (window spacing %dx%d)" % (sh, sw)),
             "seconds": cpu_s, "extrapolated_full_frame_s": windows * cpu_s / n}
     tol = 2e-2 if w.dtype == "bf16" else 1e-4
     spot = {"windows": n, "max_abs_err_over_max_abs_oracle": err, "tolerance": tol, "pass": err <= tol}

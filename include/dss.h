@@ -86,54 +86,74 @@ typedef struct dss_layer {
 } dss_layer;
 
 /* Geometry of a network applied to an H x W signal (Lemma "processing chain"
- * (a)-(c), Sect. 4.2; stuffing count of Theorem "processing chain", Sect. 4.3). */
+ * (a)-(c), Sect. 4.2; stuffing count of Theorem "processing chain", Sect. 4.3),
+ * or, for a mixed level ell > 0, of the relaxed/mixed evaluation (appendix:
+ * Definition "evalrelaxslide", Lemma "evalrelaxslide", and the operating modes
+ * of Theorem "evalrelaxslide"; ell = L is the relaxed evaluation of Definition
+ * "evalrelax").  Per axis with N samples, r = rem(N - B + k*_ell, k*_L): if
+ * r < k*_ell the last r samples are trimmed first (trimming mode), otherwise
+ * k*_L - r dummy samples are stuffed (stuffing mode).  ell = 0 is the dense
+ * evaluation: nothing is ever trimmed and the stuffing count is that of
+ * Theorem "processing chain". */
 typedef struct dss_geometry {
     int32_t ndim;           /* 1 or 2 */
     int32_t in_c, out_c;    /* input channels, output channels of the last layer */
     int32_t n_chain;        /* L: number of processing-chain layers */
     int32_t B_h, B_w;       /* receptive field per axis */
     int32_t K_h, K_w;       /* final stride product k*_L per axis */
-    int32_t r_h, r_w;       /* dummy samples stuffed at the end of each axis */
-    int32_t D_h, D_w;       /* stuffed extents H + r_h, W + r_w */
-    int32_t out_h, out_w;   /* dense output extents H - B_h + 1, W - B_w + 1 */
+    int32_t r_h, r_w;       /* dummy samples stuffed at the end of each axis (stuffing mode) */
+    int32_t D_h, D_w;       /* extents the chain runs on: H - trim_h + r_h, W - trim_w + r_w */
+    int32_t out_h, out_w;   /* output extents ceil((H - B_h + 1) / step_h), ceil((W - B_w + 1) / step_w);
+                               for ell = 0 the dense extents H - B_h + 1, W - B_w + 1 */
     int32_t dtype;          /* dss_dtype of the plan (geometry queries: the dtype passed) */
-    int32_t reserved;
-    int64_t workspace_bytes;/* device scratch that dss_eval_dense / dss_eval_slide need */
-    double conv_flops;      /* algorithmic convolution flops of one dense evaluation
+    int32_t ell;            /* mixed level: chain layers 1..ell run relaxed (strided pooling) */
+    int32_t step_h, step_w; /* output sample spacing k*_ell per axis (1 for ell = 0) */
+    int32_t trim_h, trim_w; /* samples removed from the end of each axis first (trimming mode) */
+    int64_t workspace_bytes;/* device scratch that the evaluation entry points need */
+    double conv_flops;      /* algorithmic convolution flops of one evaluation
                                (2 per multiply-add, only the samples the method needs) */
-    double pool_bytes;      /* algorithmic bytes of the sliding max-pool + Frag steps
-                               (each tensor read once, written once, at its stored width) */
+    double pool_bytes;      /* algorithmic bytes of the pooling steps (sliding max-pool + Frag,
+                               or strided max-pool for relaxed layers; each tensor read once,
+                               written once, at its stored width) */
     double total_bytes;     /* algorithmic bytes of every step (stuff, convs, pools, defrag) */
 } dss_geometry;
 
-/* Per-layer geometry for chain layer j (1-based, 1..L), or j = 0 for the stuffed input. */
+/* Per-layer geometry for chain layer j (1-based, 1..L), or j = 0 for the
+ * trimmed/stuffed input, at a mixed level ell (0 = dense). */
 typedef struct dss_layer_geometry {
     int32_t c_h, c_w;       /* dimensionality reduction constant of T_j per axis (1 for identity) */
     int32_t k_h, k_w;       /* pool size k_j per axis (1 when the layer has no pool) */
     int32_t kstar_h, kstar_w;/* stride products k*_j */
     int32_t u_h, u_w;       /* strided extent u_j (Lemma (a)) */
-    int32_t U_h, U_w;       /* fragment extent U_j^row per axis (Lemma (b)) */
-    int32_t F;              /* number of fragments k*_j,h * k*_j,w (U_j^col for both axes) */
+    int32_t U_h, U_w;       /* per-fragment extent after layer j: U_j^row per axis (Lemma (b)) for a
+                               sliding layer, W_j (Lemma "evalrelax" (b)) for a relaxed one */
+    int32_t F;              /* number of fragments: (k*_j,h / k*_ell,h) * (k*_j,w / k*_ell,w)
+                               for a sliding layer (U_j^col, Lemma "evalrelaxslide" (b)), 1 for a
+                               relaxed layer and for j = 0 */
     int32_t channels;       /* feature maps after layer j */
     int32_t has_conv, has_pool;
+    int32_t relaxed;        /* 1 if 1 <= j <= ell: the layer pools with stride k_j, no Frag */
+    int32_t reserved;
 } dss_layer_geometry;
 
 typedef struct dss_plan* dss_plan_t;
 
 /* ---------------------------------------------------------------- geometry (host only) */
 
-/* Geometry of `layers` on an H x W signal with `in_channels` channels, without a
- * plan and without touching the GPU.  `dtype` only affects workspace_bytes and
- * the byte counts.  DSS_E_SHAPE if H < B_h or W < B_w (the transformation is
- * defined only for signals at least as large as the receptive field). */
+/* Geometry of `layers` on an H x W signal with `in_channels` channels at mixed
+ * level `ell` (0 = dense evaluation, 0..L), without a plan and without touching
+ * the GPU.  `dtype` only affects workspace_bytes and the byte counts.
+ * DSS_E_SHAPE if H < B_h or W < B_w (the transformation is defined only for
+ * signals at least as large as the receptive field); DSS_E_INVALID if ell is
+ * outside 0..L. */
 dss_status dss_chain_geometry(const dss_layer* layers, int32_t n_layers, int32_t ndim,
                               int32_t in_channels, dss_dtype dtype, int32_t H, int32_t W,
-                              dss_geometry* out);
+                              int32_t ell, dss_geometry* out);
 
 /* Same for chain layer j (0..L). */
 dss_status dss_chain_layer_geometry(const dss_layer* layers, int32_t n_layers, int32_t ndim,
-                                    int32_t in_channels, int32_t H, int32_t W, int32_t j,
-                                    dss_layer_geometry* out);
+                                    int32_t in_channels, int32_t H, int32_t W, int32_t ell,
+                                    int32_t j, dss_layer_geometry* out);
 
 /* ---------------------------------------------------------------- plans */
 
@@ -151,8 +171,9 @@ dss_status dss_plan_create(const dss_layer* layers, int32_t n_layers, int32_t nd
  * evaluation that is still running on the plan. */
 void dss_plan_destroy(dss_plan_t plan);
 
-dss_status dss_plan_geometry(dss_plan_t plan, int32_t H, int32_t W, dss_geometry* out);
-dss_status dss_plan_layer_geometry(dss_plan_t plan, int32_t H, int32_t W, int32_t j,
+/* The geometries above for the plan's network (and dtype). */
+dss_status dss_plan_geometry(dss_plan_t plan, int32_t H, int32_t W, int32_t ell, dss_geometry* out);
+dss_status dss_plan_layer_geometry(dss_plan_t plan, int32_t H, int32_t W, int32_t ell, int32_t j,
                                    dss_layer_geometry* out);
 
 /* ---------------------------------------------------------------- evaluation */
@@ -173,16 +194,43 @@ dss_status dss_plan_layer_geometry(dss_plan_t plan, int32_t H, int32_t W, int32_
 dss_status dss_eval_dense(dss_plan_t plan, const void* signal, int32_t H, int32_t W, float* out,
                           void* workspace, int64_t workspace_bytes, hipStream_t stream);
 
-/* The intermediate representation EvalSlide_j(Stuff(signal)) after chain layer j
- * (0 <= j <= L; j = 0 gives the stuffed signal), as binary32 in the fragment
- * layout [F_j][C_j][U_j,h][U_j,w] (fragment index linearised as for dss_frag).
- * By Lemma "processing chain" (d), sample (y, x) of fragment
- * (i mod k*_j,h) * k*_j,w + (w mod k*_j,w) holds, for y = i div k*_j,h + mu_h and
- * x = w div k*_j,w + mu_w, sample (mu_h, mu_w) of the strided network's
- * layer-j output on the window at (i, w).  Same arguments and errors as
- * dss_eval_dense; `out` must hold F_j * C_j * U_h * U_w floats. */
-dss_status dss_eval_slide(dss_plan_t plan, const void* signal, int32_t H, int32_t W, int32_t j,
+/* Mixed evaluation (appendix: Theorem "evalrelaxslide"; for ell = L Theorem
+ * "evalrelax"): chain layers 1..ell are applied in the relaxed fashion (the
+ * convolution on the whole signal, then max-pooling with stride k_j and no
+ * fragmentation), layers ell+1..L in the sliding fashion with fragmentation,
+ * after per-axis trimming or stuffing as described at dss_geometry; the output is
+ * defragmented with k*_L / k*_ell and the superfluous samples of the stuffing
+ * mode are trimmed.  The result equals dense scanning downsampled by the
+ * intermediate stride product: Down_{k*_ell}(Slide_{EvalStride_L}(signal)).
+ *   signal     device, [in_c][H][W] in the plan's dtype
+ *   ell        mixed level, 0..L (0 gives exactly dss_eval_dense)
+ *   out        device, binary32 [out_c][out_h][out_w] with the extents of
+ *              dss_plan_geometry(plan, H, W, ell); out[c][i][j] is channel c of the
+ *              network's output on the window whose top-left sample is
+ *              (step_h * i, step_w * j)
+ *   workspace  device scratch of at least dss_geometry.workspace_bytes bytes for
+ *              this ell (256-byte aligned), owned by the caller
+ * Errors: as dss_eval_dense, and DSS_E_INVALID if ell is outside 0..L. */
+dss_status dss_eval_mixed(dss_plan_t plan, const void* signal, int32_t H, int32_t W, int32_t ell,
                           float* out, void* workspace, int64_t workspace_bytes, hipStream_t stream);
+
+/* The intermediate representation after chain layer j (0 <= j <= L; j = 0
+ * gives the trimmed/stuffed signal) of the evaluation at mixed level ell
+ * (ell = 0: EvalSlide_j(Stuff(signal)); ell > 0: EvalRelaxSlide^ell_j of the
+ * trimmed/stuffed signal), as binary32 in the fragment layout [F_j][C_j][U_j,h][U_j,w]
+ * (fragment index linearised as for dss_frag; F_j and U_j from
+ * dss_plan_layer_geometry).  For a sliding layer j > ell, Lemma "processing
+ * chain" (d) (ell = 0) and Lemma "evalrelaxslide" (d) say: with G = k*_j / k*_ell
+ * per axis, sample (y, x) of fragment (i mod G_h) * G_w + (w mod G_w) holds, for
+ * y = i div G_h + mu_h and x = w div G_w + mu_w, sample (mu_h, mu_w) of the
+ * strided network's layer-j output on the window at (k*_ell,h * i, k*_ell,w * w).
+ * For a relaxed layer j <= ell (one fragment), Lemma "evalrelaxslide" (c): the
+ * u_j-sized block at (i, w) is the layer-j output on the window at
+ * (k*_j,h * i, k*_j,w * w).  Same arguments and errors as dss_eval_mixed; `out`
+ * must hold F_j * C_j * U_h * U_w floats. */
+dss_status dss_eval_slide(dss_plan_t plan, const void* signal, int32_t H, int32_t W, int32_t ell,
+                          int32_t j, float* out, void* workspace, int64_t workspace_bytes,
+                          hipStream_t stream);
 
 /* ---------------------------------------------------------------- Frag / Defrag */
 

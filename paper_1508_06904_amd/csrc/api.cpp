@@ -4,9 +4,14 @@
 //
 // Dense evaluation (Theorem "processing chain", Sect. 4.3):
 //   Stuff_r  ->  for j = 1..L: [conv T_j]  [sliding max-pool + Frag_{k_j}]  ->  Defrag_{k*_L} + Trim_r
+// Mixed evaluation at level ell (appendix, Theorem "evalrelaxslide"):
+//   Trim or Stuff  ->  for j <= ell: [conv T_j] [max-pool with stride k_j]
+//                  ->  for j > ell:  [conv T_j] [sliding max-pool + Frag_{k_j}]
+//                  ->  Defrag_{k*_L / k*_ell} + trim to the output extent
 // Every intermediate stays in one of two ping-pong halves of the caller's
 // workspace, in the channels-last fragment layout [F][h][w][C] (fragment index
 // linearised row-major over (row fragment, column fragment)).
+#include <algorithm>
 #include <cstdarg>
 #include <cstdio>
 #include <cstdlib>
@@ -110,6 +115,11 @@ static void fill_geometry(const Chain& ch, const Geom& G, dss_dtype dt, dss_geom
     out->out_h = G.out_h;
     out->out_w = G.out_w;
     out->dtype = dt;
+    out->ell = G.ell;
+    out->step_h = G.step_h;
+    out->step_w = G.step_w;
+    out->trim_h = G.trim_h;
+    out->trim_w = G.trim_w;
     out->workspace_bytes = G.ws_bytes;
     out->conv_flops = G.conv_flops;
     out->pool_bytes = G.pool_bytes;
@@ -123,69 +133,72 @@ static dss_status fill_layer_geometry(const Chain& ch, const Geom& G, int j, dss
     out->kstar_w = ch.kstar_w[j];
     out->u_h = ch.u_h[j];
     out->u_w = ch.u_w[j];
-    out->F = ch.kstar_h[j] * ch.kstar_w[j];
     if (j == 0) {
         out->c_h = out->c_w = out->k_h = out->k_w = 1;
         out->U_h = G.D_h;
         out->U_w = G.D_w;
+        out->F = 1;
         out->channels = ch.in_c;
         return DSS_OK;
     }
     const ChainLayer& c = ch.layers[j - 1];
+    const LayerGeom& lg = G.L[j - 1];
     out->c_h = c.c_h;
     out->c_w = c.c_w;
     out->k_h = c.k_h;
     out->k_w = c.k_w;
-    out->U_h = G.L[j - 1].U_h;
-    out->U_w = G.L[j - 1].U_w;
+    out->U_h = lg.U_h;
+    out->U_w = lg.U_w;
+    out->F = lg.Fout_h * lg.Fout_w;
     out->channels = c.cout;
     out->has_conv = c.has_conv;
     out->has_pool = c.has_pool;
+    out->relaxed = lg.relaxed;
     return DSS_OK;
 }
 
 extern "C" dss_status dss_chain_geometry(const dss_layer* layers, int32_t n_layers, int32_t ndim,
                                          int32_t in_channels, dss_dtype dtype, int32_t H, int32_t W,
-                                         dss_geometry* out) {
+                                         int32_t ell, dss_geometry* out) {
     if (!out) return fail(DSS_E_INVALID, "NULL output");
     if (dtype != DSS_F32 && dtype != DSS_BF16) return fail(DSS_E_UNSUPPORTED, "unknown dtype %d", dtype);
     Chain ch;
     dss_status s = build_chain(layers, n_layers, ndim, in_channels, &ch);
     if (s != DSS_OK) return s;
     Geom G;
-    s = compute_geometry(ch, dtype, H, W, &G);
+    s = compute_geometry(ch, dtype, H, W, ell, &G);
     if (s != DSS_OK) return s;
     fill_geometry(ch, G, dtype, out);
     return DSS_OK;
 }
 
 extern "C" dss_status dss_chain_layer_geometry(const dss_layer* layers, int32_t n_layers, int32_t ndim,
-                                               int32_t in_channels, int32_t H, int32_t W, int32_t j,
+                                               int32_t in_channels, int32_t H, int32_t W, int32_t ell, int32_t j,
                                                dss_layer_geometry* out) {
     if (!out) return fail(DSS_E_INVALID, "NULL output");
     Chain ch;
     dss_status s = build_chain(layers, n_layers, ndim, in_channels, &ch);
     if (s != DSS_OK) return s;
     Geom G;
-    s = compute_geometry(ch, DSS_F32, H, W, &G);
+    s = compute_geometry(ch, DSS_F32, H, W, ell, &G);
     if (s != DSS_OK) return s;
     return fill_layer_geometry(ch, G, j, out);
 }
 
-extern "C" dss_status dss_plan_geometry(dss_plan_t plan, int32_t H, int32_t W, dss_geometry* out) {
+extern "C" dss_status dss_plan_geometry(dss_plan_t plan, int32_t H, int32_t W, int32_t ell, dss_geometry* out) {
     if (!plan || !out) return fail(DSS_E_INVALID, "NULL plan or output");
     Geom G;
-    dss_status s = compute_geometry(plan->chain, plan->dtype, H, W, &G);
+    dss_status s = compute_geometry(plan->chain, plan->dtype, H, W, ell, &G);
     if (s != DSS_OK) return s;
     fill_geometry(plan->chain, G, plan->dtype, out);
     return DSS_OK;
 }
 
-extern "C" dss_status dss_plan_layer_geometry(dss_plan_t plan, int32_t H, int32_t W, int32_t j,
+extern "C" dss_status dss_plan_layer_geometry(dss_plan_t plan, int32_t H, int32_t W, int32_t ell, int32_t j,
                                               dss_layer_geometry* out) {
     if (!plan || !out) return fail(DSS_E_INVALID, "NULL plan or output");
     Geom G;
-    dss_status s = compute_geometry(plan->chain, plan->dtype, H, W, &G);
+    dss_status s = compute_geometry(plan->chain, plan->dtype, H, W, ell, &G);
     if (s != DSS_OK) return s;
     return fill_layer_geometry(plan->chain, G, j, out);
 }
@@ -395,7 +408,8 @@ static dss_status run_chain(dss_plan* p, const Geom& G, const void* signal, int 
     int which = 0;
     const dss_dtype dt = p->dtype;
     const double es = (double)dtype_size(dt);
-    hipError_t e = T.run("stuff_pack", 0, 0.0, (double)ch.in_c * (G.H * (double)G.W + G.D_h * (double)G.D_w) * es,
+    const double in_read = (double)std::min(G.H, G.D_h) * std::min(G.W, G.D_w);
+    hipError_t e = T.run("stuff_pack", 0, 0.0, (double)ch.in_c * (in_read + G.D_h * (double)G.D_w) * es,
                          [&] { return launch_stuff_pack(dt, signal, ch.in_c, G.H, G.W, buf[0], G.D_h, G.D_w, stream); });
     if (e != hipSuccess) return hip_fail(e, "stuff_pack launch");
     void* cur = buf[0];
@@ -425,7 +439,16 @@ static dss_status run_chain(dss_plan* p, const Geom& G, const void* signal, int 
             cur = dst;
             cdt = tout;
         }
-        if (c.has_pool) {
+        if (c.has_pool && lg.relaxed) {
+            void* dst = buf[which ^ 1];
+            const double bytes = ((double)lg.E_h * lg.E_w + (double)lg.U_h * lg.U_w) * c.cout * dtype_size(cdt);
+            e = T.run("pool_stride", j, 0.0, bytes, [&] {
+                return launch_pool_stride(cdt, cur, lg.E_h, lg.E_w, c.cout, c.k_h, c.k_w, dst, stream);
+            });
+            if (e != hipSuccess) return hip_fail(e, "pool_stride launch");
+            which ^= 1;
+            cur = dst;
+        } else if (c.has_pool) {
             void* dst = buf[which ^ 1];
             const double bytes = ((double)Fin * lg.E_h * lg.E_w + (double)lg.Fout_h * lg.Fout_w * lg.U_h * lg.U_w) *
                                  c.cout * dtype_size(cdt);
@@ -443,9 +466,9 @@ static dss_status run_chain(dss_plan* p, const Geom& G, const void* signal, int 
 }
 
 static dss_status check_eval_args(dss_plan_t plan, const void* signal, const void* out, void* workspace,
-                                  int64_t workspace_bytes, int32_t H, int32_t W, Geom* G) {
+                                  int64_t workspace_bytes, int32_t H, int32_t W, int32_t ell, Geom* G) {
     if (!plan || !signal || !out) return fail(DSS_E_INVALID, "NULL plan, signal or out");
-    dss_status s = compute_geometry(plan->chain, plan->dtype, H, W, G);
+    dss_status s = compute_geometry(plan->chain, plan->dtype, H, W, ell, G);
     if (s != DSS_OK) return s;
     if (!workspace) return fail(DSS_E_INVALID, "NULL workspace (need %lld bytes)", (long long)G->ws_bytes);
     if (workspace_bytes < G->ws_bytes)
@@ -460,10 +483,10 @@ static dss_status check_eval_args(dss_plan_t plan, const void* signal, const voi
     return DSS_OK;
 }
 
-extern "C" dss_status dss_eval_dense(dss_plan_t plan, const void* signal, int32_t H, int32_t W, float* out,
-                                     void* workspace, int64_t workspace_bytes, hipStream_t stream) {
+extern "C" dss_status dss_eval_mixed(dss_plan_t plan, const void* signal, int32_t H, int32_t W, int32_t ell,
+                                     float* out, void* workspace, int64_t workspace_bytes, hipStream_t stream) {
     Geom G;
-    dss_status s = check_eval_args(plan, signal, out, workspace, workspace_bytes, H, W, &G);
+    dss_status s = check_eval_args(plan, signal, out, workspace, workspace_bytes, H, W, ell, &G);
     if (s != DSS_OK) return s;
     Timer T(plan, stream);
     void* cur = nullptr;
@@ -471,20 +494,29 @@ extern "C" dss_status dss_eval_dense(dss_plan_t plan, const void* signal, int32_
     s = run_chain(plan, G, signal, plan->chain.L(), (char*)workspace, stream, T, &cur, &cdt);
     if (s != DSS_OK) return s;
     const Chain& ch = plan->chain;
-    const double bytes = (double)ch.K_h() * ch.K_w() * G.L.back().U_h * G.L.back().U_w * ch.out_c() * dtype_size(cdt) +
+    // Defrag_{k*_L / k*_ell}, then keep the first out_h x out_w samples (this is
+    // Trim_r of the dense evaluation and the final trimming of the stuffing mode)
+    const int Gh = ch.K_h() / G.step_h, Gw = ch.K_w() / G.step_w;
+    const int Uh = G.L.back().U_h, Uw = G.L.back().U_w;
+    const double bytes = (double)Gh * Gw * Uh * Uw * ch.out_c() * dtype_size(cdt) +
                          (double)G.out_h * G.out_w * ch.out_c() * 4.0;
     hipError_t e = T.run("defrag_trim", ch.L() + 1, 0.0, bytes, [&] {
-        return launch_defrag_trim(cdt, cur, ch.K_h(), ch.K_w(), G.L.back().U_h, G.L.back().U_w, ch.out_c(), out,
-                                  G.out_h, G.out_w, stream);
+        return launch_defrag_trim(cdt, cur, Gh, Gw, Uh, Uw, ch.out_c(), out, G.out_h, G.out_w, stream);
     });
     if (e != hipSuccess) return hip_fail(e, "defrag_trim launch");
     return DSS_OK;
 }
 
-extern "C" dss_status dss_eval_slide(dss_plan_t plan, const void* signal, int32_t H, int32_t W, int32_t j,
-                                     float* out, void* workspace, int64_t workspace_bytes, hipStream_t stream) {
+extern "C" dss_status dss_eval_dense(dss_plan_t plan, const void* signal, int32_t H, int32_t W, float* out,
+                                     void* workspace, int64_t workspace_bytes, hipStream_t stream) {
+    return dss_eval_mixed(plan, signal, H, W, 0, out, workspace, workspace_bytes, stream);
+}
+
+extern "C" dss_status dss_eval_slide(dss_plan_t plan, const void* signal, int32_t H, int32_t W, int32_t ell,
+                                     int32_t j, float* out, void* workspace, int64_t workspace_bytes,
+                                     hipStream_t stream) {
     Geom G;
-    dss_status s = check_eval_args(plan, signal, out, workspace, workspace_bytes, H, W, &G);
+    dss_status s = check_eval_args(plan, signal, out, workspace, workspace_bytes, H, W, ell, &G);
     if (s != DSS_OK) return s;
     if (j < 0 || j > plan->chain.L()) return fail(DSS_E_INVALID, "chain layer %d out of range 0..%d", j, plan->chain.L());
     Timer T(plan, stream);
@@ -493,7 +525,7 @@ extern "C" dss_status dss_eval_slide(dss_plan_t plan, const void* signal, int32_
     s = run_chain(plan, G, signal, j, (char*)workspace, stream, T, &cur, &cdt);
     if (s != DSS_OK) return s;
     const Chain& ch = plan->chain;
-    const int F = ch.kstar_h[j] * ch.kstar_w[j];
+    const int F = j == 0 ? 1 : G.L[j - 1].Fout_h * G.L[j - 1].Fout_w;
     const int h = j == 0 ? G.D_h : G.L[j - 1].U_h;
     const int w = j == 0 ? G.D_w : G.L[j - 1].U_w;
     const int C = j == 0 ? ch.in_c : ch.layers[j - 1].cout;

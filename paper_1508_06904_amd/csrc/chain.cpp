@@ -9,11 +9,15 @@
 //    extents satisfy u_{j-1} - c_j + 1 = k_j u_j (Sect. 5.1), so
 //    B = u_0 and k*_j = k_1 ... k_j.
 //  * Stuffing count r = 0 if k*_L divides N - B + 1, else k*_L - rem(N - B + 1, k*_L)
-//    (Theorem "processing chain", Sect. 4.3), per axis.
+//    (Theorem "processing chain", Sect. 4.3), per axis.  At a mixed level
+//    ell > 0 the operating modes of Theorem "evalrelaxslide" (appendix) trim or
+//    stuff instead; ell = 0 is the case above.
 //  * Fragment extents of the sliding evaluation: U_0 = D = N + r, after T_j the
 //    extent is U_{j-1} - c_j + 1, after Slide_g it is one sample shorter per
 //    extra pooled sample, and Frag_k divides it by k (Lemma (b)); the fragment
-//    count per axis is k*_j.
+//    count per axis is k*_j (k*_j / k*_ell after ell relaxed layers, which keep
+//    one fragment and divide the extent by k_j: Lemma "evalrelax" (b)).
+#include <algorithm>
 #include <cstring>
 
 #include "dss_internal.h"
@@ -100,50 +104,76 @@ dss_status build_chain(const dss_layer* layers, int n, int ndim, int in_c, Chain
     return DSS_OK;
 }
 
-static int stuffing(int N, int B, int K) {
-    const int rem = (N - B + 1) % K;
-    return rem == 0 ? 0 : K - rem;
+// Operating mode per axis (Theorem "evalrelaxslide"; for k = 1 it reduces to the
+// stuffing of Theorem "processing chain", for k = K to the trimming of Theorem
+// "evalrelax"): r = rem(N - B + k, K) with k = k*_ell and K = k*_L; trim r
+// samples if r < k, else stuff K - r.
+static void operating_mode(int N, int B, int K, int k, int* trim, int* stuff) {
+    const int r = (int)(((int64_t)N - B + k) % K);
+    *trim = r < k ? r : 0;
+    *stuff = r < k ? 0 : K - r;
 }
 
-dss_status compute_geometry(const Chain& ch, dss_dtype dt, int H, int W, Geom* g) {
+dss_status compute_geometry(const Chain& ch, dss_dtype dt, int H, int W, int ell, Geom* g) {
     if (ch.ndim == 1 && H != 1) return fail(DSS_E_SHAPE, "1-D plan needs H = 1 (got %d)", H);
     if (H < ch.B_h || W < ch.B_w)
         return fail(DSS_E_SHAPE, "signal %dx%d is smaller than the receptive field %dx%d", H, W, ch.B_h, ch.B_w);
+    const int L = ch.L();
+    if (ell < 0 || ell > L) return fail(DSS_E_INVALID, "mixed level %d out of range 0..%d", ell, L);
     Geom G;
+    G.ell = ell;
+    G.step_h = ch.kstar_h[ell];
+    G.step_w = ch.kstar_w[ell];
     G.H = H;
     G.W = W;
-    G.r_h = stuffing(H, ch.B_h, ch.K_h());
-    G.r_w = stuffing(W, ch.B_w, ch.K_w());
-    G.D_h = H + G.r_h;
-    G.D_w = W + G.r_w;
-    G.out_h = H - ch.B_h + 1;
-    G.out_w = W - ch.B_w + 1;
+    operating_mode(H, ch.B_h, ch.K_h(), G.step_h, &G.trim_h, &G.r_h);
+    operating_mode(W, ch.B_w, ch.K_w(), G.step_w, &G.trim_w, &G.r_w);
+    G.D_h = H - G.trim_h + G.r_h;
+    G.D_w = W - G.trim_w + G.r_w;
+    G.out_h = (H - ch.B_h) / G.step_h + 1;   // ceil((H - B + 1) / k*_ell)
+    G.out_w = (W - ch.B_w) / G.step_w + 1;
+    // Lemma "evalrelaxslide": D = B + k*_L t - k*_ell with t >= 1
+    const int64_t th = ((int64_t)G.D_h - ch.B_h + G.step_h) / ch.K_h();
+    const int64_t tw = ((int64_t)G.D_w - ch.B_w + G.step_w) / ch.K_w();
+    if (th < 1 || tw < 1 || th * ch.K_h() != (int64_t)G.D_h - ch.B_h + G.step_h ||
+        tw * ch.K_w() != (int64_t)G.D_w - ch.B_w + G.step_w)
+        return fail(DSS_E_SHAPE, "trimmed/stuffed extents %dx%d violate the divisibility requirement", G.D_h, G.D_w);
     const double es = (double)dtype_size(dt);
-    const int L = ch.L();
 
     int Uh = G.D_h, Uw = G.D_w;
     int cur_c = ch.in_c;
     int64_t maxbuf = (int64_t)G.D_h * G.D_w * ch.in_c * (int64_t)es;
-    G.total_bytes = (double)ch.in_c * H * W * es + (double)ch.in_c * G.D_h * G.D_w * es;
+    G.total_bytes = (double)ch.in_c * std::min(H, G.D_h) * std::min(W, G.D_w) * es +
+                    (double)ch.in_c * G.D_h * G.D_w * es;
     for (int j = 1; j <= L; ++j) {
         const ChainLayer& c = ch.layers[j - 1];
         LayerGeom lg;
+        lg.relaxed = j <= ell;
         lg.Uin_h = Uh;
         lg.Uin_w = Uw;
-        lg.Fin_h = ch.kstar_h[j - 1];
-        lg.Fin_w = ch.kstar_w[j - 1];
-        lg.Fout_h = ch.kstar_h[j];
-        lg.Fout_w = ch.kstar_w[j];
+        lg.Fin_h = lg.relaxed ? 1 : ch.kstar_h[j - 1] / G.step_h;
+        lg.Fin_w = lg.relaxed ? 1 : ch.kstar_w[j - 1] / G.step_w;
+        lg.Fout_h = lg.relaxed ? 1 : ch.kstar_h[j] / G.step_h;
+        lg.Fout_w = lg.relaxed ? 1 : ch.kstar_w[j] / G.step_w;
         const int64_t Fin = (int64_t)lg.Fin_h * lg.Fin_w;
         lg.E_h = Uh - c.c_h + 1;
         lg.E_w = Uw - c.c_w + 1;
         if (lg.E_h < c.k_h || lg.E_w < c.k_w) return fail(DSS_E_SHAPE, "layer %d: extent underflow", j);
-        const int Ph = lg.E_h - c.k_h + 1, Pw = lg.E_w - c.k_w + 1;
-        if (Ph % c.k_h != 0 || Pw % c.k_w != 0)
-            return fail(DSS_E_SHAPE, "layer %d: sliding-pool extent %dx%d not divisible by %dx%d", j, Ph, Pw,
-                        c.k_h, c.k_w);
-        lg.U_h = Ph / c.k_h;
-        lg.U_w = Pw / c.k_w;
+        if (lg.relaxed) {
+            // Stride_g: non-overlapping blocks
+            if (lg.E_h % c.k_h != 0 || lg.E_w % c.k_w != 0)
+                return fail(DSS_E_SHAPE, "layer %d: relaxed extent %dx%d not divisible by %dx%d", j, lg.E_h, lg.E_w,
+                            c.k_h, c.k_w);
+            lg.U_h = lg.E_h / c.k_h;
+            lg.U_w = lg.E_w / c.k_w;
+        } else {
+            const int Ph = lg.E_h - c.k_h + 1, Pw = lg.E_w - c.k_w + 1;
+            if (Ph % c.k_h != 0 || Pw % c.k_w != 0)
+                return fail(DSS_E_SHAPE, "layer %d: sliding-pool extent %dx%d not divisible by %dx%d", j, Ph, Pw,
+                            c.k_h, c.k_w);
+            lg.U_h = Ph / c.k_h;
+            lg.U_w = Pw / c.k_w;
+        }
         // the final conv of a bfloat16 plan stores binary32
         const bool last_op = (j == L) && !c.has_pool;
         if (c.has_conv) {
@@ -162,26 +192,31 @@ dss_status compute_geometry(const Chain& ch, dss_dtype dt, int H, int W, Geom* g
             G.total_bytes += pb;
             maxbuf = std::max(maxbuf, Fout * lg.U_h * lg.U_w * c.cout * (int64_t)es);
         }
-        // Lemma (b): U_j = (D - k*_j + 1 - sum_{mu<=j} k*_{mu-1}(c_mu - 1)) / k*_j
-        int64_t sh = 0, sw = 0;
-        for (int mu = 1; mu <= j; ++mu) {
-            sh += (int64_t)ch.kstar_h[mu - 1] * (ch.layers[mu - 1].c_h - 1);
-            sw += (int64_t)ch.kstar_w[mu - 1] * (ch.layers[mu - 1].c_w - 1);
+        if (lg.relaxed) {
+            // Lemma "evalrelax" (b): W_j - u_j = (D - B) / k*_j
+            if ((int64_t)(lg.U_h - ch.u_h[j]) * ch.kstar_h[j] != (int64_t)G.D_h - ch.B_h ||
+                (int64_t)(lg.U_w - ch.u_w[j]) * ch.kstar_w[j] != (int64_t)G.D_w - ch.B_w)
+                return fail(DSS_E_SHAPE, "layer %d: relaxed extent disagrees with Lemma \"evalrelax\" (b)", j);
+        } else {
+            // Lemma "evalrelaxslide" (b) (Lemma "processing chain" (b) for ell = 0):
+            // U_j - u_j + 1 = (k*_L / k*_j) t
+            if ((int64_t)(lg.U_h - ch.u_h[j] + 1) * ch.kstar_h[j] != th * ch.K_h() ||
+                (int64_t)(lg.U_w - ch.u_w[j] + 1) * ch.kstar_w[j] != tw * ch.K_w())
+                return fail(DSS_E_SHAPE, "layer %d: fragment extent disagrees with Lemma (b)", j);
         }
-        if ((G.D_h - ch.kstar_h[j] + 1 - sh) != (int64_t)lg.U_h * ch.kstar_h[j] ||
-            (G.D_w - ch.kstar_w[j] + 1 - sw) != (int64_t)lg.U_w * ch.kstar_w[j])
-            return fail(DSS_E_SHAPE, "layer %d: fragment extent disagrees with Lemma (b)", j);
         G.L.push_back(lg);
         Uh = lg.U_h;
         Uw = lg.U_w;
         cur_c = c.cout;
     }
-    // Lemma (c) with u_L = 1: each of the k*_L fragments holds (D - B + 1)/k*_L outputs
-    if ((int64_t)Uh * ch.K_h() != (int64_t)G.D_h - ch.B_h + 1 || (int64_t)Uw * ch.K_w() != (int64_t)G.D_w - ch.B_w + 1)
-        return fail(DSS_E_SHAPE, "final fragment extent disagrees with Lemma (c)");
+    // After Defrag_{k*_L / k*_ell} there are (k*_L / k*_ell) t = (D - B)/k*_ell + 1
+    // samples per axis; the output keeps the first ceil((N - B + 1)/k*_ell).
+    const int Gh = ch.K_h() / G.step_h, Gw = ch.K_w() / G.step_w;
+    if ((int64_t)Uh * Gh < G.out_h || (int64_t)Uw * Gw < G.out_w)
+        return fail(DSS_E_SHAPE, "final fragment extent is smaller than the output");
     const bool last_f32 = dt == DSS_BF16 && !ch.layers.back().has_pool && ch.layers.back().has_conv;
     const double es_last = last_f32 ? 4.0 : es;
-    G.total_bytes += (double)ch.K_h() * ch.K_w() * Uh * Uw * cur_c * es_last + (double)G.out_h * G.out_w * cur_c * 4.0;
+    G.total_bytes += (double)Gh * Gw * Uh * Uw * cur_c * es_last + (double)G.out_h * G.out_w * cur_c * 4.0;
     G.buf_bytes = (maxbuf + 255) / 256 * 256;
     G.ws_bytes = 2 * G.buf_bytes;
     *g = std::move(G);

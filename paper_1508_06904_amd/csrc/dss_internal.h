@@ -46,16 +46,19 @@ struct Chain {
 
 dss_status build_chain(const dss_layer* layers, int n, int ndim, int in_c, Chain* out);
 
-// Geometry of one chain layer for a given stuffed signal.
+// Geometry of one chain layer for a given trimmed/stuffed signal.
 struct LayerGeom {
+    bool relaxed;       // j <= ell: Stride_g (pool with stride k, no Frag), one fragment
     int Uin_h, Uin_w;   // fragment extent entering the layer (U_{j-1})
     int E_h, E_w;       // extent after T_j (U_{j-1} - c_j + 1)
-    int U_h, U_w;       // extent after Slide_g + Frag (U_j)
-    int Fin_h, Fin_w;   // fragments entering (k*_{j-1})
-    int Fout_h, Fout_w; // fragments leaving (k*_j)
+    int U_h, U_w;       // extent after the pooling step (U_j, or W_j for a relaxed layer)
+    int Fin_h, Fin_w;   // fragments entering (k*_{j-1} / k*_ell, or 1)
+    int Fout_h, Fout_w; // fragments leaving (k*_j / k*_ell, or 1)
 };
 
 struct Geom {
+    int ell = 0, step_h = 1, step_w = 1;     // mixed level and output sample spacing k*_ell
+    int trim_h = 0, trim_w = 0;              // samples trimmed first (trimming mode)
     int H = 0, W = 0, r_h = 0, r_w = 0, D_h = 0, D_w = 0, out_h = 0, out_w = 0;
     std::vector<LayerGeom> L;
     int64_t buf_bytes = 0;      // one ping-pong buffer
@@ -64,7 +67,7 @@ struct Geom {
 };
 
 size_t dtype_size(dss_dtype dt);
-dss_status compute_geometry(const Chain& ch, dss_dtype dt, int H, int W, Geom* g);
+dss_status compute_geometry(const Chain& ch, dss_dtype dt, int H, int W, int ell, Geom* g);
 
 // ------------------------------------------------------------------ plan
 enum ConvImpl { CONV_DIRECT = 0, CONV_MFMA_F32 = 1, CONV_MFMA_BF16 = 2 };
@@ -111,6 +114,8 @@ hipError_t launch_conv_mfma_bf16(dss_dtype tout, const uint16_t* in, int F, int 
                                  const PlanConv& pc, void* out, hipStream_t s);
 hipError_t launch_pool_frag(dss_dtype dt, const void* in, int S_h, int S_w, int E_h, int E_w, int C,
                             int k_h, int k_w, void* out, hipStream_t s);
+hipError_t launch_pool_stride(dss_dtype dt, const void* in, int E_h, int E_w, int C, int k_h, int k_w,
+                              void* out, hipStream_t s);
 hipError_t launch_defrag_trim(dss_dtype dt, const void* in, int K_h, int K_w, int U_h, int U_w, int C,
                               float* out, int O_h, int O_w, hipStream_t s);
 hipError_t launch_to_planar(dss_dtype dt, const void* in, int F, int h, int w, int C, float* out,

@@ -13,6 +13,10 @@
 //               direct one.  Per axis, sliding-pool sample m*k + a of input
 //               fragment b lands at sample m of output fragment a*S + b
 //               (Lemma "frag-ops", Sect. 4.1).
+//  pool_stride  Stride_{g_max} of a relaxed layer (Definition "evalrelax",
+//               appendix): the maximum over non-overlapping k_h x k_w blocks of
+//               one channels-last signal, no fragmentation.  Every input sample
+//               is read exactly once.
 //  defrag_trim  Defrag_{k*_L} and Trim_r (appendix lemma on the simplified
 //               defragmentation; Definition "stuff-trim"): dense output sample
 //               (i, j) is sample (i div K_h, j div K_w) of fragment
@@ -180,6 +184,57 @@ hipError_t launch_pool_frag(dss_dtype dt, const void* in, int S_h, int S_w, int 
     } else {
         if (C % 4 == 0) run_pool<float, 4>(in, S_h, S_w, E_h, E_w, C, k_h, k_w, out, s);
         else run_pool<float, 1>(in, S_h, S_w, E_h, E_w, C, k_h, k_w, out, s);
+    }
+    return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ pool_stride
+// One thread per (output position, group of V channels); consecutive threads
+// take consecutive channel groups, then consecutive output columns.
+template <typename T, int V>
+__global__ __launch_bounds__(kThreads) void pool_stride_kernel(const T* __restrict__ in, int E_w, int C, int k_h,
+                                                              int k_w, T* __restrict__ out, int U_h, int U_w) {
+    const int CV = C / V;
+    const int64_t total = (int64_t)U_h * U_w * CV;
+    const int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (idx >= total) return;
+    const int cv = (int)(idx % CV);
+    const int64_t t = idx / CV;
+    const int x = (int)(t % U_w);
+    const int y = (int)(t / U_w);
+    const T* src = in + ((int64_t)y * k_h * E_w + (int64_t)x * k_w) * C + cv * V;
+    float m[V];
+    VecIO<T, V>::load(src, m);
+    for (int dy = 0; dy < k_h; ++dy) {
+        for (int dx = 0; dx < k_w; ++dx) {
+            if ((dy | dx) == 0) continue;
+            float v[V];
+            VecIO<T, V>::load(src + ((int64_t)dy * E_w + dx) * C, v);
+#pragma unroll
+            for (int e = 0; e < V; ++e) m[e] = fmaxf(m[e], v[e]);
+        }
+    }
+    VecIO<T, V>::store(out + t * C + cv * V, m);
+}
+
+template <typename T, int V>
+static void run_pool_stride(const void* in, int E_h, int E_w, int C, int k_h, int k_w, void* out, hipStream_t s) {
+    const int U_h = E_h / k_h, U_w = E_w / k_w;
+    const int64_t total = (int64_t)U_h * U_w * (C / V);
+    if (total == 0) return;
+    pool_stride_kernel<T, V><<<dim3((unsigned)ceil_div64(total, kThreads)), kThreads, 0, s>>>(
+        (const T*)in, E_w, C, k_h, k_w, (T*)out, U_h, U_w);
+}
+
+hipError_t launch_pool_stride(dss_dtype dt, const void* in, int E_h, int E_w, int C, int k_h, int k_w, void* out,
+                              hipStream_t s) {
+    if (dt == DSS_BF16) {
+        if (C % 8 == 0) run_pool_stride<uint16_t, 8>(in, E_h, E_w, C, k_h, k_w, out, s);
+        else if (C % 4 == 0) run_pool_stride<uint16_t, 4>(in, E_h, E_w, C, k_h, k_w, out, s);
+        else run_pool_stride<uint16_t, 1>(in, E_h, E_w, C, k_h, k_w, out, s);
+    } else {
+        if (C % 4 == 0) run_pool_stride<float, 4>(in, E_h, E_w, C, k_h, k_w, out, s);
+        else run_pool_stride<float, 1>(in, E_h, E_w, C, k_h, k_w, out, s);
     }
     return hipGetLastError();
 }

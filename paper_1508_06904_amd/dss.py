@@ -43,21 +43,21 @@ class Layer(ctypes.Structure):
 class Geometry(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in
                 ("ndim", "in_c", "out_c", "n_chain", "B_h", "B_w", "K_h", "K_w", "r_h", "r_w",
-                 "D_h", "D_w", "out_h", "out_w", "dtype", "reserved")] + \
+                 "D_h", "D_w", "out_h", "out_w", "dtype", "ell", "step_h", "step_w", "trim_h", "trim_w")] + \
                [("workspace_bytes", ctypes.c_int64), ("conv_flops", ctypes.c_double),
                 ("pool_bytes", ctypes.c_double), ("total_bytes", ctypes.c_double)]
 
     def as_dict(self):
-        return {n: getattr(self, n) for n, _ in self._fields_ if n != "reserved"}
+        return {n: getattr(self, n) for n, _ in self._fields_}
 
 
 class LayerGeometry(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in
                 ("c_h", "c_w", "k_h", "k_w", "kstar_h", "kstar_w", "u_h", "u_w", "U_h", "U_w", "F",
-                 "channels", "has_conv", "has_pool")]
+                 "channels", "has_conv", "has_pool", "relaxed", "reserved")]
 
     def as_dict(self):
-        return {n: getattr(self, n) for n, _ in self._fields_}
+        return {n: getattr(self, n) for n, _ in self._fields_ if n != "reserved"}
 
 
 class LaunchRecord(ctypes.Structure):
@@ -66,9 +66,9 @@ class LaunchRecord(ctypes.Structure):
 
 
 EXPORTS = ("dss_chain_geometry", "dss_chain_layer_geometry", "dss_plan_create", "dss_plan_destroy",
-           "dss_plan_geometry", "dss_plan_layer_geometry", "dss_eval_dense", "dss_eval_slide", "dss_frag",
-           "dss_defrag", "dss_plan_set_timing", "dss_plan_timings", "dss_status_string", "dss_last_error",
-           "dss_version")
+           "dss_plan_geometry", "dss_plan_layer_geometry", "dss_eval_dense", "dss_eval_mixed", "dss_eval_slide",
+           "dss_frag", "dss_defrag", "dss_plan_set_timing", "dss_plan_timings", "dss_status_string",
+           "dss_last_error", "dss_version")
 
 _lib = None
 
@@ -81,15 +81,16 @@ def lib():
             raise DssError(-1, "loading libdss.so", "%s does not exist; run __graft_entry__.build()" % LIB_PATH)
         L = ctypes.CDLL(LIB_PATH)
         P, I32, I64, VP = ctypes.POINTER, ctypes.c_int32, ctypes.c_int64, ctypes.c_void_p
-        L.dss_chain_geometry.argtypes = [P(Layer), I32, I32, I32, I32, I32, I32, P(Geometry)]
-        L.dss_chain_layer_geometry.argtypes = [P(Layer), I32, I32, I32, I32, I32, I32, P(LayerGeometry)]
+        L.dss_chain_geometry.argtypes = [P(Layer), I32, I32, I32, I32, I32, I32, I32, P(Geometry)]
+        L.dss_chain_layer_geometry.argtypes = [P(Layer), I32, I32, I32, I32, I32, I32, I32, P(LayerGeometry)]
         L.dss_plan_create.argtypes = [P(Layer), I32, I32, I32, I32, P(VP)]
         L.dss_plan_destroy.argtypes = [VP]
         L.dss_plan_destroy.restype = None
-        L.dss_plan_geometry.argtypes = [VP, I32, I32, P(Geometry)]
-        L.dss_plan_layer_geometry.argtypes = [VP, I32, I32, I32, P(LayerGeometry)]
+        L.dss_plan_geometry.argtypes = [VP, I32, I32, I32, P(Geometry)]
+        L.dss_plan_layer_geometry.argtypes = [VP, I32, I32, I32, I32, P(LayerGeometry)]
         L.dss_eval_dense.argtypes = [VP, VP, I32, I32, VP, VP, I64, VP]
-        L.dss_eval_slide.argtypes = [VP, VP, I32, I32, I32, VP, VP, I64, VP]
+        L.dss_eval_mixed.argtypes = [VP, VP, I32, I32, I32, VP, VP, I64, VP]
+        L.dss_eval_slide.argtypes = [VP, VP, I32, I32, I32, I32, VP, VP, I64, VP]
         L.dss_frag.argtypes = [I32, I32, I32, I32, I32, I32, I32, I32, VP, VP, VP]
         L.dss_defrag.argtypes = [I32, I32, I32, I32, I32, I32, I32, I32, VP, VP, VP]
         L.dss_plan_set_timing.argtypes = [VP, I32]
@@ -101,8 +102,8 @@ def lib():
         L.dss_version.argtypes = []
         L.dss_version.restype = ctypes.c_char_p
         for name in ("dss_chain_geometry", "dss_chain_layer_geometry", "dss_plan_create", "dss_plan_geometry",
-                     "dss_plan_layer_geometry", "dss_eval_dense", "dss_eval_slide", "dss_frag", "dss_defrag",
-                     "dss_plan_set_timing", "dss_plan_timings"):
+                     "dss_plan_layer_geometry", "dss_eval_dense", "dss_eval_mixed", "dss_eval_slide", "dss_frag",
+                     "dss_defrag", "dss_plan_set_timing", "dss_plan_timings"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -135,18 +136,18 @@ class _LayerArray:
         self.n = len(layers)
 
 
-def chain_geometry(layers, ndim, in_channels, H, W, dtype="f32"):
+def chain_geometry(layers, ndim, in_channels, H, W, dtype="f32", ell=0):
     la = _LayerArray(layers)
     g = Geometry()
-    _check(lib().dss_chain_geometry(la.arr, la.n, ndim, in_channels, DTYPES[dtype], H, W, ctypes.byref(g)),
+    _check(lib().dss_chain_geometry(la.arr, la.n, ndim, in_channels, DTYPES[dtype], H, W, ell, ctypes.byref(g)),
            "dss_chain_geometry")
     return g.as_dict()
 
 
-def chain_layer_geometry(layers, ndim, in_channels, H, W, j):
+def chain_layer_geometry(layers, ndim, in_channels, H, W, j, ell=0):
     la = _LayerArray(layers)
     g = LayerGeometry()
-    _check(lib().dss_chain_layer_geometry(la.arr, la.n, ndim, in_channels, H, W, j, ctypes.byref(g)),
+    _check(lib().dss_chain_layer_geometry(la.arr, la.n, ndim, in_channels, H, W, ell, j, ctypes.byref(g)),
            "dss_chain_layer_geometry")
     return g.as_dict()
 
@@ -191,20 +192,21 @@ class Plan:
         except Exception:
             pass
 
-    def geometry(self, H, W):
+    def geometry(self, H, W, ell=0):
         g = Geometry()
-        _check(lib().dss_plan_geometry(self.handle, H, W, ctypes.byref(g)), "dss_plan_geometry")
+        _check(lib().dss_plan_geometry(self.handle, H, W, ell, ctypes.byref(g)), "dss_plan_geometry")
         return g.as_dict()
 
-    def layer_geometry(self, H, W, j):
+    def layer_geometry(self, H, W, j, ell=0):
         g = LayerGeometry()
-        _check(lib().dss_plan_layer_geometry(self.handle, H, W, j, ctypes.byref(g)), "dss_plan_layer_geometry")
+        _check(lib().dss_plan_layer_geometry(self.handle, H, W, ell, j, ctypes.byref(g)), "dss_plan_layer_geometry")
         return g.as_dict()
 
-    def workspace(self, H, W, device=None):
-        """A device workspace (uint8 tensor) large enough for an H x W signal; reused across calls."""
+    def workspace(self, H, W, device=None, ell=0):
+        """A device workspace (uint8 tensor) large enough for an H x W signal at
+        mixed level ell; reused across calls."""
         import torch
-        need = self.geometry(H, W)["workspace_bytes"]
+        need = self.geometry(H, W, ell)["workspace_bytes"]
         if self._ws is None or self._ws.numel() < need:
             self._ws = None
             self._ws = torch.empty(max(need, 256), dtype=torch.uint8, device=device or "cuda")
@@ -230,16 +232,28 @@ class Plan:
                                     _stream(stream)), "dss_eval_dense")
         return out
 
-    def eval_slide(self, signal, j, out=None, workspace=None, stream=None):
+    def eval_mixed(self, signal, ell, out=None, workspace=None, stream=None):
         import torch
         self._check_signal(signal)
         _, H, W = signal.shape
-        lg = self.layer_geometry(H, W, j)
+        g = self.geometry(H, W, ell)
+        if out is None:
+            out = torch.empty((g["out_c"], g["out_h"], g["out_w"]), dtype=torch.float32, device=signal.device)
+        ws = workspace if workspace is not None else self.workspace(H, W, signal.device, ell)
+        _check(lib().dss_eval_mixed(self.handle, _ptr(signal), H, W, ell, _ptr(out), _ptr(ws), ws.numel(),
+                                    _stream(stream)), "dss_eval_mixed")
+        return out
+
+    def eval_slide(self, signal, j, out=None, workspace=None, stream=None, ell=0):
+        import torch
+        self._check_signal(signal)
+        _, H, W = signal.shape
+        lg = self.layer_geometry(H, W, j, ell)
         if out is None:
             out = torch.empty((lg["F"], lg["channels"], lg["U_h"], lg["U_w"]), dtype=torch.float32,
                               device=signal.device)
-        ws = workspace if workspace is not None else self.workspace(H, W, signal.device)
-        _check(lib().dss_eval_slide(self.handle, _ptr(signal), H, W, j, _ptr(out), _ptr(ws), ws.numel(),
+        ws = workspace if workspace is not None else self.workspace(H, W, signal.device, ell)
+        _check(lib().dss_eval_slide(self.handle, _ptr(signal), H, W, ell, j, _ptr(out), _ptr(ws), ws.numel(),
                                     _stream(stream)), "dss_eval_slide")
         return out
 

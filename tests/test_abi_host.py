@@ -166,8 +166,84 @@ def test_validation_errors(bad):
             la = dss._LayerArray(layers)
             la.arr[0].act = 7
             g = dss.Geometry()
-            dss._check(dss.lib().dss_chain_geometry(la.arr, la.n, nd, C, 0, H, W, dss.ctypes.byref(g)), "geom")
+            dss._check(dss.lib().dss_chain_geometry(la.arr, la.n, nd, C, 0, H, W, 0, dss.ctypes.byref(g)), "geom")
         else:
             dss.chain_geometry(layers, nd, C, H, W)
     assert e.value.status == want
     assert dss.lib().dss_last_error().decode() != ""
+
+
+# ----------------------------------------------------------------------------- mixed evaluation geometry
+
+from oracle import mixed  # noqa: E402
+from tests.test_oracle_mixed import ARCHS as MIXED_ARCHS  # noqa: E402
+
+
+@pytest.mark.parametrize("name", list(MIXED_ARCHS))
+def test_mixed_geometry_matches_the_oracle_algorithm(name):
+    """Per mixed level and signal length: trimming/stuffing amounts, output
+    extents, per-layer fragment counts and extents and the convolution flop count
+    agree with the oracle's literal mixed algorithm (its tensor shapes)."""
+    arch, C, nd = MIXED_ARCHS[name]
+    layers = wl.init_layers(arch, np.random.default_rng(0))
+    ch = mixed.chain_of(layers)
+    ks, us = mixed.stride_products(ch), mixed.strided_extents(ch)
+    L, B, K = len(ch), us[0], ks[-1]
+    rng = np.random.default_rng(2)
+    sizes = [(1, w) for w in range(B[1], B[1] + K[1] + 2)] if nd == 1 else \
+        [(B[0] + a, B[1] + b) for a in range(K[0] + 1) for b in (0, K[1] - 1, K[1] + 2)]
+    for (H, W) in sizes:
+        x = rng.standard_normal((C, H, W))
+        for ell in range(L + 1):
+            g = dss.chain_geometry(layers, nd, C, H, W, ell=ell)
+            assert g["ell"] == ell and (g["step_h"], g["step_w"]) == ks[ell]
+            for a, N, key in ((0, H, "h"), (1, W, "w")):
+                mode, r, tr, st, s = mixed.operating_mode(N, B[a], K[a], ks[ell][a])
+                assert (g["trim_" + key], g["r_" + key]) == (tr, st)
+                assert g["D_" + key] == N - tr + st
+                assert g["out_" + key] == mixed.output_extent(N, B[a], ks[ell][a])
+            flops = 0.0
+            prev = (1, C, g["D_h"], g["D_w"])
+            for j in range(1, L + 1):
+                lg = dss.chain_layer_geometry(layers, nd, C, H, W, j, ell=ell)
+                rep = mixed.eval_relax_slide(layers, x, ell, upto=j)
+                assert (lg["F"], lg["channels"], lg["U_h"], lg["U_w"]) == rep.shape
+                assert lg["relaxed"] == (1 if j <= ell else 0)
+                conv = ch[j - 1]["conv"]
+                if conv is not None:
+                    Eh, Ew = prev[2] - conv["fh"] + 1, prev[3] - conv["fw"] + 1
+                    flops += 2.0 * prev[0] * Eh * Ew * conv["cout"] * conv["cin"] * conv["fh"] * conv["fw"]
+                prev = rep.shape
+            assert g["conv_flops"] == flops
+            lg0 = dss.chain_layer_geometry(layers, nd, C, H, W, 0, ell=ell)
+            assert (lg0["F"], lg0["U_h"], lg0["U_w"]) == (1, g["D_h"], g["D_w"])
+
+
+def test_mixed_level_zero_is_the_dense_geometry():
+    layers = wl.init_layers(wl.arch_c4(), np.random.default_rng(0))
+    a = dss.chain_geometry(layers, 2, 3, 1080, 1920)
+    b = dss.chain_geometry(layers, 2, 3, 1080, 1920, ell=0)
+    assert a == b and a["trim_h"] == a["trim_w"] == 0 and a["step_h"] == a["step_w"] == 1
+
+
+def test_mixed_hd_frame_work_shrinks_with_the_level():
+    """The relaxed layers evaluate one fragment: the convolution work falls by
+    about k*_l^2 in the relaxed part (Sect. 5 counts for the relaxed fashion)."""
+    layers = wl.init_layers(wl.arch_c4(), np.random.default_rng(0))
+    # five chain layers; the last two have no pool, so k*_3 = k*_4 = k*_5 = 8 and
+    # relaxing them changes nothing
+    f = [dss.chain_geometry(layers, 2, 3, 1080, 1920, ell=l)["conv_flops"] for l in range(6)]
+    assert f[0] > f[1] > f[2] > f[3] == f[4] == f[5]
+    g5 = dss.chain_geometry(layers, 2, 3, 1080, 1920, ell=5)
+    assert (g5["out_h"], g5["out_w"]) == (-(-(1080 - 67) // 8), -(-(1920 - 67) // 8))
+
+
+@pytest.mark.parametrize("ell", [-1, 6])
+def test_mixed_level_out_of_range(ell):
+    layers = wl.init_layers(wl.arch_c4(), np.random.default_rng(0))
+    with pytest.raises(dss.DssError) as e:
+        dss.chain_geometry(layers, 2, 3, 512, 512, ell=ell)
+    assert e.value.status == 1
+    with pytest.raises(dss.DssError) as e:
+        dss.chain_layer_geometry(layers, 2, 3, 512, 512, 1, ell=ell)
+    assert e.value.status == 1
