@@ -12,6 +12,13 @@ kernel (per-launch HIP-event durations measured inside the timed region), a
 per-kernel breakdown, and the oracle's throughput on a bounded window sample of
 the same frame (CPU baseline, also used as a parity spot check).
 
+`--sweep` runs the paper's runtime experiment shape instead (Sect. 6.3: one
+240x320 random image, L = 1..15 layers of 3x3 convolutions with 128 maps and a
+2x2 max-pool after every third one, random weights): per L, the dense
+evaluation against the patch-by-patch baseline (dss_eval_stride, all windows
+in memory-sized batches through the same kernels), and prints one JSON line
+with both times and the speed-up.
+
 `--ell l` (l > 0) times the mixed evaluation instead (appendix, Theorem
 "evalrelaxslide"): the first l chain layers pool with stride, and the output is
 the dense output downsampled by k*_l per axis; the metric then counts those
@@ -95,6 +102,9 @@ def main():
                     help="mixed level: chain layers 1..ell run relaxed (0 = dense evaluation)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run plain 1 GiB device-to-device copies (scales the HBM byte counters of a profiler)")
+    ap.add_argument("--sweep", action="store_true",
+                    help="EvalSlide vs patch-by-patch EvalStride on the paper's 240x320 family, L = 1..15")
+    ap.add_argument("--sweep-layers", default="1-15", help="range of L for --sweep, e.g. 1-15 or 12")
     args = ap.parse_args()
     if args.calibrate_copy:
         return calibrate_copy()
@@ -111,6 +121,8 @@ def main():
     from paper_1508_06904_amd import dss, workloads as wl
 
     torch.cuda.set_device(0)
+    if args.sweep:
+        return sweep(args)
     t0 = time.time()
     w = wl.make(args.config)
     log("workload %s %s generated in %.1fs" % (args.config, w.x.shape, time.time() - t0))
@@ -204,6 +216,79 @@ def main():
     if not args.no_cpu_baseline:
         record["cpu_baseline"], record["parity_spot_check"] = cpu_baseline(w, g, out, args.cpu_seconds)
     print(json.dumps(record), flush=True)
+
+
+def sweep(args, H=240, W=320, maps=128, ws_budget=48e9):
+    """Sect. 6.3 runtime experiment shape on one MI355X.  Per L: EvalSlide is one
+    dss_eval_dense (Stuff, Frag, Defrag and Trim included, as the paper counts
+    it); EvalStride is dss_eval_stride over every window in batches that fit
+    `ws_budget` bytes of workspace.  The paper leaves patch extraction and output
+    assembly out of the EvalStride time; both figures are reported."""
+    import numpy as np
+    import torch
+
+    from paper_1508_06904_amd import dss, workloads as wl
+
+    lo, _, hi = args.sweep_layers.partition("-")
+    Ls = range(int(lo), int(hi or lo) + 1)
+    x = wl.uniform_image(np.random.default_rng(0), 1, H, W)
+    xd = torch.from_numpy(x).to("cuda").contiguous()
+    rows = []
+    for L in Ls:
+        layers = wl.init_layers(wl.arch_paper_sweep(L, maps), np.random.default_rng(100 + L))
+        plan = dss.Plan(layers, 2, 1)
+        g = plan.geometry(H, W)
+        n = g["out_h"] * g["out_w"]
+        dense = torch.empty((g["out_c"], g["out_h"], g["out_w"]), dtype=torch.float32, device="cuda")
+        ws = plan.workspace(H, W)
+        reps = max(3, args.steps)
+        for _ in range(2):
+            plan.eval_dense(xd, out=dense, workspace=ws)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            plan.eval_dense(xd, out=dense, workspace=ws)
+        e1.record()
+        torch.cuda.synchronize()
+        slide_ms = e0.elapsed_time(e1) / reps
+
+        per_ws = plan.stride_geometry(1024)[0] / 1024.0
+        batch = int(max(1, min(n, ws_budget // per_ws)))
+        sws = torch.empty(max(256, plan.stride_geometry(batch)[0]), dtype=torch.uint8, device="cuda")
+        strided = torch.full_like(dense, float("nan"))
+        plan.eval_stride(xd, 0, min(batch, n), out=strided, workspace=sws)   # warm-up batch
+        torch.cuda.synchronize()
+        plan.set_timing(True)
+        e0.record()
+        for first in range(0, n, batch):
+            plan.eval_stride(xd, first, min(batch, n - first), out=strided, workspace=sws)
+        e1.record()
+        torch.cuda.synchronize()
+        stride_ms = e0.elapsed_time(e1)
+        recs = plan.timings()
+        plan.set_timing(False)
+        io_ms = sum(r["ms"] for r in recs if r["kernel"] in ("patch_pack", "window_scatter"))
+        conv_ms = sum(r["ms"] for r in recs if r["flops"] > 0)
+        stride_flops = sum(r["flops"] for r in recs)
+        same = bool(torch.equal(strided, dense))
+        row = {"L": L, "B": g["B_h"], "k_star": g["K_h"], "windows": n, "batch": batch,
+               "slide_ms": slide_ms, "stride_ms": stride_ms, "stride_ms_without_patch_io": stride_ms - io_ms,
+               "speedup": stride_ms / slide_ms, "speedup_paper_protocol": (stride_ms - io_ms) / slide_ms,
+               "slide_conv_tflop": g["conv_flops"] / 1e12, "stride_conv_tflop": stride_flops / 1e12,
+               "stride_conv_tflops": stride_flops / conv_ms / 1e9 if conv_ms > 0 else None,
+               "bit_identical": same}
+        log("L=%2d B=%3d windows=%6d  slide %.3f ms  stride %.1f ms (%.1f without patch I/O)  speed-up %.1fx  "
+            "identical=%s" % (L, g["B_h"], n, slide_ms, stride_ms, stride_ms - io_ms, stride_ms / slide_ms, same))
+        rows.append(row)
+        del plan, dense, ws, sws, strided
+        torch.cuda.empty_cache()
+    print(json.dumps({"metric": "EvalSlide speed-up over patch-by-patch EvalStride at 1 MI355X",
+                      "unit": "x", "higher_is_better": True, "dtype": "f32", "data": "synthetic (seeded)",
+                      "config": {"workload": "paper runtime-experiment shape: 1x%dx%d U[0,1) image, L 3x3 conv+ReLU "
+                                             "layers with %d maps, 2x2 max-pool after every third conv unless last, "
+                                             "He-init weights" % (H, W, maps)},
+                      "rows": rows}), flush=True)
 
 
 def calibrate_copy(n=4, nbytes=1 << 30):

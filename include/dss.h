@@ -232,6 +232,38 @@ dss_status dss_eval_slide(dss_plan_t plan, const void* signal, int32_t H, int32_
                           int32_t j, float* out, void* workspace, int64_t workspace_bytes,
                           hipStream_t stream);
 
+/* ---------------------------------------------------------------- EvalStride baseline */
+
+/* Workspace bytes (and, if conv_flops is not NULL, the algorithmic convolution
+ * flops) of dss_eval_stride for a batch of `count` windows, for a layer list
+ * (no plan, no GPU) or for a plan.  DSS_E_INVALID if count <= 0. */
+dss_status dss_chain_stride_geometry(const dss_layer* layers, int32_t n_layers, int32_t ndim,
+                                     int32_t in_channels, dss_dtype dtype, int32_t count,
+                                     int64_t* workspace_bytes, double* conv_flops);
+dss_status dss_plan_stride_geometry(dss_plan_t plan, int32_t count, int64_t* workspace_bytes,
+                                    double* conv_flops);
+
+/* Conventional patch-by-patch scanning, the baseline the method is measured
+ * against (EvalStride of Definition "processing chain", Sect. 4.2, applied to
+ * each extracted subsignal, Sect. 2.3; the runtime comparison of Sect. 6.3):
+ * the windows with row-major indices first .. first+count-1 of the dense output
+ * grid are copied out as a batch of B_h x B_w fragments, the strided network
+ * runs on every fragment with the same convolution kernels as the dense
+ * evaluation (max-pooling with stride k_j, no fragmentation), and each window's
+ * output is written to its place in `out`.
+ *   signal     device, [in_c][H][W] in the plan's dtype
+ *   first      index of the first window, i * (W - B_w + 1) + j for window (i, j)
+ *   count      number of windows in this batch (first + count <= number of windows)
+ *   out        device, binary32 [out_c][H - B_h + 1][W - B_w + 1] (the layout of
+ *              dss_eval_dense); only the batch's positions are written
+ *   workspace  device scratch of at least dss_plan_stride_geometry(count) bytes,
+ *              256-byte aligned
+ * Errors: DSS_E_INVALID (NULL pointers, window range, device), DSS_E_SHAPE
+ * (signal smaller than the receptive field, workspace too small), DSS_E_HIP. */
+dss_status dss_eval_stride(dss_plan_t plan, const void* signal, int32_t H, int32_t W, int64_t first,
+                           int32_t count, float* out, void* workspace, int64_t workspace_bytes,
+                           hipStream_t stream);
+
 /* ---------------------------------------------------------------- Frag / Defrag */
 
 /* Fragmentation Frag_k per axis (Definition "fragmentation" and Lemma

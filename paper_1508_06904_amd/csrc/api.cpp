@@ -401,17 +401,18 @@ const char* conv_name(const PlanConv& pc, dss_dtype tout) {
 
 // Runs Stuff and chain layers 1..upto.  On return *cur points at the last
 // tensor (channels-last fragment layout) and *cur_dt is its element type.
-static dss_status run_chain(dss_plan* p, const Geom& G, const void* signal, int upto, char* ws,
-                            hipStream_t stream, Timer& T, void** cur_out, dss_dtype* cur_dt) {
+// Chain layers 1..upto on the packed input in buf[0] (the two halves of the
+// workspace ping-pong).  On return *cur points at the last tensor (channels-last
+// fragment layout) and *cur_dt is its element type.  A relaxed layer's pooling
+// runs over all Fin fragments at once as one tall signal of Fin * E_h rows:
+// every fragment's extent is a multiple of k_h, so no block straddles two.
+static dss_status run_layers(dss_plan* p, const Geom& G, int upto, char* const buf[2], hipStream_t stream, Timer& T,
+                             void** cur_out, dss_dtype* cur_dt) {
     const Chain& ch = p->chain;
-    char* buf[2] = {ws, ws + G.buf_bytes};
     int which = 0;
     const dss_dtype dt = p->dtype;
     const double es = (double)dtype_size(dt);
-    const double in_read = (double)std::min(G.H, G.D_h) * std::min(G.W, G.D_w);
-    hipError_t e = T.run("stuff_pack", 0, 0.0, (double)ch.in_c * (in_read + G.D_h * (double)G.D_w) * es,
-                         [&] { return launch_stuff_pack(dt, signal, ch.in_c, G.H, G.W, buf[0], G.D_h, G.D_w, stream); });
-    if (e != hipSuccess) return hip_fail(e, "stuff_pack launch");
+    hipError_t e;
     void* cur = buf[0];
     dss_dtype cdt = dt;
     for (int j = 1; j <= upto; ++j) {
@@ -441,9 +442,10 @@ static dss_status run_chain(dss_plan* p, const Geom& G, const void* signal, int 
         }
         if (c.has_pool && lg.relaxed) {
             void* dst = buf[which ^ 1];
-            const double bytes = ((double)lg.E_h * lg.E_w + (double)lg.U_h * lg.U_w) * c.cout * dtype_size(cdt);
+            const double bytes = (double)Fin * ((double)lg.E_h * lg.E_w + (double)lg.U_h * lg.U_w) * c.cout *
+                                 dtype_size(cdt);
             e = T.run("pool_stride", j, 0.0, bytes, [&] {
-                return launch_pool_stride(cdt, cur, lg.E_h, lg.E_w, c.cout, c.k_h, c.k_w, dst, stream);
+                return launch_pool_stride(cdt, cur, Fin * lg.E_h, lg.E_w, c.cout, c.k_h, c.k_w, dst, stream);
             });
             if (e != hipSuccess) return hip_fail(e, "pool_stride launch");
             which ^= 1;
@@ -463,6 +465,20 @@ static dss_status run_chain(dss_plan* p, const Geom& G, const void* signal, int 
     *cur_out = cur;
     *cur_dt = cdt;
     return DSS_OK;
+}
+
+// Stuff (or trim) into the workspace, then chain layers 1..upto.
+static dss_status run_chain(dss_plan* p, const Geom& G, const void* signal, int upto, char* ws,
+                            hipStream_t stream, Timer& T, void** cur_out, dss_dtype* cur_dt) {
+    const Chain& ch = p->chain;
+    char* const buf[2] = {ws, ws + G.buf_bytes};
+    const dss_dtype dt = p->dtype;
+    const double es = (double)dtype_size(dt);
+    const double in_read = (double)std::min(G.H, G.D_h) * std::min(G.W, G.D_w);
+    hipError_t e = T.run("stuff_pack", 0, 0.0, (double)ch.in_c * (in_read + G.D_h * (double)G.D_w) * es,
+                         [&] { return launch_stuff_pack(dt, signal, ch.in_c, G.H, G.W, buf[0], G.D_h, G.D_w, stream); });
+    if (e != hipSuccess) return hip_fail(e, "stuff_pack launch");
+    return run_layers(p, G, upto, buf, stream, T, cur_out, cur_dt);
 }
 
 static dss_status check_eval_args(dss_plan_t plan, const void* signal, const void* out, void* workspace,
@@ -531,6 +547,82 @@ extern "C" dss_status dss_eval_slide(dss_plan_t plan, const void* signal, int32_
     const int C = j == 0 ? ch.in_c : ch.layers[j - 1].cout;
     hipError_t e = T.run("to_planar", j, 0.0, 0.0, [&] { return launch_to_planar(cdt, cur, F, h, w, C, out, stream); });
     if (e != hipSuccess) return hip_fail(e, "to_planar launch");
+    return DSS_OK;
+}
+
+// ------------------------------------------------------------------ EvalStride baseline
+
+extern "C" dss_status dss_chain_stride_geometry(const dss_layer* layers, int32_t n_layers, int32_t ndim,
+                                                int32_t in_channels, dss_dtype dtype, int32_t count,
+                                                int64_t* workspace_bytes, double* conv_flops) {
+    if (!workspace_bytes) return fail(DSS_E_INVALID, "NULL output");
+    if (dtype != DSS_F32 && dtype != DSS_BF16) return fail(DSS_E_UNSUPPORTED, "unknown dtype %d", dtype);
+    Chain ch;
+    dss_status s = build_chain(layers, n_layers, ndim, in_channels, &ch);
+    if (s != DSS_OK) return s;
+    Geom G;
+    s = compute_stride_geometry(ch, dtype, count, &G);
+    if (s != DSS_OK) return s;
+    *workspace_bytes = G.ws_bytes;
+    if (conv_flops) *conv_flops = G.conv_flops;
+    return DSS_OK;
+}
+
+extern "C" dss_status dss_plan_stride_geometry(dss_plan_t plan, int32_t count, int64_t* workspace_bytes,
+                                               double* conv_flops) {
+    if (!plan || !workspace_bytes) return fail(DSS_E_INVALID, "NULL plan or output");
+    Geom G;
+    dss_status s = compute_stride_geometry(plan->chain, plan->dtype, count, &G);
+    if (s != DSS_OK) return s;
+    *workspace_bytes = G.ws_bytes;
+    if (conv_flops) *conv_flops = G.conv_flops;
+    return DSS_OK;
+}
+
+extern "C" dss_status dss_eval_stride(dss_plan_t plan, const void* signal, int32_t H, int32_t W, int64_t first,
+                                      int32_t count, float* out, void* workspace, int64_t workspace_bytes,
+                                      hipStream_t stream) {
+    if (!plan || !signal || !out) return fail(DSS_E_INVALID, "NULL plan, signal or out");
+    const Chain& ch = plan->chain;
+    if (ch.ndim == 1 && H != 1) return fail(DSS_E_SHAPE, "1-D plan needs H = 1 (got %d)", H);
+    if (H < ch.B_h || W < ch.B_w)
+        return fail(DSS_E_SHAPE, "signal %dx%d is smaller than the receptive field %dx%d", H, W, ch.B_h, ch.B_w);
+    const int O_h = H - ch.B_h + 1, O_w = W - ch.B_w + 1;
+    if (first < 0 || count <= 0 || first + count > (int64_t)O_h * O_w)
+        return fail(DSS_E_INVALID, "windows [%lld, %lld) outside 0..%lld", (long long)first,
+                    (long long)(first + count), (long long)O_h * O_w);
+    Geom G;
+    dss_status s = compute_stride_geometry(ch, plan->dtype, count, &G);
+    if (s != DSS_OK) return s;
+    if (!workspace) return fail(DSS_E_INVALID, "NULL workspace (need %lld bytes)", (long long)G.ws_bytes);
+    if (workspace_bytes < G.ws_bytes)
+        return fail(DSS_E_SHAPE, "workspace of %lld bytes is smaller than the %lld bytes needed",
+                    (long long)workspace_bytes, (long long)G.ws_bytes);
+    if (((uintptr_t)workspace & 255u) != 0) return fail(DSS_E_INVALID, "workspace is not 256-byte aligned");
+    int cur_dev = -1;
+    hipError_t e = hipGetDevice(&cur_dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    if (cur_dev != plan->device)
+        return fail(DSS_E_INVALID, "plan belongs to device %d but device %d is current", plan->device, cur_dev);
+
+    Timer T(plan, stream);
+    char* const buf[2] = {(char*)workspace, (char*)workspace + G.buf_bytes};
+    const double es = (double)dtype_size(plan->dtype);
+    const double pbytes = 2.0 * count * (double)ch.B_h * ch.B_w * ch.in_c * es;
+    e = T.run("patch_pack", 0, 0.0, pbytes, [&] {
+        return launch_patch_pack(plan->dtype, signal, ch.in_c, H, W, O_w, first, count, ch.B_h, ch.B_w, buf[0],
+                                 stream);
+    });
+    if (e != hipSuccess) return hip_fail(e, "patch_pack launch");
+    void* cur = nullptr;
+    dss_dtype cdt;
+    s = run_layers(plan, G, ch.L(), buf, stream, T, &cur, &cdt);
+    if (s != DSS_OK) return s;
+    const double sbytes = (double)count * ch.out_c() * (dtype_size(cdt) + 4.0);
+    e = T.run("window_scatter", ch.L() + 1, 0.0, sbytes, [&] {
+        return launch_window_scatter(cdt, cur, count, ch.out_c(), first, (int64_t)O_h * O_w, out, stream);
+    });
+    if (e != hipSuccess) return hip_fail(e, "window_scatter launch");
     return DSS_OK;
 }
 

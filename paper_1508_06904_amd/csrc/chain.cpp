@@ -223,4 +223,61 @@ dss_status compute_geometry(const Chain& ch, dss_dtype dt, int H, int W, int ell
     return DSS_OK;
 }
 
+// The strided network on a batch of `count` windows (EvalStride of Definition
+// "processing chain", Sect. 4.2): each window is a fragment of B_h x B_w samples,
+// every layer is relaxed (conv on each fragment, then max-pool with stride k_j),
+// and after layer j each fragment holds u_j samples per axis (Lemma (a)).
+dss_status compute_stride_geometry(const Chain& ch, dss_dtype dt, int count, Geom* g) {
+    if (count <= 0) return fail(DSS_E_INVALID, "window count must be positive (got %d)", count);
+    const int L = ch.L();
+    Geom G;
+    G.ell = L;
+    G.H = G.D_h = ch.B_h;
+    G.W = G.D_w = ch.B_w;
+    G.out_h = G.out_w = 1;
+    G.step_h = ch.K_h();
+    G.step_w = ch.K_w();
+    const double es = (double)dtype_size(dt);
+    int Uh = ch.B_h, Uw = ch.B_w;
+    int64_t maxbuf = (int64_t)count * Uh * Uw * ch.in_c * (int64_t)es;
+    G.total_bytes = 2.0 * (double)count * Uh * Uw * ch.in_c * es;
+    for (int j = 1; j <= L; ++j) {
+        const ChainLayer& c = ch.layers[j - 1];
+        LayerGeom lg;
+        lg.relaxed = true;
+        lg.Uin_h = Uh;
+        lg.Uin_w = Uw;
+        lg.Fin_h = lg.Fout_h = count;
+        lg.Fin_w = lg.Fout_w = 1;
+        lg.E_h = Uh - c.c_h + 1;
+        lg.E_w = Uw - c.c_w + 1;
+        lg.U_h = lg.E_h / c.k_h;
+        lg.U_w = lg.E_w / c.k_w;
+        if (lg.U_h != ch.u_h[j] || lg.U_w != ch.u_w[j] || lg.E_h != c.k_h * ch.u_h[j] || lg.E_w != c.k_w * ch.u_w[j])
+            return fail(DSS_E_SHAPE, "layer %d: strided extents disagree with Lemma (a)", j);
+        const bool last_op = (j == L) && !c.has_pool;
+        if (c.has_conv) {
+            const double es_out = (dt == DSS_BF16 && last_op) ? 4.0 : es;
+            G.conv_flops += 2.0 * (double)count * lg.E_h * lg.E_w * c.cout * (double)c.cin * c.c_h * c.c_w;
+            const int64_t out_b = (int64_t)count * lg.E_h * lg.E_w * c.cout * (int64_t)es_out;
+            maxbuf = std::max(maxbuf, out_b);
+            G.total_bytes += (double)count * Uh * Uw * c.cin * es + (double)out_b +
+                             (double)c.cout * c.cin * c.c_h * c.c_w * (dt == DSS_BF16 ? 2.0 : 4.0);
+        }
+        if (c.has_pool) {
+            const double pb = (double)count * ((double)lg.E_h * lg.E_w + (double)lg.U_h * lg.U_w) * c.cout * es;
+            G.pool_bytes += pb;
+            G.total_bytes += pb;
+            maxbuf = std::max(maxbuf, (int64_t)count * lg.U_h * lg.U_w * c.cout * (int64_t)es);
+        }
+        G.L.push_back(lg);
+        Uh = lg.U_h;
+        Uw = lg.U_w;
+    }
+    G.buf_bytes = (maxbuf + 255) / 256 * 256;
+    G.ws_bytes = 2 * G.buf_bytes;
+    *g = std::move(G);
+    return DSS_OK;
+}
+
 }  // namespace dss

@@ -78,7 +78,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
     const float* __restrict__ bias,    // [Cout_pad]
     int fh, int fw, int Cout, int act, int nchunks,
     Tout* __restrict__ out,            // [F][Hout][Wout][Cout]
-    int Hout, int Wout, int TH, int TW, int tilesY, int tilesX, int nbs, int dbl_halo) {
+    int Hout, int Wout, int TH, int TW, int tilesY, int tilesX, int nbs, int dbl_halo,
+    int flat_h, int flat_w) {           // flat mode: input fragments of flat_h x flat_w (0: spatial tiles)
     using Cfg = MfmaCfg<BF16, WGM, WGN, MT, NT>;
     constexpr int THREADS = Cfg::THREADS;
     constexpr int WSLOTS = Cfg::WSLOTS;
@@ -114,8 +115,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
     const int ty0 = (trem / tilesX) * TH;
     const int tx0 = (trem % tilesX) * TW;
 
-    const int HW = TW + fw - 1;          // halo width
-    const int halo_px = (TH + fh - 1) * HW;
+    // Spatial tiles: a TH x TW block of one fragment, halo (TH + fh - 1) x (TW + fw - 1).
+    // Flat mode (small fragments): the fragment batch is read as one sequence of
+    // samples, a tile is TW consecutive positions of it (TH = 1), tap (th, tw)
+    // sits th * flat_w + tw samples further on, and only positions that are valid
+    // outputs of their own fragment are stored.
+    const int HW = flat_w ? TW + (fh - 1) * flat_w + fw - 1 : TW + fw - 1;   // halo row width
+    const int tap_row = flat_w ? flat_w : HW;
+    const int halo_px = (flat_w ? TH : TH + fh - 1) * HW;
     const int halo_slots = halo_px * kSlotsPerRow;
     const int halo_bytes = ((halo_px * kPitchBytes + 127) / 128) * 128;
     char* halo0 = lds;
@@ -206,7 +213,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
                     stage_w(step + 1, (step & 1) ? wbuf0 : wbuf1);
                     if (last_tap && dbl_halo) stage_halo(cc + 1, (cc & 1) ? halo0 : halo1);
                 }
-                const int tap_off = (th * HW + tw) * kPitchBytes;
+                const int tap_off = (th * tap_row + tw) * kPitchBytes;
                 const char* wcur = (step & 1) ? wbuf1 : wbuf0;
                 u32x4 a[MT][2], b[NT][2];
 #pragma unroll
@@ -255,21 +262,38 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
     // -- epilogue: D[i][j] of a 32x32 tile sits in lane j + 32*((i/4)%2), register (i/8)*4 + i%4
     const int n_base = nb * Cfg::BN + wn * 32 * NT;
     const size_t f_off = (size_t)f * Hout * Wout;
+    const int frag_px = flat_h * flat_w;
+    int ncol[NT];
+    float bn[NT];
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
-        const int n = n_base + nt * 32 + l32;
-        if (n >= Cout) continue;
-        const float bn = bias[n];
+        ncol[nt] = n_base + nt * 32 + l32;
+        bn[nt] = ncol[nt] < Cout ? bias[ncol[nt]] : 0.f;
+    }
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt) {
+    for (int mt = 0; mt < MT; ++mt) {
 #pragma unroll
-            for (int v = 0; v < 16; ++v) {
-                const int i = (v >> 2) * 8 + half * 4 + (v & 3);
-                const int m = wm * 32 * MT + mt * 32 + i;
+        for (int v = 0; v < 16; ++v) {
+            const int i = (v >> 2) * 8 + half * 4 + (v & 3);
+            const int m = wm * 32 * MT + mt * 32 + i;
+            size_t o;
+            bool ok;
+            if (flat_w) {
+                const int p = tx0 + m;                 // TH = 1: position in the flat sequence (Win long)
+                const int fr = p / frag_px, r = p - fr * frag_px;
+                const int y = r / flat_w, x = r - y * flat_w;
+                ok = p < Win && y < Hout && x < Wout;
+                o = ((size_t)fr * Hout + y) * Wout + x;
+            } else {
                 const int y = ty0 + m / TW, x = tx0 + m % TW;
-                if (y < Hout && x < Wout)
-                    store_elem(out + (f_off + (size_t)y * Wout + x) * Cout + n, activate(act, acc[mt][nt][v] + bn));
+                ok = y < Hout && x < Wout;
+                o = f_off + (size_t)y * Wout + x;
             }
+            if (!ok) continue;
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt)
+                if (ncol[nt] < Cout)
+                    store_elem(out + o * Cout + ncol[nt], activate(act, acc[mt][nt][v] + bn[nt]));
         }
     }
 }
@@ -367,11 +391,38 @@ bool mfma_supports(bool bf16, int cout, int fh, int fw) {
     return pick_tile(256, bn, 1, 1, fh, fw, 64 * 1024).TH > 0 && pick_tile(256, bn, 64, 64, fh, fw, 64 * 1024).TH > 0;
 }
 
+// Flat-mode tile (TH = 1, TW = BM consecutive positions of the flattened
+// fragment batch) for fragments of Hin x Win input samples, or TH = 0 if its
+// single-row halo does not fit.
+static Tile flat_tile(int BM, int BN, int Win, int fh, int fw, size_t lds_max) {
+    const int64_t halo_px = BM + (int64_t)(fh - 1) * Win + fw - 1;
+    const size_t halo_b = (size_t)((halo_px * kPitchBytes + 127) / 128) * 128;
+    const size_t wb = 2 * (size_t)BN * kPitchBytes;
+    const size_t cap = std::min(lds_max, (size_t)kMaxLds);
+    if (2 * halo_b + wb <= cap) return Tile{1, BM, 2 * halo_b + wb, 1};
+    if (halo_b + wb <= cap) return Tile{1, BM, halo_b + wb, 0};
+    return Tile{0, 0, 0, 0};
+}
+
 template <bool BF16, typename Tout, int WGM, int WGN, int MT, int NT>
 static hipError_t run_mfma(const void* in, int F, int Hin, int Win, const PlanConv& pc, void* out, hipStream_t s) {
     using Cfg = MfmaCfg<BF16, WGM, WGN, MT, NT>;
     const int Hout = Hin - pc.fh + 1, Wout = Win - pc.fw + 1;
-    const Tile t = pick_tile(Cfg::BM, Cfg::BN, Hout, Wout, pc.fh, pc.fw, device_lds_limit());
+    Tile t = pick_tile(Cfg::BM, Cfg::BN, Hout, Wout, pc.fh, pc.fw, device_lds_limit());
+    // Small fragments waste most of a spatial tile; reading the batch as one
+    // flat sequence computes Hin*Win positions per fragment instead (only the
+    // last fh-1 rows and fw-1 columns of each are discarded).
+    int flat = 0;
+    const int64_t flat_len = (int64_t)F * Hin * Win;
+    if (flat_len < (1ll << 30)) {
+        const Tile ft = flat_tile(Cfg::BM, Cfg::BN, Win, pc.fh, pc.fw, device_lds_limit());
+        const int64_t work_tiles = t.TH ? (int64_t)F * ceil_div64(Hout, t.TH) * t.TH * ceil_div64(Wout, t.TW) * t.TW : -1;
+        const int64_t work_flat = ceil_div64(flat_len, Cfg::BM) * Cfg::BM;
+        if (ft.TH && (work_tiles < 0 || 10 * work_flat < 9 * work_tiles)) {
+            t = ft;
+            flat = 1;
+        }
+    }
     if (t.TH == 0) return hipErrorInvalidConfiguration;
     auto kern = conv_mfma_kernel<BF16, Tout, WGM, WGN, MT, NT>;
     if (t.lds > 64 * 1024) {
@@ -382,14 +433,24 @@ static hipError_t run_mfma(const void* in, int F, int Hin, int Win, const PlanCo
             attr_set = true;
         }
     }
-    const int tilesY = (int)ceil_div64(Hout, t.TH), tilesX = (int)ceil_div64(Wout, t.TW);
     const int nbs = pc.cout_pad / Cfg::BN;
+    const int nchunks = pc.cin_pad / Cfg::CC;
+    if (flat) {
+        // one "fragment" of 1 x flat_len samples for the staging and the tile grid
+        const int tilesX = (int)ceil_div64(flat_len, t.TW);
+        const int64_t nblocks = (int64_t)tilesX * nbs;
+        if (nblocks >= (1ll << 31)) return hipErrorInvalidConfiguration;
+        kern<<<dim3((unsigned)nblocks), Cfg::THREADS, t.lds, s>>>(
+            (const char*)in, 1, (int)flat_len, pc.cin, (const char*)pc.w, pc.b, pc.fh, pc.fw, pc.cout, pc.act,
+            nchunks, (Tout*)out, Hout, Wout, 1, t.TW, 1, tilesX, nbs, t.dbl, Hin, Win);
+        return hipGetLastError();
+    }
+    const int tilesY = (int)ceil_div64(Hout, t.TH), tilesX = (int)ceil_div64(Wout, t.TW);
     const int64_t nblocks = (int64_t)F * tilesY * tilesX * nbs;
     if (nblocks >= (1ll << 31)) return hipErrorInvalidConfiguration;
-    const int nchunks = pc.cin_pad / Cfg::CC;
     kern<<<dim3((unsigned)nblocks), Cfg::THREADS, t.lds, s>>>(
         (const char*)in, Hin, Win, pc.cin, (const char*)pc.w, pc.b, pc.fh, pc.fw, pc.cout, pc.act, nchunks,
-        (Tout*)out, Hout, Wout, t.TH, t.TW, tilesY, tilesX, nbs, t.dbl);
+        (Tout*)out, Hout, Wout, t.TH, t.TW, tilesY, tilesX, nbs, t.dbl, 0, 0);
     return hipGetLastError();
 }
 

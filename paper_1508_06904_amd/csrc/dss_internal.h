@@ -68,6 +68,8 @@ struct Geom {
 
 size_t dtype_size(dss_dtype dt);
 dss_status compute_geometry(const Chain& ch, dss_dtype dt, int H, int W, int ell, Geom* g);
+// EvalStride on a batch of `count` windows: every layer relaxed, Fin_h = count fragments.
+dss_status compute_stride_geometry(const Chain& ch, dss_dtype dt, int count, Geom* g);
 
 // ------------------------------------------------------------------ plan
 enum ConvImpl { CONV_DIRECT = 0, CONV_MFMA_F32 = 1, CONV_MFMA_BF16 = 2 };
@@ -114,6 +116,10 @@ hipError_t launch_conv_mfma_bf16(dss_dtype tout, const uint16_t* in, int F, int 
                                  const PlanConv& pc, void* out, hipStream_t s);
 hipError_t launch_pool_frag(dss_dtype dt, const void* in, int S_h, int S_w, int E_h, int E_w, int C,
                             int k_h, int k_w, void* out, hipStream_t s);
+hipError_t launch_patch_pack(dss_dtype dt, const void* in, int C, int H, int W, int O_w, int64_t first, int count,
+                             int B_h, int B_w, void* out, hipStream_t s);
+hipError_t launch_window_scatter(dss_dtype dt, const void* in, int count, int C, int64_t first, int64_t plane,
+                                 float* out, hipStream_t s);
 hipError_t launch_pool_stride(dss_dtype dt, const void* in, int E_h, int E_w, int C, int k_h, int k_w,
                               void* out, hipStream_t s);
 hipError_t launch_defrag_trim(dss_dtype dt, const void* in, int K_h, int K_w, int U_h, int U_w, int C,

@@ -23,6 +23,11 @@
 //               (i mod K_h) * K_w + (j mod K_w); only i < H - B_h + 1,
 //               j < W - B_w + 1 are written.  Output is planar binary32.
 //  to_planar    channels-last fragments -> planar binary32 [F][C][h][w].
+//  patch_pack   Subsignal extraction (Sect. 2.3) for the strided baseline: the
+//               B_h x B_w windows with row-major indices first..first+count-1
+//               copied to a channels-last fragment batch [count][B_h][B_w][C].
+//  window_scatter  the strided baseline's per-window outputs [count][C] written
+//               to their places in the planar binary32 dense output grid.
 //  frag_planar  dss_frag / dss_defrag on planar tensors (pure permutations of
 //               2- or 4-byte elements).
 #include "dev_common.h"
@@ -280,6 +285,59 @@ hipError_t launch_to_planar(dss_dtype dt, const void* in, int F, int h, int w, i
         to_planar_kernel<uint16_t><<<grid, kThreads, 0, s>>>((const uint16_t*)in, F, h, w, C, out);
     else
         to_planar_kernel<float><<<grid, kThreads, 0, s>>>((const float*)in, F, h, w, C, out);
+    return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ patch_pack / window_scatter
+template <typename E>
+__global__ __launch_bounds__(kThreads) void patch_pack_kernel(const E* __restrict__ in, int C, int H, int W, int O_w,
+                                                             int64_t first, int count, int B_h, int B_w,
+                                                             E* __restrict__ out) {
+    const int64_t p = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    const int64_t per = (int64_t)B_h * B_w;
+    if (p >= (int64_t)count * per) return;
+    const int64_t n = p / per;
+    const int q = (int)(p % per);
+    const int y = q / B_w, x = q % B_w;
+    const int64_t win = first + n;
+    const int i0 = (int)(win / O_w), j0 = (int)(win % O_w);
+    const E* src = in + (int64_t)(i0 + y) * W + (j0 + x);
+    E* o = out + p * C;
+    for (int c = 0; c < C; ++c) o[c] = src[(int64_t)c * H * W];
+}
+
+hipError_t launch_patch_pack(dss_dtype dt, const void* in, int C, int H, int W, int O_w, int64_t first, int count,
+                             int B_h, int B_w, void* out, hipStream_t s) {
+    const dim3 grid((unsigned)ceil_div64((int64_t)count * B_h * B_w, kThreads));
+    if (dt == DSS_BF16)
+        patch_pack_kernel<uint16_t><<<grid, kThreads, 0, s>>>((const uint16_t*)in, C, H, W, O_w, first, count, B_h,
+                                                              B_w, (uint16_t*)out);
+    else
+        patch_pack_kernel<uint32_t><<<grid, kThreads, 0, s>>>((const uint32_t*)in, C, H, W, O_w, first, count, B_h,
+                                                              B_w, (uint32_t*)out);
+    return hipGetLastError();
+}
+
+// One thread per (channel, window): consecutive threads write consecutive
+// output samples of one channel plane.
+template <typename T>
+__global__ __launch_bounds__(kThreads) void window_scatter_kernel(const T* __restrict__ in, int count, int C,
+                                                                 int64_t first, int64_t plane,
+                                                                 float* __restrict__ out) {
+    const int64_t p = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (p >= (int64_t)count * C) return;
+    const int c = (int)(p / count);
+    const int64_t n = p % count;
+    out[(int64_t)c * plane + first + n] = to_f32(in[n * C + c]);
+}
+
+hipError_t launch_window_scatter(dss_dtype dt, const void* in, int count, int C, int64_t first, int64_t plane,
+                                 float* out, hipStream_t s) {
+    const dim3 grid((unsigned)ceil_div64((int64_t)count * C, kThreads));
+    if (dt == DSS_BF16)
+        window_scatter_kernel<uint16_t><<<grid, kThreads, 0, s>>>((const uint16_t*)in, count, C, first, plane, out);
+    else
+        window_scatter_kernel<float><<<grid, kThreads, 0, s>>>((const float*)in, count, C, first, plane, out);
     return hipGetLastError();
 }
 

@@ -67,8 +67,8 @@ class LaunchRecord(ctypes.Structure):
 
 EXPORTS = ("dss_chain_geometry", "dss_chain_layer_geometry", "dss_plan_create", "dss_plan_destroy",
            "dss_plan_geometry", "dss_plan_layer_geometry", "dss_eval_dense", "dss_eval_mixed", "dss_eval_slide",
-           "dss_frag", "dss_defrag", "dss_plan_set_timing", "dss_plan_timings", "dss_status_string",
-           "dss_last_error", "dss_version")
+           "dss_chain_stride_geometry", "dss_plan_stride_geometry", "dss_eval_stride", "dss_frag", "dss_defrag",
+           "dss_plan_set_timing", "dss_plan_timings", "dss_status_string", "dss_last_error", "dss_version")
 
 _lib = None
 
@@ -91,6 +91,9 @@ def lib():
         L.dss_eval_dense.argtypes = [VP, VP, I32, I32, VP, VP, I64, VP]
         L.dss_eval_mixed.argtypes = [VP, VP, I32, I32, I32, VP, VP, I64, VP]
         L.dss_eval_slide.argtypes = [VP, VP, I32, I32, I32, I32, VP, VP, I64, VP]
+        L.dss_chain_stride_geometry.argtypes = [P(Layer), I32, I32, I32, I32, I32, P(I64), P(ctypes.c_double)]
+        L.dss_plan_stride_geometry.argtypes = [VP, I32, P(I64), P(ctypes.c_double)]
+        L.dss_eval_stride.argtypes = [VP, VP, I32, I32, I64, I32, VP, VP, I64, VP]
         L.dss_frag.argtypes = [I32, I32, I32, I32, I32, I32, I32, I32, VP, VP, VP]
         L.dss_defrag.argtypes = [I32, I32, I32, I32, I32, I32, I32, I32, VP, VP, VP]
         L.dss_plan_set_timing.argtypes = [VP, I32]
@@ -103,7 +106,8 @@ def lib():
         L.dss_version.restype = ctypes.c_char_p
         for name in ("dss_chain_geometry", "dss_chain_layer_geometry", "dss_plan_create", "dss_plan_geometry",
                      "dss_plan_layer_geometry", "dss_eval_dense", "dss_eval_mixed", "dss_eval_slide", "dss_frag",
-                     "dss_defrag", "dss_plan_set_timing", "dss_plan_timings"):
+                     "dss_defrag", "dss_plan_set_timing", "dss_plan_timings", "dss_plan_stride_geometry",
+                     "dss_chain_stride_geometry", "dss_eval_stride"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -150,6 +154,16 @@ def chain_layer_geometry(layers, ndim, in_channels, H, W, j, ell=0):
     _check(lib().dss_chain_layer_geometry(la.arr, la.n, ndim, in_channels, H, W, ell, j, ctypes.byref(g)),
            "dss_chain_layer_geometry")
     return g.as_dict()
+
+
+def chain_stride_geometry(layers, ndim, in_channels, count, dtype="f32"):
+    """(workspace bytes, conv flops) of the patch-by-patch baseline on `count` windows (host only)."""
+    la = _LayerArray(layers)
+    ws = ctypes.c_int64()
+    fl = ctypes.c_double()
+    _check(lib().dss_chain_stride_geometry(la.arr, la.n, ndim, in_channels, DTYPES[dtype], count, ctypes.byref(ws),
+                                           ctypes.byref(fl)), "dss_chain_stride_geometry")
+    return ws.value, fl.value
 
 
 def _stream(stream):
@@ -255,6 +269,30 @@ class Plan:
         ws = workspace if workspace is not None else self.workspace(H, W, signal.device, ell)
         _check(lib().dss_eval_slide(self.handle, _ptr(signal), H, W, ell, j, _ptr(out), _ptr(ws), ws.numel(),
                                     _stream(stream)), "dss_eval_slide")
+        return out
+
+    def stride_geometry(self, count):
+        """(workspace bytes, conv flops) of eval_stride on a batch of `count` windows."""
+        ws = ctypes.c_int64()
+        fl = ctypes.c_double()
+        _check(lib().dss_plan_stride_geometry(self.handle, count, ctypes.byref(ws), ctypes.byref(fl)),
+               "dss_plan_stride_geometry")
+        return ws.value, fl.value
+
+    def eval_stride(self, signal, first, count, out=None, workspace=None, stream=None):
+        """Patch-by-patch baseline on windows first..first+count-1 (row-major);
+        writes those positions of `out` ([out_c][H-B_h+1][W-B_w+1], allocated if None)."""
+        import torch
+        self._check_signal(signal)
+        _, H, W = signal.shape
+        if out is None:
+            g = self.geometry(H, W)
+            out = torch.zeros((g["out_c"], g["out_h"], g["out_w"]), dtype=torch.float32, device=signal.device)
+        if workspace is None:
+            need = self.stride_geometry(count)[0]
+            workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=signal.device)
+        _check(lib().dss_eval_stride(self.handle, _ptr(signal), H, W, first, count, _ptr(out), _ptr(workspace),
+                                     workspace.numel(), _stream(stream)), "dss_eval_stride")
         return out
 
     def set_timing(self, on=True):

@@ -247,3 +247,38 @@ def test_mixed_level_out_of_range(ell):
     with pytest.raises(dss.DssError) as e:
         dss.chain_layer_geometry(layers, 2, 3, 512, 512, 1, ell=ell)
     assert e.value.status == 1
+
+
+# ----------------------------------------------------------------------------- strided baseline geometry
+
+
+@pytest.mark.parametrize("L", [1, 4, 7, 12, 15])
+def test_stride_geometry_flops(L):
+    """Conv flops of the patch-by-patch baseline: per window sum_j 2 E_j,h E_j,w Cout Cin c_h c_w
+    with E_j = k_j u_j = u_{j-1} - c_j + 1 (Lemma (a)), times the batch size; the
+    workspace grows linearly with the batch."""
+    layers = wl.init_layers(wl.arch_paper_sweep(L, maps=16), np.random.default_rng(0))
+    ch = mixed.chain_of(layers)
+    us = mixed.strided_extents(ch)
+    per = 0.0
+    for j, e in enumerate(ch, start=1):
+        if e["conv"] is not None:
+            Eh, Ew = e["k"][0] * us[j][0], e["k"][1] * us[j][1]
+            assert (Eh, Ew) == (us[j - 1][0] - e["c"][0] + 1, us[j - 1][1] - e["c"][1] + 1)
+            c = e["conv"]
+            per += 2.0 * Eh * Ew * c["cout"] * c["cin"] * c["fh"] * c["fw"]
+    for count in (1, 7, 1000):
+        ws, fl = dss.chain_stride_geometry(layers, 2, 1, count)
+        assert fl == pytest.approx(count * per, rel=1e-12)
+        assert ws >= 2 * count * us[0][0] * us[0][1] * 4
+    # per window, the baseline does at least the dense evaluation's work per output
+    g = dss.chain_geometry(layers, 2, 1, 240, 320)
+    assert per >= g["conv_flops"] / (g["out_h"] * g["out_w"]) * (0.99 if L == 1 else 1.0)
+
+
+@pytest.mark.parametrize("count", [0, -3])
+def test_stride_geometry_rejects_empty_batch(count):
+    layers = wl.init_layers(wl.arch_c1(), np.random.default_rng(0))
+    with pytest.raises(dss.DssError) as e:
+        dss.chain_stride_geometry(layers, 2, 1, count)
+    assert e.value.status == 1
