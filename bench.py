@@ -19,6 +19,11 @@ evaluation against the patch-by-patch baseline (dss_eval_stride, all windows
 in memory-sized batches through the same kernels), and prints one JSON line
 with both times and the speed-up.
 
+`--fashion dilate` times the dilated fashion instead of the sliding one
+(appendix, Definition "evaldilate": the same dense output, computed on one
+full-resolution signal with dilated taps instead of fragments), for an A/B of
+the two schemes on the same kernels.
+
 `--ell l` (l > 0) times the mixed evaluation instead (appendix, Theorem
 "evalrelaxslide"): the first l chain layers pool with stride, and the output is
 the dense output downsampled by k*_l per axis; the metric then counts those
@@ -102,6 +107,8 @@ def main():
                     help="mixed level: chain layers 1..ell run relaxed (0 = dense evaluation)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run plain 1 GiB device-to-device copies (scales the HBM byte counters of a profiler)")
+    ap.add_argument("--fashion", default="slide", choices=("slide", "dilate"),
+                    help="dense evaluation scheme: fragments (slide) or dilated taps (dilate)")
     ap.add_argument("--sweep", action="store_true",
                     help="EvalSlide vs patch-by-patch EvalStride on the paper's 240x320 family, L = 1..15")
     ap.add_argument("--sweep-layers", default="1-15", help="range of L for --sweep, e.g. 1-15 or 12")
@@ -135,11 +142,21 @@ def main():
         x = x.to(torch.bfloat16)
     x = x.contiguous()
     out = torch.empty((g["out_c"], g["out_h"], g["out_w"]), dtype=torch.float32, device="cuda")
-    ws = plan.workspace(H, W, ell=ell)
+    if args.fashion == "dilate" and ell:
+        log("--fashion dilate evaluates the dense output; it does not combine with --ell")
+        sys.exit(2)
+    if args.fashion == "dilate":
+        _, _, need, dil_flops = plan.dilate_geometry(H, W, g["n_chain"])
+        ws = torch.empty(max(need, 256), dtype=torch.uint8, device="cuda")
+        g["conv_flops"] = dil_flops
+    else:
+        ws = plan.workspace(H, W, ell=ell)
     windows = g["out_h"] * g["out_w"]
 
     def step():
-        if ell == 0:
+        if args.fashion == "dilate":
+            plan.eval_dilate(x, out=out, workspace=ws)
+        elif ell == 0:
             plan.eval_dense(x, out=out, workspace=ws)
         else:
             plan.eval_mixed(x, ell, out=out, workspace=ws)
@@ -173,7 +190,8 @@ def main():
         ach = (domd["flops"] / domd["n"]) / (domd["ms"] / domd["n"]) / 1e9
         peak = PEAK_TFLOPS[w.dtype]
         roof = {"bound": "mfma", "kernel": dom["kernel"], "achieved": ach, "peak": peak, "unit": "TFLOP/s",
-                "frac": ach / peak, "traffic": profiled_traffic(dom["kernel"], args.config if ell == 0 else "%s_ell%d" % (args.config, ell)),
+                "frac": ach / peak, "traffic": profiled_traffic(dom["kernel"], args.config if ell == 0 and args.fashion == "slide"
+                                           else "%s_%s%d" % (args.config, args.fashion, ell)),
                 "traffic_unit": "bytes per launch (HBM, rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
                 "per_launch": {"flops": domd["flops"] / domd["n"], "avg_ms": domd["ms"] / domd["n"],
                                "launches_per_step": domd["n"] / args.steps}}
@@ -188,6 +206,8 @@ def main():
     config = {"workload": args.config + ": " + WORKLOAD_TEXT[args.config], "input": [C, H, W],
               "windows_per_step": windows, "receptive_field": [g["B_h"], g["B_w"]],
               "k_star": [g["K_h"], g["K_w"]], "conv_gflop_per_step": g["conv_flops"] / 1e9}
+    if args.fashion == "dilate":
+        config["fashion"] = "dilated taps on the full-resolution signal (no fragments)"
     if ell:
         config.update({"mixed_level": ell, "output_spacing": [g["step_h"], g["step_w"]],
                        "trimmed": [g["trim_h"], g["trim_w"]], "stuffed": [g["r_h"], g["r_w"]]})

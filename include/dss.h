@@ -264,6 +264,37 @@ dss_status dss_eval_stride(dss_plan_t plan, const void* signal, int32_t H, int32
                            int32_t count, float* out, void* workspace, int64_t workspace_bytes,
                            hipStream_t stream);
 
+/* ---------------------------------------------------------------- dilated fashion */
+
+/* Extents V_j,h x V_j,w of EvalDilate_j (Lemma "evaldilate" (a):
+ * V_j = N - sum_{mu <= j} k*_{mu-1} (c_mu + k_mu - 2) per axis), the workspace
+ * dss_eval_dilate needs and its algorithmic convolution flops (all layers), for a
+ * layer list (host only) or a plan.  Any output pointer may be NULL.
+ * DSS_E_SHAPE if the signal is smaller than the receptive field, DSS_E_INVALID if
+ * j is outside 0..L. */
+dss_status dss_chain_dilate_geometry(const dss_layer* layers, int32_t n_layers, int32_t ndim,
+                                     int32_t in_channels, dss_dtype dtype, int32_t H, int32_t W,
+                                     int32_t j, int32_t* V_h, int32_t* V_w, int64_t* workspace_bytes,
+                                     double* conv_flops);
+dss_status dss_plan_dilate_geometry(dss_plan_t plan, int32_t H, int32_t W, int32_t j, int32_t* V_h,
+                                    int32_t* V_w, int64_t* workspace_bytes, double* conv_flops);
+
+/* The network applied in the dilated fashion (appendix: Definition "evaldilate"):
+ * layer j applies its convolution and its max-pool to the whole signal with the
+ * taps k*_{j-1} samples apart (Definition "dilate"), with no stuffing,
+ * fragmentation or trimming; the intermediate EvalDilate_j for j = 0..L is
+ * returned.  By Lemma "evaldilate" (d) the strided network's layer-j output on
+ * the window at (i, w) is the u_j,h x u_j,w block of samples
+ * (i + k*_j,h a, w + k*_j,w b) of EvalDilate_j; for j = L this is the dense
+ * output itself, element for element the result of dss_eval_dense.
+ *   signal     device, [in_c][H][W] in the plan's dtype
+ *   out        device, binary32 [C_j][V_j,h][V_j,w] (for j = L: [out_c][H - B_h + 1][W - B_w + 1])
+ *   workspace  device scratch of at least the bytes dss_plan_dilate_geometry gives
+ *              (256-byte aligned)
+ * Errors: as dss_eval_dense, and DSS_E_INVALID if j is outside 0..L. */
+dss_status dss_eval_dilate(dss_plan_t plan, const void* signal, int32_t H, int32_t W, int32_t j,
+                           float* out, void* workspace, int64_t workspace_bytes, hipStream_t stream);
+
 /* ---------------------------------------------------------------- Frag / Defrag */
 
 /* Fragmentation Frag_k per axis (Definition "fragmentation" and Lemma

@@ -4,6 +4,8 @@
 //
 // Dense evaluation (Theorem "processing chain", Sect. 4.3):
 //   Stuff_r  ->  for j = 1..L: [conv T_j]  [sliding max-pool + Frag_{k_j}]  ->  Defrag_{k*_L} + Trim_r
+// Dilated evaluation (appendix, Definition "evaldilate"):
+//   pack  ->  for j = 1..L: [conv with taps k*_{j-1} apart] [max with taps k*_{j-1} apart]  ->  planar
 // Mixed evaluation at level ell (appendix, Theorem "evalrelaxslide"):
 //   Trim or Stuff  ->  for j <= ell: [conv T_j] [max-pool with stride k_j]
 //                  ->  for j > ell:  [conv T_j] [sliding max-pool + Frag_{k_j}]
@@ -430,17 +432,30 @@ static dss_status run_layers(dss_plan* p, const Geom& G, int upto, char* const b
                                  (double)c.cout * c.cin * c.c_h * c.c_w * es;
             e = T.run(conv_name(pc, tout), j, flops, bytes, [&]() -> hipError_t {
                 if (pc.impl == CONV_MFMA_F32)
-                    return launch_conv_mfma_f32((const float*)cur, Fin, lg.Uin_h, lg.Uin_w, pc, (float*)dst, stream);
+                    return launch_conv_mfma_f32((const float*)cur, Fin, lg.Uin_h, lg.Uin_w, lg.dil_h, lg.dil_w, pc,
+                                                (float*)dst, stream);
                 if (pc.impl == CONV_MFMA_BF16)
-                    return launch_conv_mfma_bf16(tout, (const uint16_t*)cur, Fin, lg.Uin_h, lg.Uin_w, pc, dst, stream);
-                return launch_conv_direct(cdt, tout, cur, Fin, lg.Uin_h, lg.Uin_w, c.cin, pc, dst, stream);
+                    return launch_conv_mfma_bf16(tout, (const uint16_t*)cur, Fin, lg.Uin_h, lg.Uin_w, lg.dil_h,
+                                                 lg.dil_w, pc, dst, stream);
+                return launch_conv_direct(cdt, tout, cur, Fin, lg.Uin_h, lg.Uin_w, lg.dil_h, lg.dil_w, c.cin, pc, dst,
+                                          stream);
             });
             if (e != hipSuccess) return hip_fail(e, "conv launch");
             which ^= 1;
             cur = dst;
             cdt = tout;
         }
-        if (c.has_pool && lg.relaxed) {
+        if (c.has_pool && lg.dilated) {
+            void* dst = buf[which ^ 1];
+            const double bytes = ((double)lg.E_h * lg.E_w + (double)lg.U_h * lg.U_w) * c.cout * dtype_size(cdt);
+            e = T.run("pool_dilate", j, 0.0, bytes, [&] {
+                return launch_pool_dilate(cdt, cur, lg.E_h, lg.E_w, c.cout, c.k_h, c.k_w, lg.dil_h, lg.dil_w, dst,
+                                          stream);
+            });
+            if (e != hipSuccess) return hip_fail(e, "pool_dilate launch");
+            which ^= 1;
+            cur = dst;
+        } else if (c.has_pool && lg.relaxed) {
             void* dst = buf[which ^ 1];
             const double bytes = (double)Fin * ((double)lg.E_h * lg.E_w + (double)lg.U_h * lg.U_w) * c.cout *
                                  dtype_size(cdt);
@@ -623,6 +638,73 @@ extern "C" dss_status dss_eval_stride(dss_plan_t plan, const void* signal, int32
         return launch_window_scatter(cdt, cur, count, ch.out_c(), first, (int64_t)O_h * O_w, out, stream);
     });
     if (e != hipSuccess) return hip_fail(e, "window_scatter launch");
+    return DSS_OK;
+}
+
+// ------------------------------------------------------------------ dilated fashion
+
+static dss_status dilate_geometry_out(const Chain& ch, const Geom& G, int j, int32_t* V_h, int32_t* V_w,
+                                      int64_t* workspace_bytes, double* conv_flops) {
+    if (j < 0 || j > ch.L()) return fail(DSS_E_INVALID, "chain layer %d out of range 0..%d", j, ch.L());
+    if (V_h) *V_h = j == 0 ? G.H : G.L[j - 1].U_h;
+    if (V_w) *V_w = j == 0 ? G.W : G.L[j - 1].U_w;
+    if (workspace_bytes) *workspace_bytes = G.ws_bytes;
+    if (conv_flops) *conv_flops = G.conv_flops;
+    return DSS_OK;
+}
+
+extern "C" dss_status dss_chain_dilate_geometry(const dss_layer* layers, int32_t n_layers, int32_t ndim,
+                                                int32_t in_channels, dss_dtype dtype, int32_t H, int32_t W, int32_t j,
+                                                int32_t* V_h, int32_t* V_w, int64_t* workspace_bytes,
+                                                double* conv_flops) {
+    if (dtype != DSS_F32 && dtype != DSS_BF16) return fail(DSS_E_UNSUPPORTED, "unknown dtype %d", dtype);
+    Chain ch;
+    dss_status s = build_chain(layers, n_layers, ndim, in_channels, &ch);
+    if (s != DSS_OK) return s;
+    Geom G;
+    s = compute_dilate_geometry(ch, dtype, H, W, &G);
+    if (s != DSS_OK) return s;
+    return dilate_geometry_out(ch, G, j, V_h, V_w, workspace_bytes, conv_flops);
+}
+
+extern "C" dss_status dss_plan_dilate_geometry(dss_plan_t plan, int32_t H, int32_t W, int32_t j, int32_t* V_h,
+                                               int32_t* V_w, int64_t* workspace_bytes, double* conv_flops) {
+    if (!plan) return fail(DSS_E_INVALID, "NULL plan");
+    Geom G;
+    dss_status s = compute_dilate_geometry(plan->chain, plan->dtype, H, W, &G);
+    if (s != DSS_OK) return s;
+    return dilate_geometry_out(plan->chain, G, j, V_h, V_w, workspace_bytes, conv_flops);
+}
+
+extern "C" dss_status dss_eval_dilate(dss_plan_t plan, const void* signal, int32_t H, int32_t W, int32_t j, float* out,
+                                      void* workspace, int64_t workspace_bytes, hipStream_t stream) {
+    if (!plan || !signal || !out) return fail(DSS_E_INVALID, "NULL plan, signal or out");
+    const Chain& ch = plan->chain;
+    if (j < 0 || j > ch.L()) return fail(DSS_E_INVALID, "chain layer %d out of range 0..%d", j, ch.L());
+    Geom G;
+    dss_status s = compute_dilate_geometry(ch, plan->dtype, H, W, &G);
+    if (s != DSS_OK) return s;
+    if (!workspace) return fail(DSS_E_INVALID, "NULL workspace (need %lld bytes)", (long long)G.ws_bytes);
+    if (workspace_bytes < G.ws_bytes)
+        return fail(DSS_E_SHAPE, "workspace of %lld bytes is smaller than the %lld bytes needed",
+                    (long long)workspace_bytes, (long long)G.ws_bytes);
+    if (((uintptr_t)workspace & 255u) != 0) return fail(DSS_E_INVALID, "workspace is not 256-byte aligned");
+    int cur_dev = -1;
+    hipError_t e = hipGetDevice(&cur_dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    if (cur_dev != plan->device)
+        return fail(DSS_E_INVALID, "plan belongs to device %d but device %d is current", plan->device, cur_dev);
+    Timer T(plan, stream);
+    void* cur = nullptr;
+    dss_dtype cdt;
+    s = run_chain(plan, G, signal, j, (char*)workspace, stream, T, &cur, &cdt);   // D = H x W: a plain pack
+    if (s != DSS_OK) return s;
+    const int h = j == 0 ? H : G.L[j - 1].U_h;
+    const int w = j == 0 ? W : G.L[j - 1].U_w;
+    const int C = j == 0 ? ch.in_c : ch.layers[j - 1].cout;
+    const double bytes = (double)h * w * C * (dtype_size(cdt) + 4.0);
+    e = T.run("to_planar", ch.L() + 1, 0.0, bytes, [&] { return launch_to_planar(cdt, cur, 1, h, w, C, out, stream); });
+    if (e != hipSuccess) return hip_fail(e, "to_planar launch");
     return DSS_OK;
 }
 

@@ -280,4 +280,68 @@ dss_status compute_stride_geometry(const Chain& ch, dss_dtype dt, int count, Geo
     return DSS_OK;
 }
 
+// The dilated fashion (appendix, Definition "evaldilate"): layer j applies the
+// convolution and the pooling kernel with their taps k*_{j-1} samples apart, on
+// one signal; no stuffing.  Extents per axis: E_j = V_{j-1} - k*_{j-1}(c_j - 1),
+// V_j = E_j - k*_{j-1}(k_j - 1), checked against Lemma "evaldilate" (a), (b).
+dss_status compute_dilate_geometry(const Chain& ch, dss_dtype dt, int H, int W, Geom* g) {
+    if (ch.ndim == 1 && H != 1) return fail(DSS_E_SHAPE, "1-D plan needs H = 1 (got %d)", H);
+    if (H < ch.B_h || W < ch.B_w)
+        return fail(DSS_E_SHAPE, "signal %dx%d is smaller than the receptive field %dx%d", H, W, ch.B_h, ch.B_w);
+    const int L = ch.L();
+    Geom G;
+    G.H = G.D_h = H;
+    G.W = G.D_w = W;
+    G.out_h = H - ch.B_h + 1;
+    G.out_w = W - ch.B_w + 1;
+    const double es = (double)dtype_size(dt);
+    int Vh = H, Vw = W;
+    int64_t maxbuf = (int64_t)H * W * ch.in_c * (int64_t)es;
+    G.total_bytes = 2.0 * (double)H * W * ch.in_c * es;
+    int64_t sum_h = 0, sum_w = 0;
+    for (int j = 1; j <= L; ++j) {
+        const ChainLayer& c = ch.layers[j - 1];
+        LayerGeom lg;
+        lg.dilated = true;
+        lg.dil_h = ch.kstar_h[j - 1];
+        lg.dil_w = ch.kstar_w[j - 1];
+        lg.Uin_h = Vh;
+        lg.Uin_w = Vw;
+        lg.Fin_h = lg.Fin_w = lg.Fout_h = lg.Fout_w = 1;
+        lg.E_h = Vh - lg.dil_h * (c.c_h - 1);
+        lg.E_w = Vw - lg.dil_w * (c.c_w - 1);
+        lg.U_h = lg.E_h - lg.dil_h * (c.k_h - 1);
+        lg.U_w = lg.E_w - lg.dil_w * (c.k_w - 1);
+        sum_h += (int64_t)ch.kstar_h[j - 1] * (c.c_h + c.k_h - 2);
+        sum_w += (int64_t)ch.kstar_w[j - 1] * (c.c_w + c.k_w - 2);
+        if (lg.U_h != (int64_t)H - sum_h || lg.U_w != (int64_t)W - sum_w ||
+            (int64_t)lg.U_h - (int64_t)ch.kstar_h[j] * (ch.u_h[j] - 1) != (int64_t)H - ch.B_h + 1 ||
+            (int64_t)lg.U_w - (int64_t)ch.kstar_w[j] * (ch.u_w[j] - 1) != (int64_t)W - ch.B_w + 1)
+            return fail(DSS_E_SHAPE, "layer %d: dilated extents disagree with Lemma \"evaldilate\"", j);
+        const bool last_op = (j == L) && !c.has_pool;
+        if (c.has_conv) {
+            const double es_out = (dt == DSS_BF16 && last_op) ? 4.0 : es;
+            G.conv_flops += 2.0 * (double)lg.E_h * lg.E_w * c.cout * (double)c.cin * c.c_h * c.c_w;
+            const int64_t out_b = (int64_t)lg.E_h * lg.E_w * c.cout * (int64_t)es_out;
+            maxbuf = std::max(maxbuf, out_b);
+            G.total_bytes += (double)Vh * Vw * c.cin * es + (double)out_b +
+                             (double)c.cout * c.cin * c.c_h * c.c_w * (dt == DSS_BF16 ? 2.0 : 4.0);
+        }
+        if (c.has_pool) {
+            const double pb = ((double)lg.E_h * lg.E_w + (double)lg.U_h * lg.U_w) * c.cout * es;
+            G.pool_bytes += pb;
+            G.total_bytes += pb;
+            maxbuf = std::max(maxbuf, (int64_t)lg.U_h * lg.U_w * c.cout * (int64_t)es);
+        }
+        G.L.push_back(lg);
+        Vh = lg.U_h;
+        Vw = lg.U_w;
+    }
+    G.total_bytes += (double)Vh * Vw * ch.out_c() * 4.0;
+    G.buf_bytes = (maxbuf + 255) / 256 * 256;
+    G.ws_bytes = 2 * G.buf_bytes;
+    *g = std::move(G);
+    return DSS_OK;
+}
+
 }  // namespace dss

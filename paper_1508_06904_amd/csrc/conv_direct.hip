@@ -4,9 +4,10 @@
 // independently (Definition "fragmentwise evaluation", Sect. 4.2):
 //   out[f][y][x][o] = act( bias[o] + sum_{t_h, t_w, i} w[t_h][t_w][i][o] * in[f][y+t_h][x+t_w][i] )
 // for y < Hin - fh + 1, x < Win - fw + 1 (valid convolution, cross-correlation
-// tap order).  Used for the layers that do not suit the MFMA implicit GEMM: the
-// first layer (few input channels) and the final projections (few output
-// channels).  One thread computes COB consecutive output channels of one output
+// tap order).  In the dilated fashion (appendix, Definition "dilate") tap
+// (t_h, t_w) reads sample (y + dil_h t_h, x + dil_w t_w) of a single signal.
+// Used for the layers that do not suit the MFMA implicit GEMM: the first layer
+// (few input channels) and the final projections (few output channels).  One thread computes COB consecutive output channels of one output
 // sample; the weight reads are uniform across the wavefront and go through the
 // scalar cache.  Accumulation is binary32 (bfloat16 activations are widened).
 #include "dev_common.h"
@@ -17,8 +18,9 @@ namespace dss {
 template <typename Tin, typename Tout, int COB, int VEC>
 __global__ __launch_bounds__(256) void conv_direct_kernel(const Tin* __restrict__ in, int Hin, int Win, int Cin,
                                                          const float* __restrict__ w, const float* __restrict__ bias,
-                                                         int fh, int fw, int Cout, int CoutP, int act,
-                                                         Tout* __restrict__ out, int Hout, int Wout, int64_t npix) {
+                                                         int fh, int fw, int dil_h, int dil_w, int Cout,
+                                                         int CoutP, int act, Tout* __restrict__ out, int Hout,
+                                                         int Wout, int64_t npix) {
     const int64_t p = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (p >= npix) return;
     const int og = blockIdx.y * COB;
@@ -32,7 +34,7 @@ __global__ __launch_bounds__(256) void conv_direct_kernel(const Tin* __restrict_
     for (int o = 0; o < COB; ++o) acc[o] = bias[og + o];
     for (int th = 0; th < fh; ++th) {
         for (int tw = 0; tw < fw; ++tw) {
-            const Tin* px = base + ((int64_t)th * Win + tw) * Cin;
+            const Tin* px = base + ((int64_t)th * dil_h * Win + (int64_t)tw * dil_w) * Cin;
             const float* wr = w + (int64_t)((th * fw + tw) * Cin) * CoutP + og;
             for (int i = 0; i < Cin; i += VEC) {
                 float v[VEC];
@@ -52,42 +54,42 @@ __global__ __launch_bounds__(256) void conv_direct_kernel(const Tin* __restrict_
 }
 
 template <typename Tin, typename Tout, int COB>
-static void run_direct(const void* in, int F, int Hin, int Win, int Cin, const PlanConv& pc, void* out,
+static void run_direct(const void* in, int F, int Hin, int Win, int dh, int dw, int Cin, const PlanConv& pc, void* out,
                        hipStream_t s) {
-    const int Hout = Hin - pc.fh + 1, Wout = Win - pc.fw + 1;
+    const int Hout = Hin - dh * (pc.fh - 1), Wout = Win - dw * (pc.fw - 1);
     const int64_t npix = (int64_t)F * Hout * Wout;
     const dim3 grid((unsigned)ceil_div64(npix, 256), (unsigned)(pc.cout_pad / COB));
     const int vec_ok = (Cin % 4 == 0);
     if (vec_ok)
         conv_direct_kernel<Tin, Tout, COB, 4><<<grid, 256, 0, s>>>((const Tin*)in, Hin, Win, Cin, (const float*)pc.w,
-                                                                   pc.b, pc.fh, pc.fw, pc.cout, pc.cout_pad, pc.act,
+                                                                   pc.b, pc.fh, pc.fw, dh, dw, pc.cout, pc.cout_pad, pc.act,
                                                                    (Tout*)out, Hout, Wout, npix);
     else
         conv_direct_kernel<Tin, Tout, COB, 1><<<grid, 256, 0, s>>>((const Tin*)in, Hin, Win, Cin, (const float*)pc.w,
-                                                                   pc.b, pc.fh, pc.fw, pc.cout, pc.cout_pad, pc.act,
+                                                                   pc.b, pc.fh, pc.fw, dh, dw, pc.cout, pc.cout_pad, pc.act,
                                                                    (Tout*)out, Hout, Wout, npix);
 }
 
 template <typename Tin, typename Tout>
-static void dispatch_cob(const void* in, int F, int Hin, int Win, int Cin, const PlanConv& pc, void* out,
-                         hipStream_t s) {
+static void dispatch_cob(const void* in, int F, int Hin, int Win, int dh, int dw, int Cin, const PlanConv& pc,
+                         void* out, hipStream_t s) {
     switch (pc.cob) {
-        case 16: run_direct<Tin, Tout, 16>(in, F, Hin, Win, Cin, pc, out, s); break;
-        case 8: run_direct<Tin, Tout, 8>(in, F, Hin, Win, Cin, pc, out, s); break;
-        case 4: run_direct<Tin, Tout, 4>(in, F, Hin, Win, Cin, pc, out, s); break;
-        case 2: run_direct<Tin, Tout, 2>(in, F, Hin, Win, Cin, pc, out, s); break;
-        default: run_direct<Tin, Tout, 1>(in, F, Hin, Win, Cin, pc, out, s); break;
+        case 16: run_direct<Tin, Tout, 16>(in, F, Hin, Win, dh, dw, Cin, pc, out, s); break;
+        case 8: run_direct<Tin, Tout, 8>(in, F, Hin, Win, dh, dw, Cin, pc, out, s); break;
+        case 4: run_direct<Tin, Tout, 4>(in, F, Hin, Win, dh, dw, Cin, pc, out, s); break;
+        case 2: run_direct<Tin, Tout, 2>(in, F, Hin, Win, dh, dw, Cin, pc, out, s); break;
+        default: run_direct<Tin, Tout, 1>(in, F, Hin, Win, dh, dw, Cin, pc, out, s); break;
     }
 }
 
-hipError_t launch_conv_direct(dss_dtype tin, dss_dtype tout, const void* in, int F, int Hin, int Win, int Cin,
-                              const PlanConv& pc, void* out, hipStream_t s) {
+hipError_t launch_conv_direct(dss_dtype tin, dss_dtype tout, const void* in, int F, int Hin, int Win, int dil_h,
+                              int dil_w, int Cin, const PlanConv& pc, void* out, hipStream_t s) {
     if (tin == DSS_F32)
-        dispatch_cob<float, float>(in, F, Hin, Win, Cin, pc, out, s);
+        dispatch_cob<float, float>(in, F, Hin, Win, dil_h, dil_w, Cin, pc, out, s);
     else if (tout == DSS_F32)
-        dispatch_cob<uint16_t, float>(in, F, Hin, Win, Cin, pc, out, s);
+        dispatch_cob<uint16_t, float>(in, F, Hin, Win, dil_h, dil_w, Cin, pc, out, s);
     else
-        dispatch_cob<uint16_t, uint16_t>(in, F, Hin, Win, Cin, pc, out, s);
+        dispatch_cob<uint16_t, uint16_t>(in, F, Hin, Win, dil_h, dil_w, Cin, pc, out, s);
     return hipGetLastError();
 }
 

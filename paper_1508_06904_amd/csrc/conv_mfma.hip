@@ -30,6 +30,9 @@
 // the channels-last output layout; binary32 or bfloat16 (round to nearest even).
 #include <algorithm>
 
+#include <mutex>
+#include <vector>
+
 #include "dev_common.h"
 #include "dss_internal.h"
 
@@ -79,7 +82,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
     int fh, int fw, int Cout, int act, int nchunks,
     Tout* __restrict__ out,            // [F][Hout][Wout][Cout]
     int Hout, int Wout, int TH, int TW, int tilesY, int tilesX, int nbs, int dbl_halo,
-    int flat_h, int flat_w) {           // flat mode: input fragments of flat_h x flat_w (0: spatial tiles)
+    int flat_h, int flat_w,             // flat mode: input fragments of flat_h x flat_w (0: spatial tiles)
+    int dil_h, int dil_w) {             // dilated mode (> 1): taps dil apart on one signal, tiled by phase
     using Cfg = MfmaCfg<BF16, WGM, WGN, MT, NT>;
     constexpr int THREADS = Cfg::THREADS;
     constexpr int WSLOTS = Cfg::WSLOTS;
@@ -150,7 +154,18 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
             for (int v = 0; v < 16; ++v) acc[mt][nt][v] = 0.f;
 
     const size_t row_bytes = (size_t)Cin * Cfg::ES;
-    const char* in_tile = in + (((size_t)f * Hin + ty0) * Win + tx0) * row_bytes;
+    // Where the tile's halo lives.  Spatial tiles: fragment f, rows and columns
+    // adjacent.  Dilated mode: the "fragments" are the dil_h x dil_w phases of one
+    // signal; phase (py, px) holds samples (py + dil_h a, px + dil_w b), so a tap
+    // step is dil samples and every tile reads and writes one phase only.
+    const bool dilated = dil_h * dil_w > 1;
+    const int py = dilated ? f / dil_w : 0, px = dilated ? f - py * dil_w : 0;
+    const size_t row_step = (size_t)(dilated ? dil_h : 1) * Win * row_bytes;
+    const size_t col_step = (size_t)(dilated ? dil_w : 1) * row_bytes;
+    const size_t f_base = dilated ? ((size_t)py * Win + px) * row_bytes : (size_t)f * Hin * Win * row_bytes;
+    const int lim_h = dilated ? (Hin - py + dil_h - 1) / dil_h : Hin;   // samples of this phase / fragment
+    const int lim_w = dilated ? (Win - px + dil_w - 1) / dil_w : Win;
+    const char* in_tile = in + f_base + (size_t)ty0 * row_step + (size_t)tx0 * col_step;
     const int taps = fh * fw;
     const int steps = nchunks * taps;
     const char* w_nb = wp + (size_t)nb * steps * (Cfg::BN * kChunkBytes);
@@ -178,8 +193,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
             const int px = S / kSlotsPerRow, q = S - px * kSlotsPerRow;
             if (S < halo_slots && q < 4) {
                 const int dy = px / HW, dx = px - dy * HW;
-                const bool ok = ty0 + dy < Hin && tx0 + dx < Win && c_base + q * (16 / Cfg::ES) < Cin;
-                dma16(ok ? src_c + ((size_t)dy * Win + dx) * row_bytes + q * 16 : zero, dst + (r0 + wave * 64) * 16);
+                const bool ok = ty0 + dy < lim_h && tx0 + dx < lim_w && c_base + q * (16 / Cfg::ES) < Cin;
+                dma16(ok ? src_c + (size_t)dy * row_step + (size_t)dx * col_step + q * 16 : zero,
+                      dst + (r0 + wave * 64) * 16);
             }
         }
     };
@@ -284,6 +300,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
                 const int y = r / flat_w, x = r - y * flat_w;
                 ok = p < Win && y < Hout && x < Wout;
                 o = ((size_t)fr * Hout + y) * Wout + x;
+            } else if (dilated) {
+                const int y = py + dil_h * (ty0 + m / TW), x = px + dil_w * (tx0 + m % TW);
+                ok = y < Hout && x < Wout;
+                o = (size_t)y * Wout + x;
             } else {
                 const int y = ty0 + m / TW, x = tx0 + m % TW;
                 ok = y < Hout && x < Wout;
@@ -391,6 +411,19 @@ bool mfma_supports(bool bf16, int cout, int fh, int fw) {
     return pick_tile(256, bn, 1, 1, fh, fw, 64 * 1024).TH > 0 && pick_tile(256, bn, 64, 64, fh, fw, 64 * 1024).TH > 0;
 }
 
+// Dynamic LDS above 64 KB needs a per-kernel opt-in (once per instantiation).
+static hipError_t allow_large_lds(const void* kern, size_t lds) {
+    if (lds <= 64 * 1024) return hipSuccess;
+    static std::mutex mu;
+    static std::vector<const void*> done;
+    std::lock_guard<std::mutex> lock(mu);
+    for (const void* k : done)
+        if (k == kern) return hipSuccess;
+    hipError_t e = hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kMaxLds);
+    if (e == hipSuccess) done.push_back(kern);
+    return e;
+}
+
 // Flat-mode tile (TH = 1, TW = BM consecutive positions of the flattened
 // fragment batch) for fragments of Hin x Win input samples, or TH = 0 if its
 // single-row halo does not fit.
@@ -405,8 +438,29 @@ static Tile flat_tile(int BM, int BN, int Win, int fh, int fw, size_t lds_max) {
 }
 
 template <bool BF16, typename Tout, int WGM, int WGN, int MT, int NT>
-static hipError_t run_mfma(const void* in, int F, int Hin, int Win, const PlanConv& pc, void* out, hipStream_t s) {
+static hipError_t run_mfma(const void* in, int F, int Hin, int Win, int dil_h, int dil_w, const PlanConv& pc,
+                           void* out, hipStream_t s) {
     using Cfg = MfmaCfg<BF16, WGM, WGN, MT, NT>;
+    if (dil_h * dil_w > 1) {
+        // dilated: one signal, tiled per phase (the largest phase has ceil(Hout/dil_h) rows)
+        if (F != 1) return hipErrorInvalidValue;
+        const int Hout = Hin - dil_h * (pc.fh - 1), Wout = Win - dil_w * (pc.fw - 1);
+        const int Hp = (int)ceil_div64(Hout, dil_h), Wp = (int)ceil_div64(Wout, dil_w);
+        const Tile t = pick_tile(Cfg::BM, Cfg::BN, Hp, Wp, pc.fh, pc.fw, device_lds_limit());
+        if (t.TH == 0) return hipErrorInvalidConfiguration;
+        auto kern = conv_mfma_kernel<BF16, Tout, WGM, WGN, MT, NT>;
+        hipError_t e = allow_large_lds((const void*)kern, t.lds);
+        if (e != hipSuccess) return e;
+        const int tilesY = (int)ceil_div64(Hp, t.TH), tilesX = (int)ceil_div64(Wp, t.TW);
+        const int nbs = pc.cout_pad / Cfg::BN;
+        const int64_t nblocks = (int64_t)dil_h * dil_w * tilesY * tilesX * nbs;
+        if (nblocks >= (1ll << 31)) return hipErrorInvalidConfiguration;
+        kern<<<dim3((unsigned)nblocks), Cfg::THREADS, t.lds, s>>>(
+            (const char*)in, Hin, Win, pc.cin, (const char*)pc.w, pc.b, pc.fh, pc.fw, pc.cout, pc.act,
+            pc.cin_pad / Cfg::CC, (Tout*)out, Hout, Wout, t.TH, t.TW, tilesY, tilesX, nbs, t.dbl, 0, 0, dil_h,
+            dil_w);
+        return hipGetLastError();
+    }
     const int Hout = Hin - pc.fh + 1, Wout = Win - pc.fw + 1;
     Tile t = pick_tile(Cfg::BM, Cfg::BN, Hout, Wout, pc.fh, pc.fw, device_lds_limit());
     // Small fragments waste most of a spatial tile; reading the batch as one
@@ -425,14 +479,8 @@ static hipError_t run_mfma(const void* in, int F, int Hin, int Win, const PlanCo
     }
     if (t.TH == 0) return hipErrorInvalidConfiguration;
     auto kern = conv_mfma_kernel<BF16, Tout, WGM, WGN, MT, NT>;
-    if (t.lds > 64 * 1024) {
-        static bool attr_set = false;   // per instantiation
-        if (!attr_set) {
-            hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kMaxLds);
-            if (e != hipSuccess) return e;
-            attr_set = true;
-        }
-    }
+    hipError_t e = allow_large_lds((const void*)kern, t.lds);
+    if (e != hipSuccess) return e;
     const int nbs = pc.cout_pad / Cfg::BN;
     const int nchunks = pc.cin_pad / Cfg::CC;
     if (flat) {
@@ -442,7 +490,7 @@ static hipError_t run_mfma(const void* in, int F, int Hin, int Win, const PlanCo
         if (nblocks >= (1ll << 31)) return hipErrorInvalidConfiguration;
         kern<<<dim3((unsigned)nblocks), Cfg::THREADS, t.lds, s>>>(
             (const char*)in, 1, (int)flat_len, pc.cin, (const char*)pc.w, pc.b, pc.fh, pc.fw, pc.cout, pc.act,
-            nchunks, (Tout*)out, Hout, Wout, 1, t.TW, 1, tilesX, nbs, t.dbl, Hin, Win);
+            nchunks, (Tout*)out, Hout, Wout, 1, t.TW, 1, tilesX, nbs, t.dbl, Hin, Win, 1, 1);
         return hipGetLastError();
     }
     const int tilesY = (int)ceil_div64(Hout, t.TH), tilesX = (int)ceil_div64(Wout, t.TW);
@@ -450,29 +498,30 @@ static hipError_t run_mfma(const void* in, int F, int Hin, int Win, const PlanCo
     if (nblocks >= (1ll << 31)) return hipErrorInvalidConfiguration;
     kern<<<dim3((unsigned)nblocks), Cfg::THREADS, t.lds, s>>>(
         (const char*)in, Hin, Win, pc.cin, (const char*)pc.w, pc.b, pc.fh, pc.fw, pc.cout, pc.act, nchunks,
-        (Tout*)out, Hout, Wout, t.TH, t.TW, tilesY, tilesX, nbs, t.dbl, 0, 0);
+        (Tout*)out, Hout, Wout, t.TH, t.TW, tilesY, tilesX, nbs, t.dbl, 0, 0, 1, 1);
     return hipGetLastError();
 }
 
 template <bool BF16, typename Tout>
-static hipError_t dispatch_bn(const void* in, int F, int Hin, int Win, const PlanConv& pc, void* out, hipStream_t s) {
+static hipError_t dispatch_bn(const void* in, int F, int Hin, int Win, int dh, int dw, const PlanConv& pc, void* out,
+                              hipStream_t s) {
     switch (pc.bn) {
-        case 128: return run_mfma<BF16, Tout, 2, 2, 4, 2>(in, F, Hin, Win, pc, out, s);
-        case 64: return run_mfma<BF16, Tout, 4, 1, 2, 2>(in, F, Hin, Win, pc, out, s);
-        case 32: return run_mfma<BF16, Tout, 4, 1, 2, 1>(in, F, Hin, Win, pc, out, s);
+        case 128: return run_mfma<BF16, Tout, 2, 2, 4, 2>(in, F, Hin, Win, dh, dw, pc, out, s);
+        case 64: return run_mfma<BF16, Tout, 4, 1, 2, 2>(in, F, Hin, Win, dh, dw, pc, out, s);
+        case 32: return run_mfma<BF16, Tout, 4, 1, 2, 1>(in, F, Hin, Win, dh, dw, pc, out, s);
     }
     return hipErrorInvalidValue;
 }
 
-hipError_t launch_conv_mfma_f32(const float* in, int F, int Hin, int Win, const PlanConv& pc, float* out,
-                                hipStream_t s) {
-    return dispatch_bn<false, float>(in, F, Hin, Win, pc, out, s);
+hipError_t launch_conv_mfma_f32(const float* in, int F, int Hin, int Win, int dil_h, int dil_w, const PlanConv& pc,
+                                float* out, hipStream_t s) {
+    return dispatch_bn<false, float>(in, F, Hin, Win, dil_h, dil_w, pc, out, s);
 }
 
-hipError_t launch_conv_mfma_bf16(dss_dtype tout, const uint16_t* in, int F, int Hin, int Win, const PlanConv& pc,
-                                 void* out, hipStream_t s) {
-    if (tout == DSS_F32) return dispatch_bn<true, float>(in, F, Hin, Win, pc, out, s);
-    return dispatch_bn<true, uint16_t>(in, F, Hin, Win, pc, out, s);
+hipError_t launch_conv_mfma_bf16(dss_dtype tout, const uint16_t* in, int F, int Hin, int Win, int dil_h, int dil_w,
+                                 const PlanConv& pc, void* out, hipStream_t s) {
+    if (tout == DSS_F32) return dispatch_bn<true, float>(in, F, Hin, Win, dil_h, dil_w, pc, out, s);
+    return dispatch_bn<true, uint16_t>(in, F, Hin, Win, dil_h, dil_w, pc, out, s);
 }
 
 }  // namespace dss

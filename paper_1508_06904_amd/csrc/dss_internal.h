@@ -48,7 +48,9 @@ dss_status build_chain(const dss_layer* layers, int n, int ndim, int in_c, Chain
 
 // Geometry of one chain layer for a given trimmed/stuffed signal.
 struct LayerGeom {
-    bool relaxed;       // j <= ell: Stride_g (pool with stride k, no Frag), one fragment
+    bool relaxed = false;   // j <= ell: Stride_g (pool with stride k, no Frag), one fragment
+    bool dilated = false;   // dilated fashion: one signal, conv and pool taps dil_h x dil_w apart
+    int dil_h = 1, dil_w = 1;
     int Uin_h, Uin_w;   // fragment extent entering the layer (U_{j-1})
     int E_h, E_w;       // extent after T_j (U_{j-1} - c_j + 1)
     int U_h, U_w;       // extent after the pooling step (U_j, or W_j for a relaxed layer)
@@ -70,6 +72,9 @@ size_t dtype_size(dss_dtype dt);
 dss_status compute_geometry(const Chain& ch, dss_dtype dt, int H, int W, int ell, Geom* g);
 // EvalStride on a batch of `count` windows: every layer relaxed, Fin_h = count fragments.
 dss_status compute_stride_geometry(const Chain& ch, dss_dtype dt, int count, Geom* g);
+// EvalDilate on an H x W signal: one fragment, layer j's taps k*_{j-1} apart;
+// LayerGeom U = V_j (Lemma "evaldilate" (a)), E = extent after the convolution.
+dss_status compute_dilate_geometry(const Chain& ch, dss_dtype dt, int H, int W, Geom* g);
 
 // ------------------------------------------------------------------ plan
 enum ConvImpl { CONV_DIRECT = 0, CONV_MFMA_F32 = 1, CONV_MFMA_BF16 = 2 };
@@ -108,18 +113,23 @@ namespace dss {
 // Element types: binary32 activations are float, bfloat16 activations uint16_t bits.
 hipError_t launch_stuff_pack(dss_dtype dt, const void* in, int C, int H, int W, void* out, int D_h,
                              int D_w, hipStream_t s);
+// Convolutions over F fragments of Hin x Win; with dil_h x dil_w > 1 (F = 1) the
+// taps are dil samples apart (the dilated fashion) and the output has
+// Hin - dil_h (fh - 1) x Win - dil_w (fw - 1) samples.
 hipError_t launch_conv_direct(dss_dtype tin, dss_dtype tout, const void* in, int F, int Hin, int Win,
-                              int Cin, const PlanConv& pc, void* out, hipStream_t s);
-hipError_t launch_conv_mfma_f32(const float* in, int F, int Hin, int Win, const PlanConv& pc,
-                                float* out, hipStream_t s);
-hipError_t launch_conv_mfma_bf16(dss_dtype tout, const uint16_t* in, int F, int Hin, int Win,
-                                 const PlanConv& pc, void* out, hipStream_t s);
+                              int dil_h, int dil_w, int Cin, const PlanConv& pc, void* out, hipStream_t s);
+hipError_t launch_conv_mfma_f32(const float* in, int F, int Hin, int Win, int dil_h, int dil_w,
+                                const PlanConv& pc, float* out, hipStream_t s);
+hipError_t launch_conv_mfma_bf16(dss_dtype tout, const uint16_t* in, int F, int Hin, int Win, int dil_h,
+                                 int dil_w, const PlanConv& pc, void* out, hipStream_t s);
 hipError_t launch_pool_frag(dss_dtype dt, const void* in, int S_h, int S_w, int E_h, int E_w, int C,
                             int k_h, int k_w, void* out, hipStream_t s);
 hipError_t launch_patch_pack(dss_dtype dt, const void* in, int C, int H, int W, int O_w, int64_t first, int count,
                              int B_h, int B_w, void* out, hipStream_t s);
 hipError_t launch_window_scatter(dss_dtype dt, const void* in, int count, int C, int64_t first, int64_t plane,
                                  float* out, hipStream_t s);
+hipError_t launch_pool_dilate(dss_dtype dt, const void* in, int E_h, int E_w, int C, int k_h, int k_w, int dil_h,
+                              int dil_w, void* out, hipStream_t s);
 hipError_t launch_pool_stride(dss_dtype dt, const void* in, int E_h, int E_w, int C, int k_h, int k_w,
                               void* out, hipStream_t s);
 hipError_t launch_defrag_trim(dss_dtype dt, const void* in, int K_h, int K_w, int U_h, int U_w, int C,

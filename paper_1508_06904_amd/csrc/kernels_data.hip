@@ -17,6 +17,9 @@
 //               appendix): the maximum over non-overlapping k_h x k_w blocks of
 //               one channels-last signal, no fragmentation.  Every input sample
 //               is read exactly once.
+//  pool_dilate  Dilate_{(g_max, k*_{j-1})} of the dilated fashion (appendix,
+//               Definition "dilate"): the maximum over k_h x k_w samples that are
+//               dil samples apart, on one channels-last signal.
 //  defrag_trim  Defrag_{k*_L} and Trim_r (appendix lemma on the simplified
 //               defragmentation; Definition "stuff-trim"): dense output sample
 //               (i, j) is sample (i div K_h, j div K_w) of fragment
@@ -240,6 +243,57 @@ hipError_t launch_pool_stride(dss_dtype dt, const void* in, int E_h, int E_w, in
     } else {
         if (C % 4 == 0) run_pool_stride<float, 4>(in, E_h, E_w, C, k_h, k_w, out, s);
         else run_pool_stride<float, 1>(in, E_h, E_w, C, k_h, k_w, out, s);
+    }
+    return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ pool_dilate
+template <typename T, int V>
+__global__ __launch_bounds__(kThreads) void pool_dilate_kernel(const T* __restrict__ in, int E_w, int C, int k_h,
+                                                              int k_w, int dil_h, int dil_w, T* __restrict__ out,
+                                                              int P_h, int P_w) {
+    const int CV = C / V;
+    const int64_t total = (int64_t)P_h * P_w * CV;
+    const int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (idx >= total) return;
+    const int cv = (int)(idx % CV);
+    const int64_t t = idx / CV;
+    const int x = (int)(t % P_w);
+    const int y = (int)(t / P_w);
+    const T* src = in + ((int64_t)y * E_w + x) * C + cv * V;
+    float m[V];
+    VecIO<T, V>::load(src, m);
+    for (int a = 0; a < k_h; ++a) {
+        for (int b = 0; b < k_w; ++b) {
+            if ((a | b) == 0) continue;
+            float v[V];
+            VecIO<T, V>::load(src + ((int64_t)a * dil_h * E_w + (int64_t)b * dil_w) * C, v);
+#pragma unroll
+            for (int e = 0; e < V; ++e) m[e] = fmaxf(m[e], v[e]);
+        }
+    }
+    VecIO<T, V>::store(out + t * C + cv * V, m);
+}
+
+template <typename T, int V>
+static void run_pool_dilate(const void* in, int E_h, int E_w, int C, int k_h, int k_w, int dh, int dw, void* out,
+                            hipStream_t s) {
+    const int P_h = E_h - dh * (k_h - 1), P_w = E_w - dw * (k_w - 1);
+    const int64_t total = (int64_t)P_h * P_w * (C / V);
+    if (total <= 0) return;
+    pool_dilate_kernel<T, V><<<dim3((unsigned)ceil_div64(total, kThreads)), kThreads, 0, s>>>(
+        (const T*)in, E_w, C, k_h, k_w, dh, dw, (T*)out, P_h, P_w);
+}
+
+hipError_t launch_pool_dilate(dss_dtype dt, const void* in, int E_h, int E_w, int C, int k_h, int k_w, int dil_h,
+                              int dil_w, void* out, hipStream_t s) {
+    if (dt == DSS_BF16) {
+        if (C % 8 == 0) run_pool_dilate<uint16_t, 8>(in, E_h, E_w, C, k_h, k_w, dil_h, dil_w, out, s);
+        else if (C % 4 == 0) run_pool_dilate<uint16_t, 4>(in, E_h, E_w, C, k_h, k_w, dil_h, dil_w, out, s);
+        else run_pool_dilate<uint16_t, 1>(in, E_h, E_w, C, k_h, k_w, dil_h, dil_w, out, s);
+    } else {
+        if (C % 4 == 0) run_pool_dilate<float, 4>(in, E_h, E_w, C, k_h, k_w, dil_h, dil_w, out, s);
+        else run_pool_dilate<float, 1>(in, E_h, E_w, C, k_h, k_w, dil_h, dil_w, out, s);
     }
     return hipGetLastError();
 }

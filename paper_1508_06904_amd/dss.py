@@ -67,7 +67,8 @@ class LaunchRecord(ctypes.Structure):
 
 EXPORTS = ("dss_chain_geometry", "dss_chain_layer_geometry", "dss_plan_create", "dss_plan_destroy",
            "dss_plan_geometry", "dss_plan_layer_geometry", "dss_eval_dense", "dss_eval_mixed", "dss_eval_slide",
-           "dss_chain_stride_geometry", "dss_plan_stride_geometry", "dss_eval_stride", "dss_frag", "dss_defrag",
+           "dss_chain_stride_geometry", "dss_plan_stride_geometry", "dss_eval_stride", "dss_chain_dilate_geometry",
+           "dss_plan_dilate_geometry", "dss_eval_dilate", "dss_frag", "dss_defrag",
            "dss_plan_set_timing", "dss_plan_timings", "dss_status_string", "dss_last_error", "dss_version")
 
 _lib = None
@@ -94,6 +95,10 @@ def lib():
         L.dss_chain_stride_geometry.argtypes = [P(Layer), I32, I32, I32, I32, I32, P(I64), P(ctypes.c_double)]
         L.dss_plan_stride_geometry.argtypes = [VP, I32, P(I64), P(ctypes.c_double)]
         L.dss_eval_stride.argtypes = [VP, VP, I32, I32, I64, I32, VP, VP, I64, VP]
+        L.dss_chain_dilate_geometry.argtypes = [P(Layer), I32, I32, I32, I32, I32, I32, I32, P(I32), P(I32), P(I64),
+                                                P(ctypes.c_double)]
+        L.dss_plan_dilate_geometry.argtypes = [VP, I32, I32, I32, P(I32), P(I32), P(I64), P(ctypes.c_double)]
+        L.dss_eval_dilate.argtypes = [VP, VP, I32, I32, I32, VP, VP, I64, VP]
         L.dss_frag.argtypes = [I32, I32, I32, I32, I32, I32, I32, I32, VP, VP, VP]
         L.dss_defrag.argtypes = [I32, I32, I32, I32, I32, I32, I32, I32, VP, VP, VP]
         L.dss_plan_set_timing.argtypes = [VP, I32]
@@ -107,7 +112,8 @@ def lib():
         for name in ("dss_chain_geometry", "dss_chain_layer_geometry", "dss_plan_create", "dss_plan_geometry",
                      "dss_plan_layer_geometry", "dss_eval_dense", "dss_eval_mixed", "dss_eval_slide", "dss_frag",
                      "dss_defrag", "dss_plan_set_timing", "dss_plan_timings", "dss_plan_stride_geometry",
-                     "dss_chain_stride_geometry", "dss_eval_stride"):
+                     "dss_chain_stride_geometry", "dss_eval_stride", "dss_chain_dilate_geometry",
+                     "dss_plan_dilate_geometry", "dss_eval_dilate"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -164,6 +170,16 @@ def chain_stride_geometry(layers, ndim, in_channels, count, dtype="f32"):
     _check(lib().dss_chain_stride_geometry(la.arr, la.n, ndim, in_channels, DTYPES[dtype], count, ctypes.byref(ws),
                                            ctypes.byref(fl)), "dss_chain_stride_geometry")
     return ws.value, fl.value
+
+
+def chain_dilate_geometry(layers, ndim, in_channels, H, W, j, dtype="f32"):
+    """(V_h, V_w, workspace bytes, conv flops) of the dilated evaluation after layer j (host only)."""
+    la = _LayerArray(layers)
+    vh, vw, ws, fl = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int64(), ctypes.c_double()
+    _check(lib().dss_chain_dilate_geometry(la.arr, la.n, ndim, in_channels, DTYPES[dtype], H, W, j, ctypes.byref(vh),
+                                           ctypes.byref(vw), ctypes.byref(ws), ctypes.byref(fl)),
+           "dss_chain_dilate_geometry")
+    return vh.value, vw.value, ws.value, fl.value
 
 
 def _stream(stream):
@@ -269,6 +285,30 @@ class Plan:
         ws = workspace if workspace is not None else self.workspace(H, W, signal.device, ell)
         _check(lib().dss_eval_slide(self.handle, _ptr(signal), H, W, ell, j, _ptr(out), _ptr(ws), ws.numel(),
                                     _stream(stream)), "dss_eval_slide")
+        return out
+
+    def dilate_geometry(self, H, W, j):
+        """(V_h, V_w, workspace bytes, conv flops) of eval_dilate after layer j."""
+        vh, vw, ws, fl = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int64(), ctypes.c_double()
+        _check(lib().dss_plan_dilate_geometry(self.handle, H, W, j, ctypes.byref(vh), ctypes.byref(vw),
+                                              ctypes.byref(ws), ctypes.byref(fl)), "dss_plan_dilate_geometry")
+        return vh.value, vw.value, ws.value, fl.value
+
+    def eval_dilate(self, signal, j=None, out=None, workspace=None, stream=None):
+        """EvalDilate_j (default j = L, the dense output) as planar binary32 [C_j][V_h][V_w]."""
+        import torch
+        self._check_signal(signal)
+        _, H, W = signal.shape
+        n_chain = self.geometry(H, W)["n_chain"]
+        j = n_chain if j is None else j
+        vh, vw, need, _ = self.dilate_geometry(H, W, j)
+        if out is None:
+            C = self.in_channels if j == 0 else self.layer_geometry(H, W, j)["channels"]
+            out = torch.empty((C, vh, vw), dtype=torch.float32, device=signal.device)
+        if workspace is None:
+            workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=signal.device)
+        _check(lib().dss_eval_dilate(self.handle, _ptr(signal), H, W, j, _ptr(out), _ptr(workspace),
+                                     workspace.numel(), _stream(stream)), "dss_eval_dilate")
         return out
 
     def stride_geometry(self, count):

@@ -282,3 +282,40 @@ def test_stride_geometry_rejects_empty_batch(count):
     with pytest.raises(dss.DssError) as e:
         dss.chain_stride_geometry(layers, 2, 1, count)
     assert e.value.status == 1
+
+
+# ----------------------------------------------------------------------------- dilated fashion geometry
+
+from oracle import dilate as odilate  # noqa: E402
+
+
+@pytest.mark.parametrize("name", list(MIXED_ARCHS))
+def test_dilate_geometry_matches_oracle(name):
+    """V_j of every layer equals the oracle's EvalDilate_j extents; the last one is
+    the dense output; with no stuffing needed, the convolution work equals the
+    sliding evaluation's (the appendix's complexity remark: equal evaluation counts)."""
+    arch, C, nd = MIXED_ARCHS[name]
+    layers = wl.init_layers(arch, np.random.default_rng(0))
+    ch = mixed.chain_of(layers)
+    ks, us = mixed.stride_products(ch), mixed.strided_extents(ch)
+    B, K = us[0], ks[-1]
+    H = 1 if nd == 1 else B[0] - 1 + 2 * K[0]
+    W = B[1] - 1 + 3 * K[1]
+    x = np.random.default_rng(1).standard_normal((C, H, W))
+    for j in range(len(ch) + 1):
+        vh, vw, ws, fl = dss.chain_dilate_geometry(layers, nd, C, H, W, j)
+        assert (vh, vw) == odilate.eval_dilate(layers, x, upto=j).shape[1:]
+    g = dss.chain_geometry(layers, nd, C, H, W)
+    assert (g["r_h"], g["r_w"]) == (0, 0)
+    assert (vh, vw) == (g["out_h"], g["out_w"])
+    assert fl == g["conv_flops"]
+
+
+def test_dilate_geometry_errors():
+    layers = wl.init_layers(wl.arch_c1(), np.random.default_rng(0))
+    with pytest.raises(dss.DssError) as e:
+        dss.chain_dilate_geometry(layers, 2, 1, 27, 64, 3)
+    assert e.value.status == 2
+    with pytest.raises(dss.DssError) as e:
+        dss.chain_dilate_geometry(layers, 2, 1, 64, 64, 4)
+    assert e.value.status == 1
