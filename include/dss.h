@@ -295,6 +295,47 @@ dss_status dss_plan_dilate_geometry(dss_plan_t plan, int32_t H, int32_t W, int32
 dss_status dss_eval_dilate(dss_plan_t plan, const void* signal, int32_t H, int32_t W, int32_t j,
                            float* out, void* workspace, int64_t workspace_bytes, hipStream_t stream);
 
+/* ---------------------------------------------------------------- backward (binary32 plans) */
+
+/* Workspace bytes, number of weight-gradient and bias-gradient floats, and the
+ * algorithmic convolution flops (forward + weight gradient + input gradient) of
+ * dss_backward_dense on an H x W signal, for a layer list (host only) or a plan.
+ * with_signal_grad: nonzero if the gradient with respect to the signal is wanted
+ * (it adds the first layer's input-gradient convolution).  Output pointers may be
+ * NULL.  Errors as dss_chain_geometry. */
+dss_status dss_chain_backward_geometry(const dss_layer* layers, int32_t n_layers, int32_t ndim,
+                                       int32_t in_channels, int32_t H, int32_t W,
+                                       int32_t with_signal_grad, int64_t* workspace_bytes,
+                                       int64_t* weight_grad_floats, int64_t* bias_grad_floats,
+                                       double* flops);
+dss_status dss_plan_backward_geometry(dss_plan_t plan, int32_t H, int32_t W, int32_t with_signal_grad,
+                                      int64_t* workspace_bytes, int64_t* weight_grad_floats,
+                                      int64_t* bias_grad_floats, double* flops);
+
+/* Gradients of l = sum(grad_out * T(signal)) for the dense evaluation T of
+ * dss_eval_dense, for fine-tuning on whole signals (the transformed network is
+ * the same function as the strided one on every window; Sect. 6.2 notes that
+ * Stuff and Trim have trivial gradients, Frag and Defrag are inverse
+ * permutations, and the sliding max-pool needs elementary calculus only).  The
+ * call runs the dense forward pass itself, keeping every layer's output in the
+ * workspace, then backpropagates through Trim, Defrag, each layer's sliding
+ * max-pool + Frag (the gradient of a window's maximum goes to its first maximal
+ * sample in row-major order), activation and convolution, and Stuff.  The result
+ * equals the sum over all windows of the strided network's gradients.
+ *   signal       device, [in_c][H][W] binary32
+ *   grad_out     device, binary32 [out_c][H - B_h + 1][W - B_w + 1]
+ *   grad_weight  device, binary32: the convolutions in descriptor order, each
+ *                [cout][cin][fh][fw] (cross-correlation order, like the weights),
+ *                concatenated; written, not accumulated
+ *   grad_bias    device, binary32: each convolution's [cout], concatenated
+ *   grad_signal  device, binary32 [in_c][H][W], or NULL to skip it
+ *   workspace    device scratch of dss_plan_backward_geometry bytes (256-byte aligned)
+ * Errors: DSS_E_UNSUPPORTED for bfloat16 plans; otherwise as dss_eval_dense. */
+dss_status dss_backward_dense(dss_plan_t plan, const void* signal, int32_t H, int32_t W,
+                              const float* grad_out, float* grad_weight, float* grad_bias,
+                              float* grad_signal, void* workspace, int64_t workspace_bytes,
+                              hipStream_t stream);
+
 /* ---------------------------------------------------------------- Frag / Defrag */
 
 /* Fragmentation Frag_k per axis (Definition "fragmentation" and Lemma

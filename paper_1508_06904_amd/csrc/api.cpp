@@ -65,15 +65,73 @@ uint16_t host_f32_to_bf16(float f) {
 // with the 32-channel N tile: the padded output channels cost MFMA cycles the
 // layer has to spare, while the direct kernel would be limited by its
 // uncoalesced reads of the wide input rows.
-static ConvImpl choose_impl(const ChainLayer& c, dss_dtype dt) {
+static ConvImpl choose_impl(int cin, int cout, int fh, int fw, dss_dtype dt) {
     // Tuning / cross-check override: DSS_CONV_KERNEL=direct selects the VALU
     // kernel for every convolution of plans created afterwards.
     const char* force = getenv("DSS_CONV_KERNEL");
     if (force && std::strcmp(force, "direct") == 0) return CONV_DIRECT;
-    if (c.cin < 16) return CONV_DIRECT;
-    if (dt == DSS_F32 && c.cin % 4 == 0 && mfma_supports(false, c.cout, c.c_h, c.c_w)) return CONV_MFMA_F32;
-    if (dt == DSS_BF16 && c.cin % 8 == 0 && mfma_supports(true, c.cout, c.c_h, c.c_w)) return CONV_MFMA_BF16;
+    if (cin < 16) return CONV_DIRECT;
+    if (dt == DSS_F32 && cin % 4 == 0 && mfma_supports(false, cout, fh, fw)) return CONV_MFMA_F32;
+    if (dt == DSS_BF16 && cin % 8 == 0 && mfma_supports(true, cout, fh, fw)) return CONV_MFMA_BF16;
     return CONV_DIRECT;
+}
+
+// Packs one convolution (weights [cout][cin][fh][fw] binary32, cross-correlation
+// order; bias [cout] or NULL) into the layout of the kernel chosen for it and
+// copies it to the current device.
+static dss_status upload_conv(int cin, int cout, int fh, int fw, int act, const float* weight, const float* bias_in,
+                              dss_dtype dtype, PlanConv& pc) {
+    pc.cin = cin;
+    pc.cout = cout;
+    pc.fh = fh;
+    pc.fw = fw;
+    pc.act = act;
+    pc.impl = choose_impl(cin, cout, fh, fw, dtype);
+    const bool bf16 = dtype == DSS_BF16;
+    std::vector<float> bias;
+    std::vector<char> wbuf;
+    size_t wbytes = 0;
+    if (pc.impl == CONV_DIRECT) {
+        // [fh][fw][cin][cout_pad] binary32 (bfloat16-rounded values for bfloat16 plans)
+        pc.cob = cout >= 16 ? 16 : cout >= 8 ? 8 : cout >= 4 ? 4 : cout >= 2 ? 2 : 1;
+        pc.cout_pad = (cout + pc.cob - 1) / pc.cob * pc.cob;
+        wbytes = sizeof(float) * (size_t)fh * fw * cin * pc.cout_pad;
+        wbuf.assign(wbytes, 0);
+        float* w = reinterpret_cast<float*>(wbuf.data());
+        for (int o = 0; o < cout; ++o)
+            for (int i = 0; i < cin; ++i)
+                for (int th = 0; th < fh; ++th)
+                    for (int tw = 0; tw < fw; ++tw) {
+                        float v = weight[(((size_t)o * cin + i) * fh + th) * fw + tw];
+                        if (bf16) {
+                            const uint32_t u = (uint32_t)host_f32_to_bf16(v) << 16;
+                            std::memcpy(&v, &u, 4);
+                        }
+                        w[(((size_t)th * fw + tw) * cin + i) * pc.cout_pad + o] = v;
+                    }
+    } else if (pc.impl == CONV_MFMA_F32) {
+        pc.bn = mfma_f32_pick_bn(cout);
+        pc.cin_pad = (cin + 15) / 16 * 16;
+        pc.cout_pad = (cout + pc.bn - 1) / pc.bn * pc.bn;
+        wbytes = sizeof(float) * mfma_f32_packed_floats(pc);
+        wbuf.assign(wbytes, 0);
+        mfma_f32_pack(pc, weight, reinterpret_cast<float*>(wbuf.data()));
+    } else {
+        pc.bn = mfma_bf16_pick_bn(cout);
+        pc.cin_pad = (cin + 31) / 32 * 32;
+        pc.cout_pad = (cout + pc.bn - 1) / pc.bn * pc.bn;
+        wbytes = sizeof(uint16_t) * mfma_bf16_packed_elems(pc);
+        wbuf.assign(wbytes, 0);
+        mfma_bf16_pack(pc, weight, reinterpret_cast<uint16_t*>(wbuf.data()));
+    }
+    bias.assign(pc.cout_pad, 0.f);
+    for (int o = 0; o < cout; ++o) bias[o] = bias_in ? bias_in[o] : 0.f;
+    hipError_t e = hipMalloc(&pc.w, wbytes);
+    if (e == hipSuccess) e = hipMalloc((void**)&pc.b, sizeof(float) * bias.size());
+    if (e == hipSuccess) e = hipMemcpy(pc.w, wbuf.data(), wbytes, hipMemcpyHostToDevice);
+    if (e == hipSuccess) e = hipMemcpy(pc.b, bias.data(), sizeof(float) * bias.size(), hipMemcpyHostToDevice);
+    if (e != hipSuccess) return hip_fail(e, "uploading weights");
+    return DSS_OK;
 }
 
 }  // namespace dss
@@ -208,12 +266,13 @@ extern "C" dss_status dss_plan_layer_geometry(dss_plan_t plan, int32_t H, int32_
 // ------------------------------------------------------------------ plans
 
 static void free_plan_memory(dss_plan* p) {
-    for (auto& c : p->convs) {
-        if (c.w) (void)hipFree(c.w);
-        if (c.b) (void)hipFree(c.b);
-        c.w = nullptr;
-        c.b = nullptr;
-    }
+    for (auto* list : {&p->convs, &p->bconvs})
+        for (auto& c : *list) {
+            if (c.w) (void)hipFree(c.w);
+            if (c.b) (void)hipFree(c.b);
+            c.w = nullptr;
+            c.b = nullptr;
+        }
     for (hipEvent_t e : p->events) (void)hipEventDestroy(e);
     p->events.clear();
 }
@@ -248,64 +307,24 @@ extern "C" dss_status dss_plan_create(const dss_layer* layers, int32_t n_layers,
     }
     const int L = p->chain.L();
     p->convs.resize(L);
+    if (dtype == DSS_F32) p->bconvs.resize(L);
     for (int j = 0; j < L; ++j) {
         const ChainLayer& c = p->chain.layers[j];
         if (!c.has_conv) continue;
         const dss_layer& d = layers[c.desc];
-        PlanConv& pc = p->convs[j];
-        pc.cin = c.cin;
-        pc.cout = c.cout;
-        pc.fh = c.c_h;
-        pc.fw = c.c_w;
-        pc.act = c.act;
-        pc.impl = choose_impl(c, dtype);
-        const bool bf16 = dtype == DSS_BF16;
-        std::vector<float> bias;
-        std::vector<char> wbuf;
-        size_t wbytes = 0;
-        if (pc.impl == CONV_DIRECT) {
-            // [fh][fw][cin][cout_pad] binary32 (bfloat16-rounded values for bfloat16 plans)
-            pc.cob = c.cout >= 16 ? 16 : c.cout >= 8 ? 8 : c.cout >= 4 ? 4 : c.cout >= 2 ? 2 : 1;
-            pc.cout_pad = (c.cout + pc.cob - 1) / pc.cob * pc.cob;
-            wbytes = sizeof(float) * (size_t)pc.fh * pc.fw * pc.cin * pc.cout_pad;
-            wbuf.assign(wbytes, 0);
-            float* w = reinterpret_cast<float*>(wbuf.data());
+        s = upload_conv(c.cin, c.cout, c.c_h, c.c_w, c.act, d.weight, d.bias, dtype, p->convs[j]);
+        if (s == DSS_OK && dtype == DSS_F32) {
+            // input gradient: w'[i][o][t_h][t_w] = w[o][i][fh-1-t_h][fw-1-t_w]
+            std::vector<float> wt((size_t)c.cin * c.cout * c.c_h * c.c_w);
             for (int o = 0; o < c.cout; ++o)
                 for (int i = 0; i < c.cin; ++i)
-                    for (int th = 0; th < pc.fh; ++th)
-                        for (int tw = 0; tw < pc.fw; ++tw) {
-                            float v = d.weight[(((size_t)o * c.cin + i) * pc.fh + th) * pc.fw + tw];
-                            if (bf16) {
-                                const uint32_t u = (uint32_t)host_f32_to_bf16(v) << 16;
-                                std::memcpy(&v, &u, 4);
-                            }
-                            w[(((size_t)th * pc.fw + tw) * pc.cin + i) * pc.cout_pad + o] = v;
-                        }
-            bias.assign(pc.cout_pad, 0.f);
-        } else if (pc.impl == CONV_MFMA_F32) {
-            pc.bn = mfma_f32_pick_bn(c.cout);
-            pc.cin_pad = (c.cin + 15) / 16 * 16;
-            pc.cout_pad = (c.cout + pc.bn - 1) / pc.bn * pc.bn;
-            wbytes = sizeof(float) * mfma_f32_packed_floats(pc);
-            wbuf.assign(wbytes, 0);
-            mfma_f32_pack(pc, d.weight, reinterpret_cast<float*>(wbuf.data()));
-            bias.assign(pc.cout_pad, 0.f);
-        } else {
-            pc.bn = mfma_bf16_pick_bn(c.cout);
-            pc.cin_pad = (c.cin + 31) / 32 * 32;
-            pc.cout_pad = (c.cout + pc.bn - 1) / pc.bn * pc.bn;
-            wbytes = sizeof(uint16_t) * mfma_bf16_packed_elems(pc);
-            wbuf.assign(wbytes, 0);
-            mfma_bf16_pack(pc, d.weight, reinterpret_cast<uint16_t*>(wbuf.data()));
-            bias.assign(pc.cout_pad, 0.f);
+                    for (int th = 0; th < c.c_h; ++th)
+                        for (int tw = 0; tw < c.c_w; ++tw)
+                            wt[(((size_t)i * c.cout + o) * c.c_h + (c.c_h - 1 - th)) * c.c_w + (c.c_w - 1 - tw)] =
+                                d.weight[(((size_t)o * c.cin + i) * c.c_h + th) * c.c_w + tw];
+            s = upload_conv(c.cout, c.cin, c.c_h, c.c_w, DSS_ACT_NONE, wt.data(), nullptr, dtype, p->bconvs[j]);
         }
-        for (int o = 0; o < c.cout; ++o) bias[o] = d.bias ? d.bias[o] : 0.f;
-        e = hipMalloc(&pc.w, wbytes);
-        if (e == hipSuccess) e = hipMalloc((void**)&pc.b, sizeof(float) * bias.size());
-        if (e == hipSuccess) e = hipMemcpy(pc.w, wbuf.data(), wbytes, hipMemcpyHostToDevice);
-        if (e == hipSuccess) e = hipMemcpy(pc.b, bias.data(), sizeof(float) * bias.size(), hipMemcpyHostToDevice);
-        if (e != hipSuccess) {
-            s = hip_fail(e, "uploading weights");
+        if (s != DSS_OK) {
             free_plan_memory(p);
             delete p;
             return s;
@@ -705,6 +724,245 @@ extern "C" dss_status dss_eval_dilate(dss_plan_t plan, const void* signal, int32
     const double bytes = (double)h * w * C * (dtype_size(cdt) + 4.0);
     e = T.run("to_planar", ch.L() + 1, 0.0, bytes, [&] { return launch_to_planar(cdt, cur, 1, h, w, C, out, stream); });
     if (e != hipSuccess) return hip_fail(e, "to_planar launch");
+    return DSS_OK;
+}
+
+// ------------------------------------------------------------------ backward
+
+namespace {
+
+// Workspace layout and work of the backward pass for one signal extent.
+struct BwdLayout {
+    Geom G;                                  // dense geometry (ell = 0)
+    std::vector<int64_t> a_off, c_off;       // byte offsets: A_0..A_L, conv outputs C_1..C_L
+    int64_t g_off[2] = {0, 0}, pad_off = 0, wpart_off = 0, bpart_off = 0, total = 0;
+    std::vector<WgradPlan> wg;               // per chain layer with a convolution
+    std::vector<int64_t> wofs, bofs;         // float offsets of each conv's gradients in the outputs
+    int64_t wfloats = 0, bfloats = 0;
+    double flops = 0;                        // forward + weight-gradient + input-gradient convolutions
+};
+
+int64_t align256(int64_t b) { return (b + 255) / 256 * 256; }
+
+dss_status backward_layout(const Chain& ch, int H, int W, bool want_dx, BwdLayout* out) {
+    BwdLayout B;
+    dss_status s = compute_geometry(ch, DSS_F32, H, W, 0, &B.G);
+    if (s != DSS_OK) return s;
+    const Geom& G = B.G;
+    const int L = ch.L();
+    int64_t off = 0;
+    auto take = [&](int64_t bytes) { const int64_t o = off; off += align256(bytes); return o; };
+    std::vector<int64_t> asz(L + 1), csz(L + 1, 0);
+    asz[0] = (int64_t)G.D_h * G.D_w * ch.in_c * 4;
+    B.a_off.assign(L + 1, 0);
+    B.c_off.assign(L + 1, 0);
+    B.a_off[0] = take(asz[0]);
+    int64_t gmax = asz[0], padmax = 0, wpmax = 0, bpmax = 0;
+    B.wg.resize(L + 1);
+    B.wofs.assign(L + 1, -1);
+    B.bofs.assign(L + 1, -1);
+    for (int j = 1; j <= L; ++j) {
+        const ChainLayer& c = ch.layers[j - 1];
+        const LayerGeom& lg = G.L[j - 1];
+        const int64_t Fin = (int64_t)lg.Fin_h * lg.Fin_w, Fout = (int64_t)lg.Fout_h * lg.Fout_w;
+        if (c.has_conv) csz[j] = Fin * lg.E_h * lg.E_w * c.cout * 4;
+        asz[j] = c.has_pool ? Fout * lg.U_h * lg.U_w * c.cout * 4 : csz[j];
+        if (c.has_conv && c.has_pool) B.c_off[j] = take(csz[j]);
+        B.a_off[j] = take(asz[j]);
+        if (c.has_conv && !c.has_pool) B.c_off[j] = B.a_off[j];
+        if (!c.has_conv) B.c_off[j] = B.a_off[j - 1];
+        gmax = std::max({gmax, asz[j], csz[j], asz[j - 1]});
+        if (c.has_conv) {
+            const double f = 2.0 * Fin * lg.E_h * lg.E_w * c.cout * (double)c.cin * c.c_h * c.c_w;
+            B.flops += 2.0 * f;                           // forward + weight gradient
+            if (j > 1 || want_dx) {
+                B.flops += f;                             // input gradient
+                padmax = std::max(padmax, Fin * (lg.E_h + 2 * (c.c_h - 1)) * (int64_t)(lg.E_w + 2 * (c.c_w - 1)) *
+                                              c.cout * 4);
+            }
+            B.wg[j] = wgrad_plan((int)Fin, lg.E_h, lg.E_w, c.cout, c.cin, c.c_h, c.c_w);
+            wpmax = std::max(wpmax, B.wg[j].partial_floats * 4);
+            bpmax = std::max(bpmax, (int64_t)bias_blocks(Fin * lg.E_h * lg.E_w) * c.cout * 4);
+            B.wofs[j] = B.wfloats;
+            B.bofs[j] = B.bfloats;
+            B.wfloats += (int64_t)c.cout * c.cin * c.c_h * c.c_w;
+            B.bfloats += c.cout;
+        }
+    }
+    B.g_off[0] = take(gmax);
+    B.g_off[1] = take(gmax);
+    B.pad_off = take(std::max<int64_t>(padmax, 256));
+    B.wpart_off = take(std::max<int64_t>(wpmax, 256));
+    B.bpart_off = take(std::max<int64_t>(bpmax, 256));
+    B.total = off;
+    *out = std::move(B);
+    return DSS_OK;
+}
+
+const char* dgrad_name(const PlanConv& pc) {
+    switch (pc.impl) {
+        case CONV_MFMA_F32:
+            return pc.bn == 128 ? "dgrad_mfma_f32_n128" : pc.bn == 64 ? "dgrad_mfma_f32_n64" : "dgrad_mfma_f32_n32";
+        default:
+            return "dgrad_direct";
+    }
+}
+
+}  // namespace
+
+static dss_status backward_geometry_out(const BwdLayout& B, int64_t* ws, int64_t* wf, int64_t* bf, double* flops) {
+    if (ws) *ws = B.total;
+    if (wf) *wf = B.wfloats;
+    if (bf) *bf = B.bfloats;
+    if (flops) *flops = B.flops;
+    return DSS_OK;
+}
+
+extern "C" dss_status dss_chain_backward_geometry(const dss_layer* layers, int32_t n_layers, int32_t ndim,
+                                                  int32_t in_channels, int32_t H, int32_t W, int32_t with_signal_grad,
+                                                  int64_t* workspace_bytes, int64_t* weight_grad_floats,
+                                                  int64_t* bias_grad_floats, double* flops) {
+    Chain ch;
+    dss_status s = build_chain(layers, n_layers, ndim, in_channels, &ch);
+    if (s != DSS_OK) return s;
+    BwdLayout B;
+    s = backward_layout(ch, H, W, with_signal_grad != 0, &B);
+    if (s != DSS_OK) return s;
+    return backward_geometry_out(B, workspace_bytes, weight_grad_floats, bias_grad_floats, flops);
+}
+
+extern "C" dss_status dss_plan_backward_geometry(dss_plan_t plan, int32_t H, int32_t W, int32_t with_signal_grad,
+                                                 int64_t* workspace_bytes, int64_t* weight_grad_floats,
+                                                 int64_t* bias_grad_floats, double* flops) {
+    if (!plan) return fail(DSS_E_INVALID, "NULL plan");
+    BwdLayout B;
+    dss_status s = backward_layout(plan->chain, H, W, with_signal_grad != 0, &B);
+    if (s != DSS_OK) return s;
+    return backward_geometry_out(B, workspace_bytes, weight_grad_floats, bias_grad_floats, flops);
+}
+
+extern "C" dss_status dss_backward_dense(dss_plan_t plan, const void* signal, int32_t H, int32_t W,
+                                         const float* grad_out, float* grad_weight, float* grad_bias,
+                                         float* grad_signal, void* workspace, int64_t workspace_bytes,
+                                         hipStream_t stream) {
+    if (!plan || !signal || !grad_out || !grad_weight || !grad_bias)
+        return fail(DSS_E_INVALID, "NULL plan, signal, grad_out, grad_weight or grad_bias");
+    if (plan->dtype != DSS_F32) return fail(DSS_E_UNSUPPORTED, "the backward pass is implemented for binary32 plans");
+    const Chain& ch = plan->chain;
+    BwdLayout B;
+    dss_status s = backward_layout(ch, H, W, grad_signal != nullptr, &B);
+    if (s != DSS_OK) return s;
+    if (!workspace) return fail(DSS_E_INVALID, "NULL workspace (need %lld bytes)", (long long)B.total);
+    if (workspace_bytes < B.total)
+        return fail(DSS_E_SHAPE, "workspace of %lld bytes is smaller than the %lld bytes needed",
+                    (long long)workspace_bytes, (long long)B.total);
+    if (((uintptr_t)workspace & 255u) != 0) return fail(DSS_E_INVALID, "workspace is not 256-byte aligned");
+    int cur_dev = -1;
+    hipError_t e = hipGetDevice(&cur_dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    if (cur_dev != plan->device)
+        return fail(DSS_E_INVALID, "plan belongs to device %d but device %d is current", plan->device, cur_dev);
+
+    const Geom& G = B.G;
+    const int L = ch.L();
+    char* ws = (char*)workspace;
+    auto A = [&](int j) { return (float*)(ws + B.a_off[j]); };
+    auto Cv = [&](int j) { return (float*)(ws + B.c_off[j]); };
+    float* gb[2] = {(float*)(ws + B.g_off[0]), (float*)(ws + B.g_off[1])};
+    float* padb = (float*)(ws + B.pad_off);
+    float* wpart = (float*)(ws + B.wpart_off);
+    float* bpart = (float*)(ws + B.bpart_off);
+    Timer T(plan, stream);
+
+    // forward, keeping every layer's convolution output and pool output
+    e = T.run("stuff_pack", 0, 0.0, (double)ch.in_c * ((double)H * W + (double)G.D_h * G.D_w) * 4.0, [&] {
+        return launch_stuff_pack(DSS_F32, signal, ch.in_c, H, W, A(0), G.D_h, G.D_w, stream);
+    });
+    if (e != hipSuccess) return hip_fail(e, "stuff_pack launch");
+    for (int j = 1; j <= L; ++j) {
+        const ChainLayer& c = ch.layers[j - 1];
+        const LayerGeom& lg = G.L[j - 1];
+        const int Fin = lg.Fin_h * lg.Fin_w;
+        if (c.has_conv) {
+            const PlanConv& pc = plan->convs[j - 1];
+            const double fl = 2.0 * Fin * (double)lg.E_h * lg.E_w * c.cout * (double)c.cin * c.c_h * c.c_w;
+            e = T.run(conv_name(pc, DSS_F32), j, fl, 0.0, [&]() -> hipError_t {
+                if (pc.impl == CONV_MFMA_F32)
+                    return launch_conv_mfma_f32(A(j - 1), Fin, lg.Uin_h, lg.Uin_w, 1, 1, pc, Cv(j), stream);
+                return launch_conv_direct(DSS_F32, DSS_F32, A(j - 1), Fin, lg.Uin_h, lg.Uin_w, 1, 1, c.cin, pc, Cv(j),
+                                          stream);
+            });
+            if (e != hipSuccess) return hip_fail(e, "conv launch");
+        }
+        if (c.has_pool) {
+            e = T.run("pool_frag", j, 0.0, 0.0, [&] {
+                return launch_pool_frag(DSS_F32, Cv(j), lg.Fin_h, lg.Fin_w, lg.E_h, lg.E_w, c.cout, c.k_h, c.k_w, A(j),
+                                        stream);
+            });
+            if (e != hipSuccess) return hip_fail(e, "pool_frag launch");
+        }
+    }
+
+    // upstream gradient into the final fragment layout (transpose of Defrag + Trim)
+    int cur = 0;
+    e = T.run("frag_scatter_grad", L + 1, 0.0, 0.0, [&] {
+        return launch_frag_scatter_grad(grad_out, ch.out_c(), G.out_h, G.out_w, ch.K_h(), ch.K_w(), G.L.back().U_h,
+                                        G.L.back().U_w, gb[cur], stream);
+    });
+    if (e != hipSuccess) return hip_fail(e, "frag_scatter_grad launch");
+    for (int j = L; j >= 1; --j) {
+        const ChainLayer& c = ch.layers[j - 1];
+        const LayerGeom& lg = G.L[j - 1];
+        const int Fin = lg.Fin_h * lg.Fin_w;
+        if (c.has_pool) {
+            const int act = c.has_conv ? c.act : DSS_ACT_NONE;
+            e = T.run("pool_frag_backward", j, 0.0, 0.0, [&] {
+                return launch_pool_frag_backward(gb[cur], Cv(j), lg.Fin_h, lg.Fin_w, lg.E_h, lg.E_w, c.cout, c.k_h,
+                                                 c.k_w, act, gb[cur ^ 1], stream);
+            });
+            if (e != hipSuccess) return hip_fail(e, "pool_frag_backward launch");
+            cur ^= 1;
+        } else if (c.act != DSS_ACT_NONE) {
+            const int64_t n = (int64_t)Fin * lg.E_h * lg.E_w * c.cout;
+            e = T.run("act_backward", j, 0.0, 0.0,
+                      [&] { return launch_act_backward(gb[cur], Cv(j), n, c.act, gb[cur ^ 1], stream); });
+            if (e != hipSuccess) return hip_fail(e, "act_backward launch");
+            cur ^= 1;
+        }
+        if (!c.has_conv) continue;   // the pool backward produced the gradient of A_{j-1}
+        const double fl = 2.0 * Fin * (double)lg.E_h * lg.E_w * c.cout * (double)c.cin * c.c_h * c.c_w;
+        const WgradPlan& wp = B.wg[j];
+        e = T.run("wgrad_mfma", j, fl, 0.0, [&] {
+            return launch_wgrad(gb[cur], A(j - 1), Fin, lg.E_h, lg.E_w, lg.Uin_h, lg.Uin_w, c.cout, c.cin, c.c_h, c.c_w,
+                                wp, wpart, grad_weight + B.wofs[j], stream);
+        });
+        if (e != hipSuccess) return hip_fail(e, "wgrad launch");
+        e = T.run("bias_grad", j, 0.0, 0.0, [&] {
+            return launch_bias_grad(gb[cur], (int64_t)Fin * lg.E_h * lg.E_w, c.cout, bpart, grad_bias + B.bofs[j],
+                                    stream);
+        });
+        if (e != hipSuccess) return hip_fail(e, "bias_grad launch");
+        if (j == 1 && !grad_signal) break;
+        const int ph = c.c_h - 1, pw = c.c_w - 1;
+        e = T.run("pad_grad", j, 0.0, 0.0, [&] {
+            return launch_pad_grad(gb[cur], Fin, lg.E_h, lg.E_w, c.cout, ph, pw, padb, stream);
+        });
+        if (e != hipSuccess) return hip_fail(e, "pad_grad launch");
+        const PlanConv& bpc = plan->bconvs[j - 1];
+        const int Hp = lg.E_h + 2 * ph, Wp = lg.E_w + 2 * pw;
+        e = T.run(dgrad_name(bpc), j, fl, 0.0, [&]() -> hipError_t {
+            if (bpc.impl == CONV_MFMA_F32)
+                return launch_conv_mfma_f32(padb, Fin, Hp, Wp, 1, 1, bpc, gb[cur ^ 1], stream);
+            return launch_conv_direct(DSS_F32, DSS_F32, padb, Fin, Hp, Wp, 1, 1, c.cout, bpc, gb[cur ^ 1], stream);
+        });
+        if (e != hipSuccess) return hip_fail(e, "input-gradient conv launch");
+        cur ^= 1;
+    }
+    if (grad_signal) {
+        e = T.run("crop_to_planar", 0, 0.0, 0.0,
+                  [&] { return launch_crop_to_planar(gb[cur], G.D_w, ch.in_c, H, W, grad_signal, stream); });
+        if (e != hipSuccess) return hip_fail(e, "crop_to_planar launch");
+    }
     return DSS_OK;
 }
 

@@ -88,6 +88,12 @@ struct PlanConv {
     float* b = nullptr;         // device bias [cout_pad], zero padded
 };
 
+// Host-side description of a weight-gradient launch (backward.hip).
+struct WgradPlan {
+    int segs = 0, otiles = 0, itiles = 0, splits = 0;
+    int64_t nchunks = 0, partial_floats = 0;
+};
+
 struct LaunchRec {
     const char* name;
     int layer;
@@ -102,6 +108,8 @@ struct dss_plan {
     dss_dtype dtype = DSS_F32;
     int device = 0;
     std::vector<dss::PlanConv> convs;     // one per chain layer (impl unused if no conv)
+    std::vector<dss::PlanConv> bconvs;    // binary32 plans: the input-gradient convolutions (transposed,
+                                          // flipped filters, no bias, no activation)
     bool timing = false;
     std::vector<hipEvent_t> events;
     std::vector<dss::LaunchRec> recs;
@@ -138,6 +146,21 @@ hipError_t launch_to_planar(dss_dtype dt, const void* in, int F, int h, int w, i
                             hipStream_t s);
 hipError_t launch_frag_planar(int elem_bytes, bool inverse, const void* in, int k_h, int k_w, int S_h,
                               int S_w, int C, int H, int W, void* out, hipStream_t s);
+
+// backward (backward.hip)
+hipError_t launch_frag_scatter_grad(const float* g, int C, int O_h, int O_w, int K_h, int K_w, int U_h, int U_w,
+                                    float* out, hipStream_t s);
+hipError_t launch_pool_frag_backward(const float* g, const float* a, int S_h, int S_w, int E_h, int E_w, int C,
+                                     int k_h, int k_w, int act, float* out, hipStream_t s);
+hipError_t launch_act_backward(const float* g, const float* a, int64_t n, int act, float* out, hipStream_t s);
+hipError_t launch_pad_grad(const float* in, int F, int E_h, int E_w, int C, int p_h, int p_w, float* out,
+                           hipStream_t s);
+WgradPlan wgrad_plan(int F, int E_h, int E_w, int Cout, int Cin, int fh, int fw);
+hipError_t launch_wgrad(const float* dy, const float* x, int F, int E_h, int E_w, int U_h, int U_w, int Cout, int Cin,
+                        int fh, int fw, const WgradPlan& w, float* partial, float* dw, hipStream_t s);
+int bias_blocks(int64_t P);
+hipError_t launch_bias_grad(const float* dy, int64_t P, int C, float* part, float* db, hipStream_t s);
+hipError_t launch_crop_to_planar(const float* in, int D_w, int C, int H, int W, float* out, hipStream_t s);
 
 // host-side weight packing for the MFMA kernels (conv_mfma.hip)
 bool mfma_supports(bool bf16, int cout, int fh, int fw);

@@ -68,7 +68,8 @@ class LaunchRecord(ctypes.Structure):
 EXPORTS = ("dss_chain_geometry", "dss_chain_layer_geometry", "dss_plan_create", "dss_plan_destroy",
            "dss_plan_geometry", "dss_plan_layer_geometry", "dss_eval_dense", "dss_eval_mixed", "dss_eval_slide",
            "dss_chain_stride_geometry", "dss_plan_stride_geometry", "dss_eval_stride", "dss_chain_dilate_geometry",
-           "dss_plan_dilate_geometry", "dss_eval_dilate", "dss_frag", "dss_defrag",
+           "dss_plan_dilate_geometry", "dss_eval_dilate", "dss_chain_backward_geometry",
+           "dss_plan_backward_geometry", "dss_backward_dense", "dss_frag", "dss_defrag",
            "dss_plan_set_timing", "dss_plan_timings", "dss_status_string", "dss_last_error", "dss_version")
 
 _lib = None
@@ -99,6 +100,10 @@ def lib():
                                                 P(ctypes.c_double)]
         L.dss_plan_dilate_geometry.argtypes = [VP, I32, I32, I32, P(I32), P(I32), P(I64), P(ctypes.c_double)]
         L.dss_eval_dilate.argtypes = [VP, VP, I32, I32, I32, VP, VP, I64, VP]
+        L.dss_chain_backward_geometry.argtypes = [P(Layer), I32, I32, I32, I32, I32, I32, P(I64), P(I64), P(I64),
+                                                  P(ctypes.c_double)]
+        L.dss_plan_backward_geometry.argtypes = [VP, I32, I32, I32, P(I64), P(I64), P(I64), P(ctypes.c_double)]
+        L.dss_backward_dense.argtypes = [VP, VP, I32, I32, VP, VP, VP, VP, VP, I64, VP]
         L.dss_frag.argtypes = [I32, I32, I32, I32, I32, I32, I32, I32, VP, VP, VP]
         L.dss_defrag.argtypes = [I32, I32, I32, I32, I32, I32, I32, I32, VP, VP, VP]
         L.dss_plan_set_timing.argtypes = [VP, I32]
@@ -113,7 +118,8 @@ def lib():
                      "dss_plan_layer_geometry", "dss_eval_dense", "dss_eval_mixed", "dss_eval_slide", "dss_frag",
                      "dss_defrag", "dss_plan_set_timing", "dss_plan_timings", "dss_plan_stride_geometry",
                      "dss_chain_stride_geometry", "dss_eval_stride", "dss_chain_dilate_geometry",
-                     "dss_plan_dilate_geometry", "dss_eval_dilate"):
+                     "dss_plan_dilate_geometry", "dss_eval_dilate", "dss_chain_backward_geometry",
+                     "dss_plan_backward_geometry", "dss_backward_dense"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -180,6 +186,16 @@ def chain_dilate_geometry(layers, ndim, in_channels, H, W, j, dtype="f32"):
                                            ctypes.byref(vw), ctypes.byref(ws), ctypes.byref(fl)),
            "dss_chain_dilate_geometry")
     return vh.value, vw.value, ws.value, fl.value
+
+
+def chain_backward_geometry(layers, ndim, in_channels, H, W, with_signal_grad=True):
+    """(workspace bytes, weight-gradient floats, bias-gradient floats, flops) of the backward pass (host only)."""
+    la = _LayerArray(layers)
+    ws, wf, bf, fl = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64(), ctypes.c_double()
+    _check(lib().dss_chain_backward_geometry(la.arr, la.n, ndim, in_channels, H, W, 1 if with_signal_grad else 0,
+                                             ctypes.byref(ws), ctypes.byref(wf), ctypes.byref(bf), ctypes.byref(fl)),
+           "dss_chain_backward_geometry")
+    return ws.value, wf.value, bf.value, fl.value
 
 
 def _stream(stream):
@@ -310,6 +326,51 @@ class Plan:
         _check(lib().dss_eval_dilate(self.handle, _ptr(signal), H, W, j, _ptr(out), _ptr(workspace),
                                      workspace.numel(), _stream(stream)), "dss_eval_dilate")
         return out
+
+    def backward_geometry(self, H, W, with_signal_grad=True):
+        """(workspace bytes, weight-gradient floats, bias-gradient floats, flops) of backward()."""
+        ws, wf, bf, fl = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64(), ctypes.c_double()
+        _check(lib().dss_plan_backward_geometry(self.handle, H, W, 1 if with_signal_grad else 0, ctypes.byref(ws),
+                                                ctypes.byref(wf), ctypes.byref(bf), ctypes.byref(fl)),
+               "dss_plan_backward_geometry")
+        return ws.value, wf.value, bf.value, fl.value
+
+    def backward(self, signal, grad_out, with_signal_grad=True, grad_weight=None, grad_bias=None, workspace=None,
+                 stream=None):
+        """Gradients of sum(grad_out * eval_dense(signal)).  Returns (flat weight
+        gradients, flat bias gradients, signal gradient or None) as CUDA tensors;
+        `split_grads` cuts the flat ones per convolution."""
+        import torch
+        self._check_signal(signal)
+        _, H, W = signal.shape
+        need, wf, bf, _ = self.backward_geometry(H, W, with_signal_grad)
+        dev = signal.device
+        if grad_weight is None:
+            grad_weight = torch.empty(max(wf, 1), dtype=torch.float32, device=dev)
+        if grad_bias is None:
+            grad_bias = torch.empty(max(bf, 1), dtype=torch.float32, device=dev)
+        gx = torch.empty_like(signal) if with_signal_grad else None
+        if workspace is None:
+            workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=dev)
+        if not grad_out.is_cuda or grad_out.dtype != torch.float32 or not grad_out.is_contiguous():
+            raise ValueError("grad_out must be a contiguous CUDA float32 tensor")
+        _check(lib().dss_backward_dense(self.handle, _ptr(signal), H, W, _ptr(grad_out), _ptr(grad_weight),
+                                        _ptr(grad_bias), _ptr(gx) if gx is not None else None, _ptr(workspace),
+                                        workspace.numel(), _stream(stream)), "dss_backward_dense")
+        return grad_weight, grad_bias, gx
+
+    def split_grads(self, grad_weight, grad_bias):
+        """Per-convolution views [cout][cin][fh][fw] and [cout] of the flat gradients."""
+        ws, bs, ow, ob = [], [], 0, 0
+        for l in self.layers:
+            if l["kind"] != "conv":
+                continue
+            n = l["cout"] * l["cin"] * l["fh"] * l["fw"]
+            ws.append(grad_weight[ow:ow + n].view(l["cout"], l["cin"], l["fh"], l["fw"]))
+            bs.append(grad_bias[ob:ob + l["cout"]])
+            ow += n
+            ob += l["cout"]
+        return ws, bs
 
     def stride_geometry(self, count):
         """(workspace bytes, conv flops) of eval_stride on a batch of `count` windows."""

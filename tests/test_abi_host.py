@@ -319,3 +319,29 @@ def test_dilate_geometry_errors():
     with pytest.raises(dss.DssError) as e:
         dss.chain_dilate_geometry(layers, 2, 1, 64, 64, 4)
     assert e.value.status == 1
+
+
+# ----------------------------------------------------------------------------- backward geometry
+
+
+@pytest.mark.parametrize("name", ["c1", "c3", "c4"])
+def test_backward_geometry(name):
+    """Gradient buffer sizes are the weight and bias counts; the work is the
+    forward convolutions plus a weight gradient and an input gradient of the same
+    size each (the first layer's input gradient only when the signal's is wanted)."""
+    arch, C, H, W, nd, B, K, r = NAMED[name]
+    layers = wl.init_layers(arch, np.random.default_rng(0))
+    g = dss.chain_geometry(layers, nd, C, H, W)
+    convs = [l for l in layers if l["kind"] == "conv"]
+    ws1, wf, bf, fl1 = dss.chain_backward_geometry(layers, nd, C, H, W, True)
+    ws0, wf0, bf0, fl0 = dss.chain_backward_geometry(layers, nd, C, H, W, False)
+    assert wf == wf0 == sum(l["cout"] * l["cin"] * l["fh"] * l["fw"] for l in convs)
+    assert bf == bf0 == sum(l["cout"] for l in convs)
+    assert fl1 == pytest.approx(3 * g["conv_flops"], rel=1e-12)
+    ch = mixed.chain_of(layers)
+    first = ch[0]["conv"]
+    D = (g["D_h"], g["D_w"])
+    first_flops = 2.0 * (D[0] - first["fh"] + 1) * (D[1] - first["fw"] + 1) * first["cout"] * first["cin"] * \
+        first["fh"] * first["fw"]
+    assert fl0 == pytest.approx(3 * g["conv_flops"] - first_flops, rel=1e-12)
+    assert ws1 >= ws0 >= 2 * g["workspace_bytes"] // 2

@@ -1,0 +1,192 @@
+"""GPU parity of the backward pass (dss_backward_dense) against the oracle's
+window-by-window backpropagation.  Integer-valued chains are exact (every
+partial sum is an integer below 2^24, so any summation order gives the same
+bits, and ties in the max-pool exercise the shared first-maximum rule); random
+binary32 chains within 1e-4 * max|oracle| per gradient tensor."""
+import numpy as np
+import pytest
+
+import oracle
+from oracle import backward as ob
+from paper_1508_06904_amd import dss, workloads as wl
+from tests.gpu_helpers import log, sampled_windows, to_device
+from tests.test_gpu_parity import CHAINS, EXACT_ARCH
+
+pytestmark = pytest.mark.gpu
+
+TOL = 1e-4
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    dss.lib()
+    yield
+    torch.cuda.synchronize()
+
+
+def gpu_backward(plan, x, G, with_dx=True):
+    import torch
+    gw, gb, gx = plan.backward(to_device(x, "f32"), to_device(G, "f32"), with_signal_grad=with_dx)
+    torch.cuda.synchronize()
+    ws, bs = plan.split_grads(gw, gb)
+    return ([w.cpu().numpy().astype(np.float64) for w in ws], [b.cpu().numpy().astype(np.float64) for b in bs],
+            None if gx is None else gx.cpu().numpy().astype(np.float64))
+
+
+def close(got, ref, what, tol=TOL):
+    scale = float(np.abs(ref).max())
+    err = float(np.abs(got - ref).max())
+    log("  %s max|err| = %.3e, max|oracle| = %.3e, ratio %.2e" % (what, err, scale, err / max(scale, 1e-300)))
+    assert got.shape == ref.shape and np.all(np.isfinite(got))
+    assert err <= tol * scale, what
+
+
+def check_all(got, ref, tag, tol=TOL):
+    for t, (a, b) in enumerate(zip(got[0], ref[0])):
+        close(a, b, "%s dW%d" % (tag, t), tol)
+    for t, (a, b) in enumerate(zip(got[1], ref[1])):
+        close(a, b, "%s db%d" % (tag, t), tol)
+    if got[2] is not None:
+        close(got[2], ref[2], "%s dx" % tag, tol)
+
+
+@pytest.mark.parametrize("name", ["2d_small_direct", "2d_mfma_mixed", "2d_pool_first", "2d_pool_pool", "1d_c2_like",
+                                  "2d_ragged_cin"])
+def test_backward_random_chain(name):
+    arch, C, nd = CHAINS[name]
+    w0 = wl.custom(arch, C, 1, 1, seed=1)
+    B = oracle.receptive_field(w0.layers)
+    K = (1, 1)
+    for l in w0.layers:
+        if l["kind"] == "maxpool":
+            K = (K[0] * l["kh"], K[1] * l["kw"])
+    H = 1 if nd == 1 else B[0] + K[0] + 3
+    W = B[1] + (120 if nd == 1 else 2 * K[1] + 1)
+    w = wl.custom(arch, C, H, W, seed=11, value_kind="normal")
+    G = np.random.default_rng(12).standard_normal((w.layers[-1]["cout"], H - B[0] + 1, W - B[1] + 1))
+    plan = dss.Plan(w.layers, nd, C)
+    log("backward %s on %s" % (name, w.x.shape))
+    check_all(gpu_backward(plan, w.x, G), ob.dense_backward(w.layers, w.x, G), name)
+
+
+@pytest.mark.parametrize("kernel", ["mfma", "direct"])
+def test_backward_exact_integer_chain(kernel, monkeypatch):
+    if kernel == "direct":
+        monkeypatch.setenv("DSS_CONV_KERNEL", "direct")
+    w = wl.custom(EXACT_ARCH, 16, 27, 31, seed=3, weight_kind="int", value_kind="int")
+    B = oracle.receptive_field(w.layers)
+    G = np.random.default_rng(5).integers(-2, 3, size=(w.layers[-1]["cout"], 27 - B[0] + 1, 31 - B[1] + 1)).astype(
+        np.float64)
+    plan = dss.Plan(w.layers, 2, 16)
+    got = gpu_backward(plan, w.x, G)
+    ref = ob.dense_backward(w.layers, w.x, G)
+    for a, b in zip(got[0] + got[1] + [got[2]], ref[0] + ref[1] + [ref[2]]):
+        assert np.abs(b).max() < 2 ** 23
+        np.testing.assert_array_equal(a, b)
+
+
+def test_backward_without_signal_gradient():
+    arch, C, nd = CHAINS["2d_mfma_mixed"]
+    w = wl.custom(arch, C, 60, 61, seed=2, value_kind="normal")
+    B = oracle.receptive_field(w.layers)
+    G = np.random.default_rng(3).standard_normal((w.layers[-1]["cout"], 60 - B[0] + 1, 61 - B[1] + 1))
+    plan = dss.Plan(w.layers, nd, C)
+    a = gpu_backward(plan, w.x, G, with_dx=True)
+    b = gpu_backward(plan, w.x, G, with_dx=False)
+    assert b[2] is None
+    for u, v in zip(a[0] + a[1], b[0] + b[1]):
+        np.testing.assert_array_equal(u, v)
+
+
+@pytest.mark.parametrize("name,H,W,widths", [("c3_512", 80, 84, (16, 32, 48, 64)), ("c1_64x64", 64, 64, None)])
+def test_backward_named_reduced(name, H, W, widths):
+    w = wl.make(name, H=H, W=W, widths=widths)
+    g = dss.chain_geometry(w.layers, w.ndim, w.x.shape[0], H, W)
+    G = np.random.default_rng(9).standard_normal((g["out_c"], g["out_h"], g["out_w"]))
+    plan = dss.Plan.from_workload(w)
+    log("backward %s reduced %s" % (name, w.x.shape))
+    check_all(gpu_backward(plan, w.x, G), ob.dense_backward(w.layers, w.x, G), name)
+
+
+def close_l2(got, ref, what, rel_l2=2e-3, rel_max=5e-3):
+    """Relative L2 bound plus an elementwise one, for full-size checks.  The
+    gradients depend on discrete decisions of the forward pass (ReLU masks, the
+    position of each pool maximum).  At full size a binary32 forward pass takes a
+    few of them differently from a float64 one where two candidates lie within
+    rounding of each other: for the 17 sampled HD windows (9.5e6 decisions) a
+    binary32 numpy forward pass already differs from float64 in 2 pool decisions.
+    One such flip in the second pool moves the gradient of one activation and
+    spreads through the first layer's input gradient into every first-layer
+    weight gradient, by about 3e-4 of the largest entry (relative L2 error).  The
+    bounds leave room for a few flips; the exact agreement of the kernels is
+    checked at small sizes (no flips) and on integer data (bit-exact)."""
+    scale = float(np.abs(ref).max())
+    err = np.abs(got - ref)
+    l2 = float(np.linalg.norm(got - ref) / max(np.linalg.norm(ref), 1e-300))
+    n_out = int(np.sum(err > TOL * scale))
+    log("  %s rel L2 %.2e, max|err|/max|oracle| %.2e, elements above 1e-4: %d of %d" % (
+        what, l2, float(err.max()) / scale, n_out, err.size))
+    assert got.shape == ref.shape and np.all(np.isfinite(got))
+    assert l2 <= rel_l2 and float(err.max()) <= rel_max * scale, what
+
+
+def test_backward_hd_frame_sampled_windows():
+    """The HD frame at full size in the launch configuration of the benchmark.
+    The upstream gradient is nonzero on 17 sampled windows only, so the oracle's
+    gradient is the sum of 17 per-window backpropagations."""
+    w = wl.make("c4_hd")
+    plan = dss.Plan.from_workload(w)
+    g = plan.geometry(1080, 1920)
+    i, j = sampled_windows(g["out_h"], g["out_w"], g["K_h"], g["K_w"], per_phase=1, max_phases=8, seed=4)
+    G = np.zeros((g["out_c"], g["out_h"], g["out_w"]))
+    G[:, i, j] = np.random.default_rng(6).standard_normal((g["out_c"], len(i)))
+    log("HD backward with %d nonzero windows" % len(i))
+    got = gpu_backward(plan, w.x, G, with_dx=False)
+    B = (g["B_h"], g["B_w"])
+    patches = np.stack([w.x[:, a:a + B[0], b:b + B[1]] for a, b in zip(i, j)]).astype(np.float64)
+    dW, db, _ = ob.strided_backward(w.layers, patches, G[:, i, j].T)
+    for t, (a, b) in enumerate(zip(got[0], dW)):
+        close_l2(a, b, "hd dW%d" % t)
+    for t, (a, b) in enumerate(zip(got[1], db)):
+        close_l2(a, b, "hd db%d" % t)
+    # the last layer is linear and its input needs no decision: tight bound
+    close(got[1][-1], G.sum(axis=(1, 2)), "hd db_last vs sum(G)")
+    # the backward pass is linear in G with the forward decisions fixed: doubling
+    # G doubles every intermediate exactly, so every gradient doubles bit for bit
+    got2 = gpu_backward(plan, w.x, 2.0 * G, with_dx=False)
+    for a, b in zip(got[0] + got[1], got2[0] + got2[1]):
+        np.testing.assert_array_equal(2.0 * a, b)
+
+
+def test_backward_rejects_bf16_and_short_workspace():
+    import torch
+    w = wl.make("c1_64x64")
+    G = to_device(np.ones((1, 37, 37)), "f32")
+    plan = dss.Plan(w.layers, 2, 1, "bf16")
+    with pytest.raises(dss.DssError) as e:
+        plan.backward(to_device(w.x, "bf16"), G)
+    assert e.value.status == 3
+    plan = dss.Plan.from_workload(w)
+    gw = torch.full((plan.backward_geometry(64, 64)[1],), 9.0, device="cuda")
+    gb = torch.full((plan.backward_geometry(64, 64)[2],), 9.0, device="cuda")
+    ws = torch.empty(4096, dtype=torch.uint8, device="cuda")
+    with pytest.raises(dss.DssError) as e:
+        plan.backward(to_device(w.x, "f32"), G, grad_weight=gw, grad_bias=gb, workspace=ws)
+    assert e.value.status == 2
+    torch.cuda.synchronize()
+    assert torch.all(gw == 9.0) and torch.all(gb == 9.0)
+
+
+def test_backward_timing_records():
+    w = wl.make("c3_512", H=100, W=104, widths=(16, 32, 64, 128))
+    plan = dss.Plan.from_workload(w)
+    g = plan.geometry(100, 104)
+    G = np.random.default_rng(1).standard_normal((g["out_c"], g["out_h"], g["out_w"]))
+    plan.set_timing(True)
+    gpu_backward(plan, w.x, G)
+    recs = plan.timings()
+    names = [r["kernel"] for r in recs]
+    assert names.count("wgrad_mfma") == 5 and names.count("pool_frag_backward") == 3
+    assert sum(r["flops"] for r in recs) == pytest.approx(plan.backward_geometry(100, 104)[3], rel=1e-9)
