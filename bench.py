@@ -24,6 +24,12 @@ with both times and the speed-up.
 full-resolution signal with dilated taps instead of fragments), for an A/B of
 the two schemes on the same kernels.
 
+`--backward` times one whole-image gradient step instead (dss_backward_dense:
+the dense forward pass keeping every layer's output, then the gradients of all
+weights and biases for a random upstream gradient of the dense output -- the
+fine-tuning step of Sect. 6.2); the metric counts the windows whose gradients a
+step accumulates.
+
 `--ell l` (l > 0) times the mixed evaluation instead (appendix, Theorem
 "evalrelaxslide"): the first l chain layers pool with stride, and the output is
 the dense output downsampled by k*_l per axis; the metric then counts those
@@ -109,6 +115,8 @@ def main():
                     help="only run plain 1 GiB device-to-device copies (scales the HBM byte counters of a profiler)")
     ap.add_argument("--fashion", default="slide", choices=("slide", "dilate"),
                     help="dense evaluation scheme: fragments (slide) or dilated taps (dilate)")
+    ap.add_argument("--backward", action="store_true",
+                    help="time dss_backward_dense (forward + weight/bias gradients) instead of the forward pass")
     ap.add_argument("--sweep", action="store_true",
                     help="EvalSlide vs patch-by-patch EvalStride on the paper's 240x320 family, L = 1..15")
     ap.add_argument("--sweep-layers", default="1-15", help="range of L for --sweep, e.g. 1-15 or 12")
@@ -142,10 +150,22 @@ def main():
         x = x.to(torch.bfloat16)
     x = x.contiguous()
     out = torch.empty((g["out_c"], g["out_h"], g["out_w"]), dtype=torch.float32, device="cuda")
+    if args.backward and (ell or args.fashion != "slide" or w.dtype != "f32"):
+        log("--backward times the binary32 dense evaluation's gradient step only")
+        sys.exit(2)
     if args.fashion == "dilate" and ell:
         log("--fashion dilate evaluates the dense output; it does not combine with --ell")
         sys.exit(2)
-    if args.fashion == "dilate":
+    if args.backward:
+        need, wf, bf, bwd_flops = plan.backward_geometry(H, W, False)
+        ws = torch.empty(max(need, 256), dtype=torch.uint8, device="cuda")
+        gw = torch.empty(wf, dtype=torch.float32, device="cuda")
+        gb = torch.empty(bf, dtype=torch.float32, device="cuda")
+        gen = torch.Generator(device="cuda")
+        gen.manual_seed(7)
+        gout = torch.randn((g["out_c"], g["out_h"], g["out_w"]), generator=gen, device="cuda")
+        g["conv_flops"] = bwd_flops
+    elif args.fashion == "dilate":
         _, _, need, dil_flops = plan.dilate_geometry(H, W, g["n_chain"])
         ws = torch.empty(max(need, 256), dtype=torch.uint8, device="cuda")
         g["conv_flops"] = dil_flops
@@ -154,7 +174,9 @@ def main():
     windows = g["out_h"] * g["out_w"]
 
     def step():
-        if args.fashion == "dilate":
+        if args.backward:
+            plan.backward(x, gout, with_signal_grad=False, grad_weight=gw, grad_bias=gb, workspace=ws)
+        elif args.fashion == "dilate":
             plan.eval_dilate(x, out=out, workspace=ws)
         elif ell == 0:
             plan.eval_dense(x, out=out, workspace=ws)
@@ -191,7 +213,9 @@ def main():
         peak = PEAK_TFLOPS[w.dtype]
         roof = {"bound": "mfma", "kernel": dom["kernel"], "achieved": ach, "peak": peak, "unit": "TFLOP/s",
                 "frac": ach / peak, "traffic": profiled_traffic(dom["kernel"], args.config if ell == 0 and args.fashion == "slide"
-                                           else "%s_%s%d" % (args.config, args.fashion, ell)),
+                                           and not args.backward
+                                           else "%s_%s%d%s" % (args.config, args.fashion, ell,
+                                                               "_backward" if args.backward else "")),
                 "traffic_unit": "bytes per launch (HBM, rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
                 "per_launch": {"flops": domd["flops"] / domd["n"], "avg_ms": domd["ms"] / domd["n"],
                                "launches_per_step": domd["n"] / args.steps}}
@@ -208,12 +232,16 @@ def main():
               "k_star": [g["K_h"], g["K_w"]], "conv_gflop_per_step": g["conv_flops"] / 1e9}
     if args.fashion == "dilate":
         config["fashion"] = "dilated taps on the full-resolution signal (no fragments)"
+    if args.backward:
+        config["step"] = ("dss_backward_dense: forward keeping every layer's output + weight and bias gradients "
+                          "of a random upstream gradient (no signal gradient)")
     if ell:
         config.update({"mixed_level": ell, "output_spacing": [g["step_h"], g["step_w"]],
                        "trimmed": [g["trim_h"], g["trim_w"]], "stuffed": [g["r_h"], g["r_w"]]})
     record = {
-        "metric": "dense window outputs/sec at 1 MI355X" if ell == 0 else
-                  "mixed-fashion window outputs/sec at 1 MI355X (every k*_l-th window per axis)",
+        "metric": ("whole-image gradient steps: windows/sec at 1 MI355X" if args.backward else
+                   "dense window outputs/sec at 1 MI355X" if ell == 0 else
+                   "mixed-fashion window outputs/sec at 1 MI355X (every k*_l-th window per axis)"),
         "value": windows / (ms_per_step / 1e3),
         "unit": "windows/s",
         "n_gpus": 1,
@@ -233,7 +261,9 @@ def main():
         "cpu_baseline": None,
     }
 
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and args.backward:
+        record["cpu_baseline"] = cpu_baseline_backward(w, g, args.cpu_seconds)
+    elif not args.no_cpu_baseline:
         record["cpu_baseline"], record["parity_spot_check"] = cpu_baseline(w, g, out, args.cpu_seconds)
     print(json.dumps(record), flush=True)
 
@@ -323,6 +353,42 @@ def calibrate_copy(n=4, nbytes=1 << 30):
     torch.cuda.synchronize()
     print(json.dumps({"calibration": "device copy", "bytes_read_per_launch": nbytes,
                       "bytes_written_per_launch": nbytes, "launches": n}), flush=True)
+
+
+def cpu_baseline_backward(w, g, target_s):
+    """Times the oracle's window-by-window backpropagation (float64 numpy, BLAS
+    threads) on a bounded seeded sample of the frame's windows."""
+    import numpy as np
+
+    from oracle import backward as ob
+    from paper_1508_06904_amd import workloads as wl
+
+    try:
+        import threadpoolctl
+        cores = max([i.get("num_threads", 1) for i in threadpoolctl.threadpool_info()] or [1])
+    except Exception:
+        cores = 1
+    si, sj = wl.sample_windows(g["out_h"], g["out_w"], g["K_h"], g["K_w"], per_phase=1, seed=2)
+    B = (g["B_h"], g["B_w"])
+    rng = np.random.default_rng(3)
+
+    def run(first, n):
+        sel = slice(first, first + n)
+        patches = np.stack([w.x[:, a:a + B[0], b:b + B[1]] for a, b in zip(si[sel], sj[sel])]).astype(np.float64)
+        ob.strided_backward(w.layers, patches, rng.standard_normal((n, g["out_c"])))
+
+    t = time.perf_counter()
+    run(0, 1)
+    probe = time.perf_counter() - t
+    n = int(max(1, min(len(si), target_s / max(probe, 1e-6))))
+    t = time.perf_counter()
+    for first in range(0, n, 16):
+        run(first, min(16, n - first))
+    cpu_s = time.perf_counter() - t
+    log("cpu baseline (backward): %d windows in %.1fs" % (n, cpu_s))
+    return {"value": n / cpu_s, "unit": "windows/s", "cores": cores, "kind": "oracle",
+            "sample": "%d seeded windows of the frame (corners, edges, fragment phases); float64 window-by-window "
+                      "backpropagation through the strided network" % n, "seconds": cpu_s}
 
 
 def cpu_baseline(w, g, out, target_s):
