@@ -339,10 +339,24 @@ WgradPlan wgrad_plan(int F, int E_h, int E_w, int Cout, int Cin, int fh, int fw)
     w.otiles = (Cout + kWM - 1) / kWM;
     w.itiles = (Cin + kWN - 1) / kWN;
     const int64_t base = (int64_t)w.otiles * w.itiles * fh * fw;
-    // about four workgroups per CU in total, each split at least 8 chunks long
-    int64_t splits = std::max<int64_t>(1, (256 * 4 + base - 1) / base);
-    splits = std::min<int64_t>(splits, std::max<int64_t>(1, w.nchunks / 8));
-    w.splits = (int)std::min<int64_t>(splits, 4096);
+    // Two workgroups fit a CU (80 KB of LDS each), 512 run at once.  Take at
+    // least eight rounds of 512 workgroups and, among the split counts up to
+    // twice that, the one whose last round is fullest; every split keeps at least
+    // 8 chunks.
+    const int64_t max_splits = std::max<int64_t>(1, std::min<int64_t>(4096, w.nchunks / 8));
+    const int64_t lo = std::min(max_splits, std::max<int64_t>(1, (512 * 8 + base - 1) / base));
+    const int64_t hi = std::min(max_splits, 2 * lo);
+    int64_t best = lo;
+    double best_fill = -1.0;
+    for (int64_t sp = lo; sp <= hi; ++sp) {
+        const int64_t total = base * sp;
+        const double fill = (double)total / (double)(((total + 511) / 512) * 512);
+        if (fill > best_fill + 1e-9) {
+            best_fill = fill;
+            best = sp;
+        }
+    }
+    w.splits = (int)best;
     w.partial_floats = (int64_t)w.splits * fh * fw * Cout * Cin;
     return w;
 }
