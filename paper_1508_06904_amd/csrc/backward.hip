@@ -188,25 +188,39 @@ hipError_t launch_pad_grad(const float* in, int F, int E_h, int E_w, int C, int 
 // ------------------------------------------------------------------ wgrad (MFMA)
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 
-constexpr int kWM = 128, kWN = 128;   // workgroup tile: output channels x input channels
-constexpr int kKC = 32;               // positions per chunk (one row segment)
+constexpr int kWM = 128;              // workgroup tile: output channels
+constexpr int kKC = 32;               // positions per chunk
 constexpr int kWP = 160;              // LDS row pitch in floats: 128 + 32, so the two half-waves
                                       // of a read hit disjoint banks
 constexpr size_t kWgradLds = 2 * 2 * kKC * kWP * sizeof(float);
 
-// Workgroup (o tile, i tile, tap, split): 4 waves, each a 64 x 64 block of 2 x 2
-// MFMA 32x32x2 tiles.  The positions of a chunk are 32 consecutive samples of
-// one output row of one fragment; chunk c of the layer is (fragment, row,
-// segment) in row-major order, and split s takes chunks [c0, c1).
-template <bool VEC>
+// Workgroup (o tile, i tile, tap, split): 4 waves in a 2 x 2 grid, each a
+// 64 x (32 NTW) block of MFMA 32x32x2 tiles, so the workgroup covers 128 output
+// channels and 64 NTW input channels (NTW = 1 for layers with at most 64 input
+// channels).  The output positions p of all fragments are numbered row-major
+// (fragment, row, column); chunk c holds positions 32c .. 32c + 31 and split s
+// takes chunks [c0, c1).  Position p's gradient row is dy[p]; its input sample
+// for tap (t_h, t_w) is x[f][y + t_h][x + t_w].
+template <bool VEC, int NTW>
 __global__ __launch_bounds__(256) void wgrad_mfma_kernel(const float* __restrict__ dy, const float* __restrict__ x,
                                                         int E_h, int E_w, int U_h, int U_w, int Cout, int Cin,
-                                                        int fh, int fw, int segs, int64_t nchunks, int otiles,
+                                                        int fh, int fw, int64_t P, int64_t nchunks, int otiles,
                                                         int itiles, int splits, float* __restrict__ partial) {
+    constexpr int BNW = 64 * NTW;                 // input channels per workgroup
+    constexpr int TPR = BNW / 4;                  // staging threads per B row (4 channels each)
+    constexpr int RPP = 256 / TPR;                // B rows per staging pass
+    constexpr int BPASS = kKC / RPP;
     extern __shared__ __attribute__((aligned(16))) float wl[];
     // A (output-gradient) chunks in buffers 0/1, B (input) chunks in buffers 2/3
     auto lds_buf = [&](int k) { return wl + k * (kKC * kWP); };
-    int bid = blockIdx.x;
+    // Workgroups are handed to the 8 XCDs round-robin by id; remap so that every
+    // XCD runs one contiguous range of the logical order (o tile, i tile, tap
+    // fastest, split slowest): the workgroups on an XCD then read the same chunks
+    // of dy and x from its L2.
+    const int total = gridDim.x;
+    const int xcd = blockIdx.x % 8, slot = blockIdx.x / 8;
+    const int q8 = total / 8, r8 = total % 8;
+    int bid = xcd < r8 ? xcd * (q8 + 1) + slot : r8 * (q8 + 1) + (xcd - r8) * q8 + slot;
     const int ot = bid % otiles;
     bid /= otiles;
     const int it = bid % itiles;
@@ -216,21 +230,22 @@ __global__ __launch_bounds__(256) void wgrad_mfma_kernel(const float* __restrict
     const int split = bid / taps;
     const int th = tap / fw, tw = tap % fw;
     const int64_t c0 = nchunks * split / splits, c1 = nchunks * (split + 1) / splits;
-    const int o0 = ot * kWM, i0 = it * kWN;
+    const int o0 = ot * kWM, i0 = it * BNW;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave & 1, wn = wave >> 1, half = lane >> 5, l32 = lane & 31;
-    const int col4 = (tid & 31) * 4;    // staging: 4 consecutive channels
-    const int row0 = tid >> 5;          // staging rows row0 + 8 k
+    const int a_col = (tid & 31) * 4, a_row = tid >> 5;        // A staging: rows a_row + 8 k
+    const int b_col = (tid % TPR) * 4, b_row = tid / TPR;      // B staging: rows b_row + RPP k
+    const int64_t plane = (int64_t)E_h * E_w;
 
-    floatx16 acc[2][2];
+    floatx16 acc[2][NTW];
 #pragma unroll
     for (int a = 0; a < 2; ++a)
 #pragma unroll
-        for (int b = 0; b < 2; ++b)
+        for (int b = 0; b < NTW; ++b)
 #pragma unroll
             for (int v = 0; v < 16; ++v) acc[a][b][v] = 0.f;
 
-    float4 ra[4], rb[4];
+    float4 ra[4], rb[BPASS];
     auto load4 = [&](const float* base, int c_lo, int C, bool ok) -> float4 {
         if (!ok) return make_float4(0.f, 0.f, 0.f, 0.f);
         if (VEC) return c_lo + 3 < C ? *reinterpret_cast<const float4*>(base + c_lo) : make_float4(0.f, 0.f, 0.f, 0.f);
@@ -240,25 +255,28 @@ __global__ __launch_bounds__(256) void wgrad_mfma_kernel(const float* __restrict
         return make_float4(v[0], v[1], v[2], v[3]);
     };
     auto load_chunk = [&](int64_t c) {
-        const int seg = (int)(c % segs);
-        const int64_t fy = c / segs;
-        const int y = (int)(fy % E_h);
-        const int64_t f = fy / E_h;
-        const int x0 = seg * kKC;
+        const int64_t pc = c * kKC;
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
-            const int xr = x0 + row0 + 8 * k;
-            const bool ok = xr < E_w;
-            ra[k] = load4(dy + ((f * E_h + y) * E_w + xr) * Cout, o0 + col4, Cout, ok);
-            rb[k] = load4(x + ((f * U_h + y + th) * U_w + xr + tw) * Cin, i0 + col4, Cin, ok);
+            const int64_t p = pc + a_row + 8 * k;
+            ra[k] = load4(dy + p * Cout, o0 + a_col, Cout, p < P);
+        }
+#pragma unroll
+        for (int k = 0; k < BPASS; ++k) {
+            const int64_t p = pc + b_row + RPP * k;
+            const int64_t f = p / plane;
+            const int r = (int)(p - f * plane);
+            const int y = r / E_w, xx = r - y * E_w;
+            rb[k] = load4(x + ((f * U_h + y + th) * U_w + xx + tw) * Cin, i0 + b_col, Cin, p < P);
         }
     };
     auto store_chunk = [&](int buf) {
 #pragma unroll
-        for (int k = 0; k < 4; ++k) {
-            *reinterpret_cast<float4*>(lds_buf(buf) + (row0 + 8 * k) * kWP + col4) = ra[k];
-            *reinterpret_cast<float4*>(lds_buf(2 + buf) + (row0 + 8 * k) * kWP + col4) = rb[k];
-        }
+        for (int k = 0; k < 4; ++k)
+            *reinterpret_cast<float4*>(lds_buf(buf) + (a_row + 8 * k) * kWP + a_col) = ra[k];
+#pragma unroll
+        for (int k = 0; k < BPASS; ++k)
+            *reinterpret_cast<float4*>(lds_buf(2 + buf) + (b_row + RPP * k) * kWP + b_col) = rb[k];
     };
 
     if (c0 < c1) {
@@ -275,15 +293,15 @@ __global__ __launch_bounds__(256) void wgrad_mfma_kernel(const float* __restrict
 #pragma unroll 4
         for (int ks = 0; ks < kKC / 2; ++ks) {
             const int p = 2 * ks + half;
-            float av[2], bv[2];
+            float av[2], bv[NTW];
 #pragma unroll
             for (int mt = 0; mt < 2; ++mt) av[mt] = A[p * kWP + wm * 64 + mt * 32 + l32];
 #pragma unroll
-            for (int nt = 0; nt < 2; ++nt) bv[nt] = Bm[p * kWP + wn * 64 + nt * 32 + l32];
+            for (int nt = 0; nt < NTW; ++nt) bv[nt] = Bm[p * kWP + wn * 32 * NTW + nt * 32 + l32];
 #pragma unroll
             for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
-                for (int nt = 0; nt < 2; ++nt)
+                for (int nt = 0; nt < NTW; ++nt)
                     acc[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[mt], bv[nt], acc[mt][nt], 0, 0, 0);
         }
         if (more) store_chunk(buf ^ 1);
@@ -295,8 +313,8 @@ __global__ __launch_bounds__(256) void wgrad_mfma_kernel(const float* __restrict
 #pragma unroll
     for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
-        for (int nt = 0; nt < 2; ++nt) {
-            const int ii = i0 + wn * 64 + nt * 32 + l32;
+        for (int nt = 0; nt < NTW; ++nt) {
+            const int ii = i0 + wn * 32 * NTW + nt * 32 + l32;
 #pragma unroll
             for (int v = 0; v < 16; ++v) {
                 const int o = o0 + wm * 64 + mt * 32 + (v >> 2) * 8 + half * 4 + (v & 3);
@@ -334,10 +352,11 @@ static hipError_t allow_lds(const void* kern, size_t lds) {
 
 WgradPlan wgrad_plan(int F, int E_h, int E_w, int Cout, int Cin, int fh, int fw) {
     WgradPlan w;
-    w.segs = (E_w + kKC - 1) / kKC;
-    w.nchunks = (int64_t)F * E_h * w.segs;
+    w.ntw = Cin <= 64 ? 1 : 2;
+    w.positions = (int64_t)F * E_h * E_w;
+    w.nchunks = (w.positions + kKC - 1) / kKC;
     w.otiles = (Cout + kWM - 1) / kWM;
-    w.itiles = (Cin + kWN - 1) / kWN;
+    w.itiles = (Cin + 64 * w.ntw - 1) / (64 * w.ntw);
     const int64_t base = (int64_t)w.otiles * w.itiles * fh * fw;
     // Two workgroups fit a CU (80 KB of LDS each), 512 run at once.  Take at
     // least eight rounds of 512 workgroups and, among the split counts up to
@@ -361,21 +380,30 @@ WgradPlan wgrad_plan(int F, int E_h, int E_w, int Cout, int Cin, int fh, int fw)
     return w;
 }
 
-hipError_t launch_wgrad(const float* dy, const float* x, int F, int E_h, int E_w, int U_h, int U_w, int Cout, int Cin,
-                        int fh, int fw, const WgradPlan& w, float* partial, float* dw, hipStream_t s) {
-    const bool vec = Cout % 4 == 0 && Cin % 4 == 0;
-    const void* kern = vec ? (const void*)wgrad_mfma_kernel<true> : (const void*)wgrad_mfma_kernel<false>;
-    hipError_t e = allow_lds(kern, kWgradLds);
+template <bool VEC, int NTW>
+static hipError_t run_wgrad(const float* dy, const float* x, int E_h, int E_w, int U_h, int U_w, int Cout, int Cin,
+                            int fh, int fw, const WgradPlan& w, float* partial, hipStream_t s) {
+    auto kern = wgrad_mfma_kernel<VEC, NTW>;
+    hipError_t e = allow_lds((const void*)kern, kWgradLds);
     if (e != hipSuccess) return e;
     const int64_t nblocks = (int64_t)w.otiles * w.itiles * fh * fw * w.splits;
     if (nblocks >= (1ll << 31)) return hipErrorInvalidConfiguration;
-    if (vec)
-        wgrad_mfma_kernel<true><<<dim3((unsigned)nblocks), 256, kWgradLds, s>>>(
-            dy, x, E_h, E_w, U_h, U_w, Cout, Cin, fh, fw, w.segs, w.nchunks, w.otiles, w.itiles, w.splits, partial);
+    kern<<<dim3((unsigned)nblocks), 256, kWgradLds, s>>>(dy, x, E_h, E_w, U_h, U_w, Cout, Cin, fh, fw, w.positions,
+                                                         w.nchunks, w.otiles, w.itiles, w.splits, partial);
+    return hipGetLastError();
+}
+
+hipError_t launch_wgrad(const float* dy, const float* x, int F, int E_h, int E_w, int U_h, int U_w, int Cout, int Cin,
+                        int fh, int fw, const WgradPlan& w, float* partial, float* dw, hipStream_t s) {
+    (void)F;
+    const bool vec = Cout % 4 == 0 && Cin % 4 == 0;
+    hipError_t e;
+    if (w.ntw == 1)
+        e = vec ? run_wgrad<true, 1>(dy, x, E_h, E_w, U_h, U_w, Cout, Cin, fh, fw, w, partial, s)
+                : run_wgrad<false, 1>(dy, x, E_h, E_w, U_h, U_w, Cout, Cin, fh, fw, w, partial, s);
     else
-        wgrad_mfma_kernel<false><<<dim3((unsigned)nblocks), 256, kWgradLds, s>>>(
-            dy, x, E_h, E_w, U_h, U_w, Cout, Cin, fh, fw, w.segs, w.nchunks, w.otiles, w.itiles, w.splits, partial);
-    e = hipGetLastError();
+        e = vec ? run_wgrad<true, 2>(dy, x, E_h, E_w, U_h, U_w, Cout, Cin, fh, fw, w, partial, s)
+                : run_wgrad<false, 2>(dy, x, E_h, E_w, U_h, U_w, Cout, Cin, fh, fw, w, partial, s);
     if (e != hipSuccess) return e;
     const int64_t n = (int64_t)Cout * Cin * fh * fw;
     wgrad_reduce_kernel<<<dim3((unsigned)ceil_div64(n, kBT)), kBT, 0, s>>>(partial, w.splits, fh * fw, Cout, Cin, dw);

@@ -90,8 +90,9 @@ struct PlanConv {
 
 // Host-side description of a weight-gradient launch (backward.hip).
 struct WgradPlan {
-    int segs = 0, otiles = 0, itiles = 0, splits = 0;
-    int64_t nchunks = 0, partial_floats = 0;
+    int ntw = 2;                 // MFMA tiles per wave along the input channels (1 or 2)
+    int otiles = 0, itiles = 0, splits = 0;
+    int64_t positions = 0, nchunks = 0, partial_floats = 0;
 };
 
 struct LaunchRec {
