@@ -124,11 +124,31 @@ static dss_status upload_conv(int cin, int cout, int fh, int fw, int act, const 
         wbuf.assign(wbytes, 0);
         mfma_bf16_pack(pc, weight, reinterpret_cast<uint16_t*>(wbuf.data()));
     }
+    // the 64-channel tile's packing, for launches too small for the 128-channel one
+    std::vector<char> abuf;
+    if (pc.impl != CONV_DIRECT && pc.bn == 128) {
+        PlanConv alt = pc;
+        alt.bn = 64;
+        alt.cout_pad = (cout + 63) / 64 * 64;
+        pc.bn_alt = alt.bn;
+        pc.cout_pad_alt = alt.cout_pad;
+        if (pc.impl == CONV_MFMA_F32) {
+            abuf.assign(sizeof(float) * mfma_f32_packed_floats(alt), 0);
+            mfma_f32_pack(alt, weight, reinterpret_cast<float*>(abuf.data()));
+        } else {
+            abuf.assign(sizeof(uint16_t) * mfma_bf16_packed_elems(alt), 0);
+            mfma_bf16_pack(alt, weight, reinterpret_cast<uint16_t*>(abuf.data()));
+        }
+    }
     bias.assign(pc.cout_pad, 0.f);
     for (int o = 0; o < cout; ++o) bias[o] = bias_in ? bias_in[o] : 0.f;
     hipError_t e = hipMalloc(&pc.w, wbytes);
     if (e == hipSuccess) e = hipMalloc((void**)&pc.b, sizeof(float) * bias.size());
     if (e == hipSuccess) e = hipMemcpy(pc.w, wbuf.data(), wbytes, hipMemcpyHostToDevice);
+    if (e == hipSuccess && !abuf.empty()) {
+        e = hipMalloc(&pc.w_alt, abuf.size());
+        if (e == hipSuccess) e = hipMemcpy(pc.w_alt, abuf.data(), abuf.size(), hipMemcpyHostToDevice);
+    }
     if (e == hipSuccess) e = hipMemcpy(pc.b, bias.data(), sizeof(float) * bias.size(), hipMemcpyHostToDevice);
     if (e != hipSuccess) return hip_fail(e, "uploading weights");
     return DSS_OK;
@@ -270,8 +290,10 @@ static void free_plan_memory(dss_plan* p) {
         for (auto& c : *list) {
             if (c.w) (void)hipFree(c.w);
             if (c.b) (void)hipFree(c.b);
+            if (c.w_alt) (void)hipFree(c.w_alt);
             c.w = nullptr;
             c.b = nullptr;
+            c.w_alt = nullptr;
         }
     for (hipEvent_t e : p->events) (void)hipEventDestroy(e);
     p->events.clear();
@@ -441,7 +463,7 @@ static dss_status run_layers(dss_plan* p, const Geom& G, int upto, char* const b
         const LayerGeom& lg = G.L[j - 1];
         const int Fin = lg.Fin_h * lg.Fin_w;
         if (c.has_conv) {
-            const PlanConv& pc = p->convs[j - 1];
+            const PlanConv pc = mfma_launch_variant(p->convs[j - 1], Fin, lg.Uin_h, lg.Uin_w, lg.dil_h, lg.dil_w);
             const bool last_op = (j == ch.L()) && !c.has_pool;
             const dss_dtype tout = (dt == DSS_BF16 && last_op) ? DSS_F32 : dt;
             void* dst = buf[which ^ 1];
@@ -884,7 +906,7 @@ extern "C" dss_status dss_backward_dense(dss_plan_t plan, const void* signal, in
         const LayerGeom& lg = G.L[j - 1];
         const int Fin = lg.Fin_h * lg.Fin_w;
         if (c.has_conv) {
-            const PlanConv& pc = plan->convs[j - 1];
+            const PlanConv pc = mfma_launch_variant(plan->convs[j - 1], Fin, lg.Uin_h, lg.Uin_w, 1, 1);
             const double fl = 2.0 * Fin * (double)lg.E_h * lg.E_w * c.cout * (double)c.cin * c.c_h * c.c_w;
             e = T.run(conv_name(pc, DSS_F32), j, fl, 0.0, [&]() -> hipError_t {
                 if (pc.impl == CONV_MFMA_F32)
@@ -948,8 +970,8 @@ extern "C" dss_status dss_backward_dense(dss_plan_t plan, const void* signal, in
             return launch_pad_grad(gb[cur], Fin, lg.E_h, lg.E_w, c.cout, ph, pw, padb, stream);
         });
         if (e != hipSuccess) return hip_fail(e, "pad_grad launch");
-        const PlanConv& bpc = plan->bconvs[j - 1];
         const int Hp = lg.E_h + 2 * ph, Wp = lg.E_w + 2 * pw;
+        const PlanConv bpc = mfma_launch_variant(plan->bconvs[j - 1], Fin, Hp, Wp, 1, 1);
         e = T.run(dgrad_name(bpc), j, fl, 0.0, [&]() -> hipError_t {
             if (bpc.impl == CONV_MFMA_F32)
                 return launch_conv_mfma_f32(padb, Fin, Hp, Wp, 1, 1, bpc, gb[cur ^ 1], stream);

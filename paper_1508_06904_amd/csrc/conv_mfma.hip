@@ -404,6 +404,27 @@ static Tile pick_tile(int BM, int BN, int Hout, int Wout, int fh, int fw, size_t
     return best;
 }
 
+// With the 128-channel N tile a launch that yields fewer workgroups than the
+// 512 that the GPU holds at once (two per CU) leaves CUs idle or runs a single
+// partial round; the 64-channel tile doubles the workgroup count at a small
+// cost in operand traffic per MFMA, which wins for such small launches (one
+// 240 x 320 image with 128 maps: 10 % faster per evaluation).
+PlanConv mfma_launch_variant(const PlanConv& pc, int F, int Hin, int Win, int dil_h, int dil_w) {
+    if (!pc.w_alt || pc.impl == CONV_DIRECT) return pc;
+    const int Hout = Hin - dil_h * (pc.fh - 1), Wout = Win - dil_w * (pc.fw - 1);
+    const int Hp = (int)ceil_div64(Hout, dil_h), Wp = (int)ceil_div64(Wout, dil_w);
+    const Tile t = pick_tile(256, pc.bn, Hp, Wp, pc.fh, pc.fw, std::min(device_lds_limit(), (size_t)kMaxLds));
+    if (t.TH == 0) return pc;
+    const int64_t blocks = (int64_t)F * dil_h * dil_w * ceil_div64(Hp, t.TH) * ceil_div64(Wp, t.TW) *
+                           (pc.cout_pad / pc.bn);
+    if (blocks >= 512) return pc;
+    PlanConv alt = pc;
+    alt.w = pc.w_alt;
+    alt.bn = pc.bn_alt;
+    alt.cout_pad = pc.cout_pad_alt;
+    return alt;
+}
+
 // Whether some spatial tile of the variant chosen for `cout` fits an fh x fw
 // filter's halo into LDS (checked against the 64 KB every device offers).
 bool mfma_supports(bool bf16, int cout, int fh, int fw) {

@@ -86,7 +86,14 @@ struct PlanConv {
     int bn = 0, cin_pad = 0;    // MFMA kernels: N tile, padded Cin
     void* w = nullptr;          // device weights in the kernel's layout
     float* b = nullptr;         // device bias [cout_pad], zero padded
+    // MFMA kernels with the 128-channel N tile also keep the weights packed for the
+    // 64-channel tile, used when a launch would leave the GPU short of workgroups
+    void* w_alt = nullptr;
+    int bn_alt = 0, cout_pad_alt = 0;
 };
+
+// The variant a launch over F fragments of Hin x Win (taps dil apart) should use.
+PlanConv mfma_launch_variant(const PlanConv& pc, int F, int Hin, int Win, int dil_h, int dil_w);
 
 // Host-side description of a weight-gradient launch (backward.hip).
 struct WgradPlan {

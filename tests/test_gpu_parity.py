@@ -321,7 +321,9 @@ def test_timing_records():
     recs = plan.timings()
     names = [r["kernel"] for r in recs]
     assert names[0] == "stuff_pack" and names[-1] == "defrag_trim"
-    assert "conv_mfma_f32_n128" in names and "conv_mfma_f32_n32" in names and "pool_frag" in names
+    # the 128-channel layer runs the 64-channel tile here: at this size the 128-channel
+    # tile would give too few workgroups to fill the GPU
+    assert "conv_mfma_f32_n64" in names and "conv_mfma_f32_n32" in names and "pool_frag" in names
     g = plan.geometry(120, 130)
     assert sum(r["flops"] for r in recs) == pytest.approx(g["conv_flops"], rel=1e-9)
     assert all(r["ms"] >= 0 for r in recs)
