@@ -48,6 +48,15 @@ __global__ __launch_bounds__(256) void conv_direct_kernel(const Tin* __restrict_
         }
     }
     Tout* op = out + p * Cout + og;
+    if constexpr (sizeof(Tout) == 4 && COB % 4 == 0) {
+        if (Cout % 4 == 0 && og + COB <= Cout) {   // 16-byte aligned: full vectors
+#pragma unroll
+            for (int o = 0; o < COB; o += 4)
+                *reinterpret_cast<float4*>(op + o) = make_float4(activate(act, acc[o]), activate(act, acc[o + 1]),
+                                                                 activate(act, acc[o + 2]), activate(act, acc[o + 3]));
+            return;
+        }
+    }
 #pragma unroll
     for (int o = 0; o < COB; ++o)
         if (og + o < Cout) store_elem(op + o, activate(act, acc[o]));
