@@ -66,11 +66,12 @@ def log(*a):
 def profiled_traffic(kernel, config):
     """HBM bytes per launch of `kernel` on `config` from the committed rocprofv3
     counter summaries (FETCH_SIZE + WRITE_SIZE, scaled by a plain copy), or None
-    when no summary covers it or the kernel source changed since it was taken."""
+    when no summary covers it or the kernel source changed since it was taken
+    (the hash covers the kernel's own source file and the shared device header)."""
     import glob
     import hashlib
-    src = b"".join(open(os.path.join(ROOT, "paper_1508_06904_amd", "csrc", f), "rb").read()
-                   for f in ("conv_mfma.hip", "dev_common.h"))
+    files = ("backward.hip" if kernel.startswith("wgrad") else "conv_mfma.hip", "dev_common.h")
+    src = b"".join(open(os.path.join(ROOT, "paper_1508_06904_amd", "csrc", f), "rb").read() for f in files)
     h = hashlib.sha256(src).hexdigest()[:16]
     for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "*.md"))):
         for line in open(path):

@@ -404,27 +404,6 @@ static Tile pick_tile(int BM, int BN, int Hout, int Wout, int fh, int fw, size_t
     return best;
 }
 
-// With the 128-channel N tile a launch that yields fewer workgroups than the
-// 512 that the GPU holds at once (two per CU) leaves CUs idle or runs a single
-// partial round; the 64-channel tile doubles the workgroup count at a small
-// cost in operand traffic per MFMA, which wins for such small launches (one
-// 240 x 320 image with 128 maps: 10 % faster per evaluation).
-PlanConv mfma_launch_variant(const PlanConv& pc, int F, int Hin, int Win, int dil_h, int dil_w) {
-    if (!pc.w_alt || pc.impl == CONV_DIRECT) return pc;
-    const int Hout = Hin - dil_h * (pc.fh - 1), Wout = Win - dil_w * (pc.fw - 1);
-    const int Hp = (int)ceil_div64(Hout, dil_h), Wp = (int)ceil_div64(Wout, dil_w);
-    const Tile t = pick_tile(256, pc.bn, Hp, Wp, pc.fh, pc.fw, std::min(device_lds_limit(), (size_t)kMaxLds));
-    if (t.TH == 0) return pc;
-    const int64_t blocks = (int64_t)F * dil_h * dil_w * ceil_div64(Hp, t.TH) * ceil_div64(Wp, t.TW) *
-                           (pc.cout_pad / pc.bn);
-    if (blocks >= 512) return pc;
-    PlanConv alt = pc;
-    alt.w = pc.w_alt;
-    alt.bn = pc.bn_alt;
-    alt.cout_pad = pc.cout_pad_alt;
-    return alt;
-}
-
 // Whether some spatial tile of the variant chosen for `cout` fits an fh x fw
 // filter's halo into LDS (checked against the 64 KB every device offers).
 bool mfma_supports(bool bf16, int cout, int fh, int fw) {
@@ -458,68 +437,106 @@ static Tile flat_tile(int BM, int BN, int Win, int fh, int fw, size_t lds_max) {
     return Tile{0, 0, 0, 0};
 }
 
+// The grid of one launch: a spatial tile per fragment (per phase when dilated),
+// or the flat reading of the whole fragment batch when that computes at least
+// 10 % fewer positions (small fragments waste most of a spatial tile; the flat
+// sequence computes Hin*Win positions per fragment, of which only the last
+// fh-1 rows and fw-1 columns are discarded).
+struct LaunchShape {
+    Tile t;
+    int flat;
+    int tilesY, tilesX;
+    int64_t nblocks;    // 0 if no tile fits
+};
+
+static LaunchShape launch_shape(int BM, int BN, int F, int Hin, int Win, int dil_h, int dil_w, int fh, int fw,
+                                int nbs) {
+    LaunchShape L{Tile{0, 0, 0, 0}, 0, 0, 0, 0};
+    const size_t lds = device_lds_limit();
+    if (dil_h * dil_w > 1) {
+        const int Hout = Hin - dil_h * (fh - 1), Wout = Win - dil_w * (fw - 1);
+        const int Hp = (int)ceil_div64(Hout, dil_h), Wp = (int)ceil_div64(Wout, dil_w);
+        L.t = pick_tile(BM, BN, Hp, Wp, fh, fw, lds);
+        if (L.t.TH == 0) return L;
+        L.tilesY = (int)ceil_div64(Hp, L.t.TH);
+        L.tilesX = (int)ceil_div64(Wp, L.t.TW);
+        L.nblocks = (int64_t)dil_h * dil_w * L.tilesY * L.tilesX * nbs;
+        return L;
+    }
+    const int Hout = Hin - fh + 1, Wout = Win - fw + 1;
+    L.t = pick_tile(BM, BN, Hout, Wout, fh, fw, lds);
+    const int64_t flat_len = (int64_t)F * Hin * Win;
+    if (flat_len < (1ll << 30)) {
+        const Tile ft = flat_tile(BM, BN, Win, fh, fw, lds);
+        const int64_t work_tiles =
+            L.t.TH ? (int64_t)F * ceil_div64(Hout, L.t.TH) * L.t.TH * ceil_div64(Wout, L.t.TW) * L.t.TW : -1;
+        const int64_t work_flat = ceil_div64(flat_len, BM) * BM;
+        if (ft.TH && (work_tiles < 0 || 10 * work_flat < 9 * work_tiles)) {
+            L.t = ft;
+            L.flat = 1;
+            L.tilesY = 1;
+            L.tilesX = (int)ceil_div64(flat_len, ft.TW);
+            L.nblocks = (int64_t)L.tilesX * nbs;
+            return L;
+        }
+    }
+    if (L.t.TH == 0) return L;
+    L.tilesY = (int)ceil_div64(Hout, L.t.TH);
+    L.tilesX = (int)ceil_div64(Wout, L.t.TW);
+    L.nblocks = (int64_t)F * L.tilesY * L.tilesX * nbs;
+    return L;
+}
+
+// The 128-channel N tile or the 64-channel one for a launch.  A launch of fewer
+// workgroups than the 512 that the GPU holds at once (two per CU) leaves CUs
+// idle or half-loaded; the 64-channel tile doubles the workgroup count at a
+// cost of about 10 % per MFMA in operand traffic (measured on the conv6x6
+// 256->512 layer of a 135 x 240 fragment).  With every workgroup resident, the
+// busiest CU sets the time: ceil(blocks / 256) workgroups of the 128-channel
+// tile against ceil(blocks64 / 256) of half the work each.  A lone workgroup
+// per CU (one wave per SIMD) hides no MFMA latency, so up to 256 workgroups
+// the 64-channel tile is taken.
+PlanConv mfma_launch_variant(const PlanConv& pc, int F, int Hin, int Win, int dil_h, int dil_w) {
+    if (!pc.w_alt || pc.impl == CONV_DIRECT) return pc;
+    const LaunchShape a = launch_shape(256, pc.bn, F, Hin, Win, dil_h, dil_w, pc.fh, pc.fw, pc.cout_pad / pc.bn);
+    if (a.nblocks == 0 || a.nblocks >= 512) return pc;
+    const LaunchShape b =
+        launch_shape(256, pc.bn_alt, F, Hin, Win, dil_h, dil_w, pc.fh, pc.fw, pc.cout_pad_alt / pc.bn_alt);
+    if (b.nblocks == 0) return pc;
+    if (a.nblocks > 256 && 11 * ceil_div64(b.nblocks, 256) >= 20 * ceil_div64(a.nblocks, 256)) return pc;
+    PlanConv alt = pc;
+    alt.w = pc.w_alt;
+    alt.bn = pc.bn_alt;
+    alt.cout_pad = pc.cout_pad_alt;
+    return alt;
+}
+
 template <bool BF16, typename Tout, int WGM, int WGN, int MT, int NT>
 static hipError_t run_mfma(const void* in, int F, int Hin, int Win, int dil_h, int dil_w, const PlanConv& pc,
                            void* out, hipStream_t s) {
     using Cfg = MfmaCfg<BF16, WGM, WGN, MT, NT>;
-    if (dil_h * dil_w > 1) {
-        // dilated: one signal, tiled per phase (the largest phase has ceil(Hout/dil_h) rows)
-        if (F != 1) return hipErrorInvalidValue;
-        const int Hout = Hin - dil_h * (pc.fh - 1), Wout = Win - dil_w * (pc.fw - 1);
-        const int Hp = (int)ceil_div64(Hout, dil_h), Wp = (int)ceil_div64(Wout, dil_w);
-        const Tile t = pick_tile(Cfg::BM, Cfg::BN, Hp, Wp, pc.fh, pc.fw, device_lds_limit());
-        if (t.TH == 0) return hipErrorInvalidConfiguration;
-        auto kern = conv_mfma_kernel<BF16, Tout, WGM, WGN, MT, NT>;
-        hipError_t e = allow_large_lds((const void*)kern, t.lds);
-        if (e != hipSuccess) return e;
-        const int tilesY = (int)ceil_div64(Hp, t.TH), tilesX = (int)ceil_div64(Wp, t.TW);
-        const int nbs = pc.cout_pad / Cfg::BN;
-        const int64_t nblocks = (int64_t)dil_h * dil_w * tilesY * tilesX * nbs;
-        if (nblocks >= (1ll << 31)) return hipErrorInvalidConfiguration;
-        kern<<<dim3((unsigned)nblocks), Cfg::THREADS, t.lds, s>>>(
-            (const char*)in, Hin, Win, pc.cin, (const char*)pc.w, pc.b, pc.fh, pc.fw, pc.cout, pc.act,
-            pc.cin_pad / Cfg::CC, (Tout*)out, Hout, Wout, t.TH, t.TW, tilesY, tilesX, nbs, t.dbl, 0, 0, dil_h,
-            dil_w);
-        return hipGetLastError();
-    }
-    const int Hout = Hin - pc.fh + 1, Wout = Win - pc.fw + 1;
-    Tile t = pick_tile(Cfg::BM, Cfg::BN, Hout, Wout, pc.fh, pc.fw, device_lds_limit());
-    // Small fragments waste most of a spatial tile; reading the batch as one
-    // flat sequence computes Hin*Win positions per fragment instead (only the
-    // last fh-1 rows and fw-1 columns of each are discarded).
-    int flat = 0;
-    const int64_t flat_len = (int64_t)F * Hin * Win;
-    if (flat_len < (1ll << 30)) {
-        const Tile ft = flat_tile(Cfg::BM, Cfg::BN, Win, pc.fh, pc.fw, device_lds_limit());
-        const int64_t work_tiles = t.TH ? (int64_t)F * ceil_div64(Hout, t.TH) * t.TH * ceil_div64(Wout, t.TW) * t.TW : -1;
-        const int64_t work_flat = ceil_div64(flat_len, Cfg::BM) * Cfg::BM;
-        if (ft.TH && (work_tiles < 0 || 10 * work_flat < 9 * work_tiles)) {
-            t = ft;
-            flat = 1;
-        }
-    }
-    if (t.TH == 0) return hipErrorInvalidConfiguration;
-    auto kern = conv_mfma_kernel<BF16, Tout, WGM, WGN, MT, NT>;
-    hipError_t e = allow_large_lds((const void*)kern, t.lds);
-    if (e != hipSuccess) return e;
+    const bool dilated = dil_h * dil_w > 1;
+    if (dilated && F != 1) return hipErrorInvalidValue;   // dilated: one signal, tiled per phase
     const int nbs = pc.cout_pad / Cfg::BN;
+    const LaunchShape L = launch_shape(Cfg::BM, Cfg::BN, F, Hin, Win, dil_h, dil_w, pc.fh, pc.fw, nbs);
+    if (L.nblocks == 0) return hipErrorInvalidConfiguration;
+    if (L.nblocks >= (1ll << 31)) return hipErrorInvalidConfiguration;
+    auto kern = conv_mfma_kernel<BF16, Tout, WGM, WGN, MT, NT>;
+    hipError_t e = allow_large_lds((const void*)kern, L.t.lds);
+    if (e != hipSuccess) return e;
     const int nchunks = pc.cin_pad / Cfg::CC;
-    if (flat) {
-        // one "fragment" of 1 x flat_len samples for the staging and the tile grid
-        const int tilesX = (int)ceil_div64(flat_len, t.TW);
-        const int64_t nblocks = (int64_t)tilesX * nbs;
-        if (nblocks >= (1ll << 31)) return hipErrorInvalidConfiguration;
-        kern<<<dim3((unsigned)nblocks), Cfg::THREADS, t.lds, s>>>(
-            (const char*)in, 1, (int)flat_len, pc.cin, (const char*)pc.w, pc.b, pc.fh, pc.fw, pc.cout, pc.act,
-            nchunks, (Tout*)out, Hout, Wout, 1, t.TW, 1, tilesX, nbs, t.dbl, Hin, Win, 1, 1);
+    const int Hout = Hin - dil_h * (pc.fh - 1), Wout = Win - dil_w * (pc.fw - 1);
+    if (L.flat) {
+        // one "fragment" of 1 x (F * Hin * Win) samples for the staging and the tile grid
+        const int flat_len = (int)((int64_t)F * Hin * Win);   // below 2^30 in flat mode
+        kern<<<dim3((unsigned)L.nblocks), Cfg::THREADS, L.t.lds, s>>>(
+            (const char*)in, 1, flat_len, pc.cin, (const char*)pc.w, pc.b, pc.fh, pc.fw, pc.cout, pc.act, nchunks,
+            (Tout*)out, Hout, Wout, 1, L.t.TW, 1, L.tilesX, nbs, L.t.dbl, Hin, Win, 1, 1);
         return hipGetLastError();
     }
-    const int tilesY = (int)ceil_div64(Hout, t.TH), tilesX = (int)ceil_div64(Wout, t.TW);
-    const int64_t nblocks = (int64_t)F * tilesY * tilesX * nbs;
-    if (nblocks >= (1ll << 31)) return hipErrorInvalidConfiguration;
-    kern<<<dim3((unsigned)nblocks), Cfg::THREADS, t.lds, s>>>(
+    kern<<<dim3((unsigned)L.nblocks), Cfg::THREADS, L.t.lds, s>>>(
         (const char*)in, Hin, Win, pc.cin, (const char*)pc.w, pc.b, pc.fh, pc.fw, pc.cout, pc.act, nchunks,
-        (Tout*)out, Hout, Wout, t.TH, t.TW, tilesY, tilesX, nbs, t.dbl, 0, 0, 1, 1);
+        (Tout*)out, Hout, Wout, L.t.TH, L.t.TW, L.tilesY, L.tilesX, nbs, L.t.dbl, 0, 0, dil_h, dil_w);
     return hipGetLastError();
 }
 
