@@ -23,8 +23,10 @@
 //                      flipped filters (the forward convolution kernels run it).
 //  wgrad_mfma          dW[o][i][t] = sum_p dy[p][o] x[p + t][i]: per tap a GEMM
 //                      over all output positions p of all fragments (MFMA
-//                      32x32x2 binary32, split over p, partial sums reduced in a
-//                      fixed order by wgrad_reduce).
+//                      32x32x2 binary32); a workgroup takes the taps of one
+//                      filter row, which share their operand rows shifted by
+//                      the tap; split over p, partial sums reduced in a fixed
+//                      order by wgrad_reduce.
 //  bias_partial/reduce db[o] = sum_p dy[p][o], two fixed-order passes.
 //  crop_to_planar      transpose of Stuff: the stuffed input's gradient cropped
 //                      to the signal and written planar.
@@ -188,35 +190,41 @@ hipError_t launch_pad_grad(const float* in, int F, int E_h, int E_w, int C, int 
 // ------------------------------------------------------------------ wgrad (MFMA)
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 
-constexpr int kWM = 128;              // workgroup tile: output channels
+constexpr int kWT = 64;               // workgroup tile: 64 output x 64 input channels
 constexpr int kKC = 32;               // positions per chunk
-constexpr int kWP = 160;              // LDS row pitch in floats: 128 + 32, so the two half-waves
-                                      // of a read hit disjoint banks
-constexpr size_t kWgradLds = 2 * 2 * kKC * kWP * sizeof(float);
+constexpr int kWP = kWT + 32;         // LDS row pitch in floats: the two half-waves of a read
+                                      // (rows p and p + 1) hit disjoint banks
+constexpr int kMaxTT = 8;             // taps of one filter row per workgroup
 
-// Workgroup (o tile, i tile, tap, split): 4 waves in a 2 x 2 grid, each a
-// 64 x (32 NTW) block of MFMA 32x32x2 tiles, so the workgroup covers 128 output
-// channels and 64 NTW input channels (NTW = 1 for layers with at most 64 input
-// channels).  The output positions p of all fragments are numbered row-major
-// (fragment, row, column); chunk c holds positions 32c .. 32c + 31 and split s
-// takes chunks [c0, c1).  Position p's gradient row is dy[p]; its input sample
-// for tap (t_h, t_w) is x[f][y + t_h][x + t_w].
-template <bool VEC, int NTW>
-__global__ __launch_bounds__(256) void wgrad_mfma_kernel(const float* __restrict__ dy, const float* __restrict__ x,
-                                                        int E_h, int E_w, int U_h, int U_w, int Cout, int Cin,
-                                                        int fh, int fw, int64_t P, int64_t nchunks, int otiles,
-                                                        int itiles, int splits, float* __restrict__ partial) {
-    constexpr int BNW = 64 * NTW;                 // input channels per workgroup
-    constexpr int TPR = BNW / 4;                  // staging threads per B row (4 channels each)
-    constexpr int RPP = 256 / TPR;                // B rows per staging pass
-    constexpr int BPASS = kKC / RPP;
+static size_t wgrad_lds_bytes(int tt) { return 2 * (size_t)(kKC + kKC + tt - 1) * kWP * sizeof(float); }
+
+// Workgroup (o tile, i tile, tap row t_h, tap group, split) computes
+//   dW[o][i][t_h][t_w] = sum_p dy[p][o] x[f][y + t_h][x + t_w][i]
+// for 64 output channels, 64 input channels and the taps t_w of one group of up
+// to TT consecutive taps of filter row t_h.  4 waves in a 2 x 2 grid, each a
+// 32 x 32 MFMA tile per tap.
+//
+// Positions are numbered over the input width: q = (f E_h + y) U_w + x for
+// x < U_w, of which x < E_w are output positions (dy row (f E_h + y) E_w + x)
+// and the rest carry a zero gradient.  Then the input sample of tap (t_h, t_w)
+// at q is the tap (t_h, 0) sample at q + t_w: within a row x + t_w < U_w for
+// every output position.  A chunk of 32 positions therefore stages the dy rows
+// of its 32 positions and the x rows of 32 + TT - 1 positions once, and every tap
+// of the group reads its operand rows t_w further on in LDS -- TT times fewer
+// global reads than one workgroup per tap.
+template <bool VEC, int TT>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void wgrad_mfma_kernel(const float* __restrict__ dy, const float* __restrict__ x,
+                                                        int E_h, int E_w, int U_h, int U_w, int Cout, int Cin, int fh,
+                                                        int fw, int Q, int nchunks, int otiles, int itiles, int ntg,
+                                                        int splits, float* __restrict__ partial) {
+    constexpr int RB = kKC + TT - 1;              // staged x rows per chunk
     extern __shared__ __attribute__((aligned(16))) float wl[];
-    // A (output-gradient) chunks in buffers 0/1, B (input) chunks in buffers 2/3
-    auto lds_buf = [&](int k) { return wl + k * (kKC * kWP); };
+    auto lds_a = [&](int buf) { return wl + buf * (kKC * kWP); };                  // dy rows
+    auto lds_b = [&](int buf) { return wl + 2 * kKC * kWP + buf * (RB * kWP); };   // x rows
     // Workgroups are handed to the 8 XCDs round-robin by id; remap so that every
     // XCD runs one contiguous range of the logical order (o tile, i tile, tap
-    // fastest, split slowest): the workgroups on an XCD then read the same chunks
-    // of dy and x from its L2.
+    // group, tap row fastest, split slowest): the workgroups on an XCD then read
+    // the same chunks of dy and x from its L2.
     const int total = gridDim.x;
     const int xcd = blockIdx.x % 8, slot = blockIdx.x / 8;
     const int q8 = total / 8, r8 = total % 8;
@@ -225,27 +233,26 @@ __global__ __launch_bounds__(256) void wgrad_mfma_kernel(const float* __restrict
     bid /= otiles;
     const int it = bid % itiles;
     bid /= itiles;
-    const int taps = fh * fw;
-    const int tap = bid % taps;
-    const int split = bid / taps;
-    const int th = tap / fw, tw = tap % fw;
-    const int64_t c0 = nchunks * split / splits, c1 = nchunks * (split + 1) / splits;
-    const int o0 = ot * kWM, i0 = it * BNW;
+    const int tg = bid % ntg;
+    bid /= ntg;
+    const int th = bid % fh;
+    const int split = bid / fh;
+    const int tw0 = tg * TT;
+    const int ntt = min(TT, fw - tw0);            // taps of this group
+    const int c0 = (int)((int64_t)nchunks * split / splits), c1 = (int)((int64_t)nchunks * (split + 1) / splits);
+    const int o0 = ot * kWT, i0 = it * kWT;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave & 1, wn = wave >> 1, half = lane >> 5, l32 = lane & 31;
-    const int a_col = (tid & 31) * 4, a_row = tid >> 5;        // A staging: rows a_row + 8 k
-    const int b_col = (tid % TPR) * 4, b_row = tid / TPR;      // B staging: rows b_row + RPP k
-    const int64_t plane = (int64_t)E_h * E_w;
+    const int s_col = (tid & 15) * 4, s_row = tid >> 4;          // staging: 16 float4 per row, 16 rows per pass
+    const int rowlen = E_h * U_w;                                // positions per fragment
 
-    floatx16 acc[2][NTW];
+    floatx16 acc[TT];
 #pragma unroll
-    for (int a = 0; a < 2; ++a)
+    for (int t = 0; t < TT; ++t)
 #pragma unroll
-        for (int b = 0; b < NTW; ++b)
-#pragma unroll
-            for (int v = 0; v < 16; ++v) acc[a][b][v] = 0.f;
+        for (int v = 0; v < 16; ++v) acc[t][v] = 0.f;
 
-    float4 ra[4], rb[BPASS];
+    float4 ra[2], rb[3];
     auto load4 = [&](const float* base, int c_lo, int C, bool ok) -> float4 {
         if (!ok) return make_float4(0.f, 0.f, 0.f, 0.f);
         if (VEC) return c_lo + 3 < C ? *reinterpret_cast<const float4*>(base + c_lo) : make_float4(0.f, 0.f, 0.f, 0.f);
@@ -254,29 +261,30 @@ __global__ __launch_bounds__(256) void wgrad_mfma_kernel(const float* __restrict
         for (int e = 0; e < 4; ++e) v[e] = c_lo + e < C ? base[c_lo + e] : 0.f;
         return make_float4(v[0], v[1], v[2], v[3]);
     };
-    auto load_chunk = [&](int64_t c) {
-        const int64_t pc = c * kKC;
+    auto load_chunk = [&](int c) {
+        const int qc = c * kKC;
 #pragma unroll
-        for (int k = 0; k < 4; ++k) {
-            const int64_t p = pc + a_row + 8 * k;
-            ra[k] = load4(dy + p * Cout, o0 + a_col, Cout, p < P);
+        for (int k = 0; k < 2; ++k) {
+            const int q = qc + s_row + 16 * k;
+            const int r = q / U_w, xx = q - r * U_w;              // r = f E_h + y
+            ra[k] = load4(dy + ((int64_t)r * E_w + xx) * Cout, o0 + s_col, Cout, q < Q && xx < E_w);
         }
 #pragma unroll
-        for (int k = 0; k < BPASS; ++k) {
-            const int64_t p = pc + b_row + RPP * k;
-            const int64_t f = p / plane;
-            const int r = (int)(p - f * plane);
-            const int y = r / E_w, xx = r - y * E_w;
-            rb[k] = load4(x + ((f * U_h + y + th) * U_w + xx + tw) * Cin, i0 + b_col, Cin, p < P);
+        for (int k = 0; k < 3; ++k) {
+            const int row = s_row + 16 * k;
+            const int q = qc + tw0 + row;
+            const int f = q / rowlen;
+            const int64_t src = (int64_t)q + (int64_t)f * (fh - 1) * U_w + (int64_t)th * U_w;
+            rb[k] = row < RB ? load4(x + src * Cin, i0 + s_col, Cin, q < Q) : make_float4(0.f, 0.f, 0.f, 0.f);
         }
     };
     auto store_chunk = [&](int buf) {
 #pragma unroll
-        for (int k = 0; k < 4; ++k)
-            *reinterpret_cast<float4*>(lds_buf(buf) + (a_row + 8 * k) * kWP + a_col) = ra[k];
+        for (int k = 0; k < 2; ++k)
+            *reinterpret_cast<float4*>(lds_a(buf) + (s_row + 16 * k) * kWP + s_col) = ra[k];
 #pragma unroll
-        for (int k = 0; k < BPASS; ++k)
-            *reinterpret_cast<float4*>(lds_buf(2 + buf) + (b_row + RPP * k) * kWP + b_col) = rb[k];
+        for (int k = 0; k < 3; ++k)
+            if (s_row + 16 * k < RB) *reinterpret_cast<float4*>(lds_b(buf) + (s_row + 16 * k) * kWP + s_col) = rb[k];
     };
 
     if (c0 < c1) {
@@ -284,43 +292,41 @@ __global__ __launch_bounds__(256) void wgrad_mfma_kernel(const float* __restrict
         store_chunk(0);
     }
     __syncthreads();
-    for (int64_t c = c0; c < c1; ++c) {
-        const int buf = (int)((c - c0) & 1);
+    for (int c = c0; c < c1; ++c) {
+        const int buf = (c - c0) & 1;
         const bool more = c + 1 < c1;
         if (more) load_chunk(c + 1);
-        const float* A = lds_buf(buf);
-        const float* Bm = lds_buf(2 + buf);
+        const float* A = lds_a(buf) + wm * 32 + l32;
+        const float* Bm = lds_b(buf) + wn * 32 + l32;
+        // all TT taps even in a ragged last group (the extra ones are not stored):
+        // a tap-dependent branch here would keep a second copy of the accumulators
 #pragma unroll 4
         for (int ks = 0; ks < kKC / 2; ++ks) {
             const int p = 2 * ks + half;
-            float av[2], bv[NTW];
+            const float av = A[p * kWP];
+            float bv[TT];
 #pragma unroll
-            for (int mt = 0; mt < 2; ++mt) av[mt] = A[p * kWP + wm * 64 + mt * 32 + l32];
+            for (int t = 0; t < TT; ++t) bv[t] = Bm[(p + t) * kWP];
 #pragma unroll
-            for (int nt = 0; nt < NTW; ++nt) bv[nt] = Bm[p * kWP + wn * 32 * NTW + nt * 32 + l32];
-#pragma unroll
-            for (int mt = 0; mt < 2; ++mt)
-#pragma unroll
-                for (int nt = 0; nt < NTW; ++nt)
-                    acc[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[mt], bv[nt], acc[mt][nt], 0, 0, 0);
+            for (int t = 0; t < TT; ++t) acc[t] = __builtin_amdgcn_mfma_f32_32x32x2f32(av, bv[t], acc[t], 0, 0, 0);
         }
         if (more) store_chunk(buf ^ 1);
         __syncthreads();
     }
 
     // D[i][j] of a 32x32 tile sits in lane j + 32*((i/4)%2), register (i/8)*4 + i%4
-    float* dst = partial + ((size_t)split * taps + tap) * Cout * Cin;
+    const int taps = fh * fw;
+    const int ii = i0 + wn * 32 + l32;
 #pragma unroll
-    for (int mt = 0; mt < 2; ++mt)
+    for (int t = 0; t < TT; ++t) {
+        if (t >= ntt) break;
+        float* dst = partial + ((size_t)split * taps + th * fw + tw0 + t) * Cout * Cin;
 #pragma unroll
-        for (int nt = 0; nt < NTW; ++nt) {
-            const int ii = i0 + wn * 32 * NTW + nt * 32 + l32;
-#pragma unroll
-            for (int v = 0; v < 16; ++v) {
-                const int o = o0 + wm * 64 + mt * 32 + (v >> 2) * 8 + half * 4 + (v & 3);
-                if (o < Cout && ii < Cin) dst[(size_t)o * Cin + ii] = acc[mt][nt][v];
-            }
+        for (int v = 0; v < 16; ++v) {
+            const int o = o0 + wm * 32 + (v >> 2) * 8 + half * 4 + (v & 3);
+            if (o < Cout && ii < Cin) dst[(size_t)o * Cin + ii] = acc[t][v];
         }
+    }
 }
 
 // dW[o][i][th][tw] = sum over splits (in order) of partial[s][tap][o][i].
@@ -352,16 +358,25 @@ static hipError_t allow_lds(const void* kern, size_t lds) {
 
 WgradPlan wgrad_plan(int F, int E_h, int E_w, int Cout, int Cin, int fh, int fw) {
     WgradPlan w;
-    w.ntw = Cin <= 64 ? 1 : 2;
-    w.positions = (int64_t)F * E_h * E_w;
+    // the largest group of taps (at most kMaxTT) whose ragged last group wastes at
+    // most a tenth of the row's MFMA work
+    for (int tt = std::min(fw, kMaxTT); tt >= 1; --tt) {
+        const int ntg = (fw + tt - 1) / tt;
+        if (10 * (ntg * tt - fw) <= fw) {
+            w.tt = tt;
+            w.ntg = ntg;
+            break;
+        }
+    }
+    w.positions = (int64_t)F * E_h * (E_w + fw - 1);
     w.nchunks = (w.positions + kKC - 1) / kKC;
-    w.otiles = (Cout + kWM - 1) / kWM;
-    w.itiles = (Cin + 64 * w.ntw - 1) / (64 * w.ntw);
-    const int64_t base = (int64_t)w.otiles * w.itiles * fh * fw;
-    // Two workgroups fit a CU (80 KB of LDS each), 512 run at once.  Take at
-    // least eight rounds of 512 workgroups and, among the split counts up to
-    // twice that, the one whose last round is fullest; every split keeps at least
-    // 8 chunks.
+    w.otiles = (Cout + kWT - 1) / kWT;
+    w.itiles = (Cin + kWT - 1) / kWT;
+    const int64_t base = (int64_t)w.otiles * w.itiles * fh * w.ntg;
+    // About 512 workgroups run at once (two or three per CU, 53-55 KB of LDS
+    // each).  Take at least eight rounds of 512 and, among the split counts up
+    // to twice that, the one whose last round is fullest; every split keeps at
+    // least 8 chunks.
     const int64_t max_splits = std::max<int64_t>(1, std::min<int64_t>(4096, w.nchunks / 8));
     const int64_t lo = std::min(max_splits, std::max<int64_t>(1, (512 * 8 + base - 1) / base));
     const int64_t hi = std::min(max_splits, 2 * lo);
@@ -380,30 +395,45 @@ WgradPlan wgrad_plan(int F, int E_h, int E_w, int Cout, int Cin, int fh, int fw)
     return w;
 }
 
-template <bool VEC, int NTW>
+template <bool VEC, int TT>
 static hipError_t run_wgrad(const float* dy, const float* x, int E_h, int E_w, int U_h, int U_w, int Cout, int Cin,
                             int fh, int fw, const WgradPlan& w, float* partial, hipStream_t s) {
-    auto kern = wgrad_mfma_kernel<VEC, NTW>;
-    hipError_t e = allow_lds((const void*)kern, kWgradLds);
+    auto kern = wgrad_mfma_kernel<VEC, TT>;
+    const size_t lds = wgrad_lds_bytes(TT);
+    hipError_t e = allow_lds((const void*)kern, lds);
     if (e != hipSuccess) return e;
-    const int64_t nblocks = (int64_t)w.otiles * w.itiles * fh * fw * w.splits;
+    const int64_t nblocks = (int64_t)w.otiles * w.itiles * fh * w.ntg * w.splits;
     if (nblocks >= (1ll << 31)) return hipErrorInvalidConfiguration;
-    kern<<<dim3((unsigned)nblocks), 256, kWgradLds, s>>>(dy, x, E_h, E_w, U_h, U_w, Cout, Cin, fh, fw, w.positions,
-                                                         w.nchunks, w.otiles, w.itiles, w.splits, partial);
+    kern<<<dim3((unsigned)nblocks), 256, lds, s>>>(dy, x, E_h, E_w, U_h, U_w, Cout, Cin, fh, fw, (int)w.positions,
+                                                   (int)w.nchunks, w.otiles, w.itiles, w.ntg, w.splits, partial);
     return hipGetLastError();
+}
+
+template <bool VEC>
+static hipError_t dispatch_wgrad(const float* dy, const float* x, int E_h, int E_w, int U_h, int U_w, int Cout,
+                                 int Cin, int fh, int fw, const WgradPlan& w, float* partial, hipStream_t s) {
+    switch (w.tt) {
+        case 1: return run_wgrad<VEC, 1>(dy, x, E_h, E_w, U_h, U_w, Cout, Cin, fh, fw, w, partial, s);
+        case 2: return run_wgrad<VEC, 2>(dy, x, E_h, E_w, U_h, U_w, Cout, Cin, fh, fw, w, partial, s);
+        case 3: return run_wgrad<VEC, 3>(dy, x, E_h, E_w, U_h, U_w, Cout, Cin, fh, fw, w, partial, s);
+        case 4: return run_wgrad<VEC, 4>(dy, x, E_h, E_w, U_h, U_w, Cout, Cin, fh, fw, w, partial, s);
+        case 5: return run_wgrad<VEC, 5>(dy, x, E_h, E_w, U_h, U_w, Cout, Cin, fh, fw, w, partial, s);
+        case 6: return run_wgrad<VEC, 6>(dy, x, E_h, E_w, U_h, U_w, Cout, Cin, fh, fw, w, partial, s);
+        case 7: return run_wgrad<VEC, 7>(dy, x, E_h, E_w, U_h, U_w, Cout, Cin, fh, fw, w, partial, s);
+        case 8: return run_wgrad<VEC, 8>(dy, x, E_h, E_w, U_h, U_w, Cout, Cin, fh, fw, w, partial, s);
+    }
+    return hipErrorInvalidValue;
 }
 
 hipError_t launch_wgrad(const float* dy, const float* x, int F, int E_h, int E_w, int U_h, int U_w, int Cout, int Cin,
                         int fh, int fw, const WgradPlan& w, float* partial, float* dw, hipStream_t s) {
     (void)F;
+    // positions and chunks are 32-bit in the kernel
+    if (w.positions + w.tt + kKC >= (1ll << 31) || U_w != E_w + fw - 1 || U_h != E_h + fh - 1)
+        return hipErrorInvalidConfiguration;
     const bool vec = Cout % 4 == 0 && Cin % 4 == 0;
-    hipError_t e;
-    if (w.ntw == 1)
-        e = vec ? run_wgrad<true, 1>(dy, x, E_h, E_w, U_h, U_w, Cout, Cin, fh, fw, w, partial, s)
-                : run_wgrad<false, 1>(dy, x, E_h, E_w, U_h, U_w, Cout, Cin, fh, fw, w, partial, s);
-    else
-        e = vec ? run_wgrad<true, 2>(dy, x, E_h, E_w, U_h, U_w, Cout, Cin, fh, fw, w, partial, s)
-                : run_wgrad<false, 2>(dy, x, E_h, E_w, U_h, U_w, Cout, Cin, fh, fw, w, partial, s);
+    hipError_t e = vec ? dispatch_wgrad<true>(dy, x, E_h, E_w, U_h, U_w, Cout, Cin, fh, fw, w, partial, s)
+                       : dispatch_wgrad<false>(dy, x, E_h, E_w, U_h, U_w, Cout, Cin, fh, fw, w, partial, s);
     if (e != hipSuccess) return e;
     const int64_t n = (int64_t)Cout * Cin * fh * fw;
     wgrad_reduce_kernel<<<dim3((unsigned)ceil_div64(n, kBT)), kBT, 0, s>>>(partial, w.splits, fh * fw, Cout, Cin, dw);

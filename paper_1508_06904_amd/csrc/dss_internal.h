@@ -97,9 +97,10 @@ PlanConv mfma_launch_variant(const PlanConv& pc, int F, int Hin, int Win, int di
 
 // Host-side description of a weight-gradient launch (backward.hip).
 struct WgradPlan {
-    int ntw = 2;                 // MFMA tiles per wave along the input channels (1 or 2)
+    int tt = 1, ntg = 1;         // taps per workgroup and tap groups per filter row
     int otiles = 0, itiles = 0, splits = 0;
-    int64_t positions = 0, nchunks = 0, partial_floats = 0;
+    int64_t positions = 0;       // F * E_h * U_w: output rows read over the input width
+    int64_t nchunks = 0, partial_floats = 0;
 };
 
 struct LaunchRec {
