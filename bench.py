@@ -190,17 +190,19 @@ def main():
         log("warmup %d done" % i)
 
     plan.set_timing(True)
-    start = torch.cuda.Event(enable_timing=True)
-    end = torch.cuda.Event(enable_timing=True)
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     torch.cuda.synchronize()
     t_wall = time.perf_counter()
-    start.record()
-    for _ in range(args.steps):
+    evs[0].record()
+    for i in range(args.steps):
         step()
-    end.record()
+        evs[i + 1].record()
     torch.cuda.synchronize()
     wall_s = time.perf_counter() - t_wall
-    ms_total = start.elapsed_time(end)
+    ms_total = evs[0].elapsed_time(evs[-1])
+    ms_steps = sorted(evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps))
+    ms_median = ms_steps[len(ms_steps) // 2] if len(ms_steps) % 2 else 0.5 * (
+        ms_steps[len(ms_steps) // 2 - 1] + ms_steps[len(ms_steps) // 2])
     recs = plan.timings()
     plan.set_timing(False)
     ms_per_step = ms_total / args.steps
@@ -249,6 +251,7 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": ms_per_step,
+        "ms_per_step_median": ms_median,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,

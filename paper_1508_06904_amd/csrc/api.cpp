@@ -757,7 +757,7 @@ namespace {
 struct BwdLayout {
     Geom G;                                  // dense geometry (ell = 0)
     std::vector<int64_t> a_off, c_off;       // byte offsets: A_0..A_L, conv outputs C_1..C_L
-    int64_t g_off[2] = {0, 0}, pad_off = 0, wpart_off = 0, bpart_off = 0, total = 0;
+    int64_t g_off[2] = {0, 0}, pad_off = 0, wpart_off = 0, total = 0;
     std::vector<WgradPlan> wg;               // per chain layer with a convolution
     std::vector<int64_t> wofs, bofs;         // float offsets of each conv's gradients in the outputs
     int64_t wfloats = 0, bfloats = 0;
@@ -779,7 +779,7 @@ dss_status backward_layout(const Chain& ch, int H, int W, bool want_dx, BwdLayou
     B.a_off.assign(L + 1, 0);
     B.c_off.assign(L + 1, 0);
     B.a_off[0] = take(asz[0]);
-    int64_t gmax = asz[0], padmax = 0, wpmax = 0, bpmax = 0;
+    int64_t gmax = asz[0], padmax = 0, wpmax = 0;
     B.wg.resize(L + 1);
     B.wofs.assign(L + 1, -1);
     B.bofs.assign(L + 1, -1);
@@ -803,8 +803,7 @@ dss_status backward_layout(const Chain& ch, int H, int W, bool want_dx, BwdLayou
                                               c.cout * 4);
             }
             B.wg[j] = wgrad_plan((int)Fin, lg.E_h, lg.E_w, c.cout, c.cin, c.c_h, c.c_w);
-            wpmax = std::max(wpmax, B.wg[j].partial_floats * 4);
-            bpmax = std::max(bpmax, (int64_t)bias_blocks(Fin * lg.E_h * lg.E_w) * c.cout * 4);
+            wpmax = std::max(wpmax, (B.wg[j].partial_floats + B.wg[j].bias_partial_floats) * 4);
             B.wofs[j] = B.wfloats;
             B.bofs[j] = B.bfloats;
             B.wfloats += (int64_t)c.cout * c.cin * c.c_h * c.c_w;
@@ -815,7 +814,6 @@ dss_status backward_layout(const Chain& ch, int H, int W, bool want_dx, BwdLayou
     B.g_off[1] = take(gmax);
     B.pad_off = take(std::max<int64_t>(padmax, 256));
     B.wpart_off = take(std::max<int64_t>(wpmax, 256));
-    B.bpart_off = take(std::max<int64_t>(bpmax, 256));
     B.total = off;
     *out = std::move(B);
     return DSS_OK;
@@ -893,7 +891,6 @@ extern "C" dss_status dss_backward_dense(dss_plan_t plan, const void* signal, in
     float* gb[2] = {(float*)(ws + B.g_off[0]), (float*)(ws + B.g_off[1])};
     float* padb = (float*)(ws + B.pad_off);
     float* wpart = (float*)(ws + B.wpart_off);
-    float* bpart = (float*)(ws + B.bpart_off);
     Timer T(plan, stream);
 
     // forward, keeping every layer's convolution output and pool output
@@ -956,14 +953,9 @@ extern "C" dss_status dss_backward_dense(dss_plan_t plan, const void* signal, in
         const WgradPlan& wp = B.wg[j];
         e = T.run("wgrad_mfma", j, fl, 0.0, [&] {
             return launch_wgrad(gb[cur], A(j - 1), Fin, lg.E_h, lg.E_w, lg.Uin_h, lg.Uin_w, c.cout, c.cin, c.c_h, c.c_w,
-                                wp, wpart, grad_weight + B.wofs[j], stream);
+                                wp, wpart, grad_weight + B.wofs[j], grad_bias + B.bofs[j], stream);
         });
         if (e != hipSuccess) return hip_fail(e, "wgrad launch");
-        e = T.run("bias_grad", j, 0.0, 0.0, [&] {
-            return launch_bias_grad(gb[cur], (int64_t)Fin * lg.E_h * lg.E_w, c.cout, bpart, grad_bias + B.bofs[j],
-                                    stream);
-        });
-        if (e != hipSuccess) return hip_fail(e, "bias_grad launch");
         if (j == 1 && !grad_signal) break;
         const int ph = c.c_h - 1, pw = c.c_w - 1;
         e = T.run("pad_grad", j, 0.0, 0.0, [&] {

@@ -26,8 +26,8 @@
 //                      32x32x2 binary32); a workgroup takes the taps of one
 //                      filter row, which share their operand rows shifted by
 //                      the tap; split over p, partial sums reduced in a fixed
-//                      order by wgrad_reduce.
-//  bias_partial/reduce db[o] = sum_p dy[p][o], two fixed-order passes.
+//                      order by wgrad_reduce.  The same launch sums dy over p for
+//                      the bias gradient db[o].
 //  crop_to_planar      transpose of Stuff: the stuffed input's gradient cropped
 //                      to the signal and written planar.
 #include <algorithm>
@@ -216,7 +216,8 @@ template <bool VEC, int TT>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void wgrad_mfma_kernel(const float* __restrict__ dy, const float* __restrict__ x,
                                                         int E_h, int E_w, int U_h, int U_w, int Cout, int Cin, int fh,
                                                         int fw, int Q, int nchunks, int otiles, int itiles, int ntg,
-                                                        int splits, float* __restrict__ partial) {
+                                                        int splits, float* __restrict__ partial,
+                                                        float* __restrict__ bias_partial) {
     constexpr int RB = kKC + TT - 1;              // staged x rows per chunk
     extern __shared__ __attribute__((aligned(16))) float wl[];
     auto lds_a = [&](int buf) { return wl + buf * (kKC * kWP); };                  // dy rows
@@ -252,6 +253,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void w
 #pragma unroll
         for (int v = 0; v < 16; ++v) acc[t][v] = 0.f;
 
+    float bsum = 0.f;   // sum of this lane's dy column over its positions (bias gradient)
     float4 ra[2], rb[3];
     auto load4 = [&](const float* base, int c_lo, int C, bool ok) -> float4 {
         if (!ok) return make_float4(0.f, 0.f, 0.f, 0.f);
@@ -304,6 +306,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void w
         for (int ks = 0; ks < kKC / 2; ++ks) {
             const int p = 2 * ks + half;
             const float av = A[p * kWP];
+            bsum += av;
             float bv[TT];
 #pragma unroll
             for (int t = 0; t < TT; ++t) bv[t] = Bm[(p + t) * kWP];
@@ -313,6 +316,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void w
         if (more) store_chunk(buf ^ 1);
         __syncthreads();
     }
+
+    // db[o] = sum_p dy[p][o]: one wave per output-channel half of the workgroups
+    // of the first input tile, tap row and tap group adds its two half-wave sums
+    bsum += __shfl_xor(bsum, 32);
+    if (it == 0 && tg == 0 && th == 0 && wn == 0 && half == 0 && o0 + wm * 32 + l32 < Cout)
+        bias_partial[(size_t)split * Cout + o0 + wm * 32 + l32] = bsum;
 
     // D[i][j] of a 32x32 tile sits in lane j + 32*((i/4)%2), register (i/8)*4 + i%4
     const int taps = fh * fw;
@@ -329,12 +338,22 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void w
     }
 }
 
-// dW[o][i][th][tw] = sum over splits (in order) of partial[s][tap][o][i].
-__global__ __launch_bounds__(kBT) void wgrad_reduce_kernel(const float* __restrict__ partial, int splits, int taps,
-                                                          int Cout, int Cin, float* __restrict__ dw) {
+// dW[o][i][th][tw] = sum over splits (in order) of partial[s][tap][o][i], and
+// db[o] = sum over splits (in order) of bias_partial[s][o].
+__global__ __launch_bounds__(kBT) void wgrad_reduce_kernel(const float* __restrict__ partial,
+                                                          const float* __restrict__ bias_partial, int splits,
+                                                          int taps, int Cout, int Cin, float* __restrict__ dw,
+                                                          float* __restrict__ db) {
     const int64_t n = (int64_t)Cout * Cin * taps;
     const int64_t p = (int64_t)blockIdx.x * kBT + threadIdx.x;
-    if (p >= n) return;
+    if (p >= n) {
+        const int64_t o = p - n;
+        if (o >= Cout) return;
+        float s = 0.f;
+        for (int k = 0; k < splits; ++k) s += bias_partial[(int64_t)k * Cout + o];
+        db[o] = s;
+        return;
+    }
     const int tap = (int)(p % taps);
     const int64_t oi = p / taps;                 // o * Cin + i
     const int64_t stride = (int64_t)taps * Cout * Cin;
@@ -392,12 +411,13 @@ WgradPlan wgrad_plan(int F, int E_h, int E_w, int Cout, int Cin, int fh, int fw)
     }
     w.splits = (int)best;
     w.partial_floats = (int64_t)w.splits * fh * fw * Cout * Cin;
+    w.bias_partial_floats = (int64_t)w.splits * Cout;
     return w;
 }
 
 template <bool VEC, int TT>
 static hipError_t run_wgrad(const float* dy, const float* x, int E_h, int E_w, int U_h, int U_w, int Cout, int Cin,
-                            int fh, int fw, const WgradPlan& w, float* partial, hipStream_t s) {
+                            int fh, int fw, const WgradPlan& w, float* partial, float* bpart, hipStream_t s) {
     auto kern = wgrad_mfma_kernel<VEC, TT>;
     const size_t lds = wgrad_lds_bytes(TT);
     hipError_t e = allow_lds((const void*)kern, lds);
@@ -405,72 +425,42 @@ static hipError_t run_wgrad(const float* dy, const float* x, int E_h, int E_w, i
     const int64_t nblocks = (int64_t)w.otiles * w.itiles * fh * w.ntg * w.splits;
     if (nblocks >= (1ll << 31)) return hipErrorInvalidConfiguration;
     kern<<<dim3((unsigned)nblocks), 256, lds, s>>>(dy, x, E_h, E_w, U_h, U_w, Cout, Cin, fh, fw, (int)w.positions,
-                                                   (int)w.nchunks, w.otiles, w.itiles, w.ntg, w.splits, partial);
+                                                   (int)w.nchunks, w.otiles, w.itiles, w.ntg, w.splits, partial,
+                                                   bpart);
     return hipGetLastError();
 }
 
 template <bool VEC>
 static hipError_t dispatch_wgrad(const float* dy, const float* x, int E_h, int E_w, int U_h, int U_w, int Cout,
-                                 int Cin, int fh, int fw, const WgradPlan& w, float* partial, hipStream_t s) {
+                                 int Cin, int fh, int fw, const WgradPlan& w, float* partial, float* bpart,
+                                 hipStream_t s) {
     switch (w.tt) {
-        case 1: return run_wgrad<VEC, 1>(dy, x, E_h, E_w, U_h, U_w, Cout, Cin, fh, fw, w, partial, s);
-        case 2: return run_wgrad<VEC, 2>(dy, x, E_h, E_w, U_h, U_w, Cout, Cin, fh, fw, w, partial, s);
-        case 3: return run_wgrad<VEC, 3>(dy, x, E_h, E_w, U_h, U_w, Cout, Cin, fh, fw, w, partial, s);
-        case 4: return run_wgrad<VEC, 4>(dy, x, E_h, E_w, U_h, U_w, Cout, Cin, fh, fw, w, partial, s);
-        case 5: return run_wgrad<VEC, 5>(dy, x, E_h, E_w, U_h, U_w, Cout, Cin, fh, fw, w, partial, s);
-        case 6: return run_wgrad<VEC, 6>(dy, x, E_h, E_w, U_h, U_w, Cout, Cin, fh, fw, w, partial, s);
-        case 7: return run_wgrad<VEC, 7>(dy, x, E_h, E_w, U_h, U_w, Cout, Cin, fh, fw, w, partial, s);
-        case 8: return run_wgrad<VEC, 8>(dy, x, E_h, E_w, U_h, U_w, Cout, Cin, fh, fw, w, partial, s);
+        case 1: return run_wgrad<VEC, 1>(dy, x, E_h, E_w, U_h, U_w, Cout, Cin, fh, fw, w, partial, bpart, s);
+        case 2: return run_wgrad<VEC, 2>(dy, x, E_h, E_w, U_h, U_w, Cout, Cin, fh, fw, w, partial, bpart, s);
+        case 3: return run_wgrad<VEC, 3>(dy, x, E_h, E_w, U_h, U_w, Cout, Cin, fh, fw, w, partial, bpart, s);
+        case 4: return run_wgrad<VEC, 4>(dy, x, E_h, E_w, U_h, U_w, Cout, Cin, fh, fw, w, partial, bpart, s);
+        case 5: return run_wgrad<VEC, 5>(dy, x, E_h, E_w, U_h, U_w, Cout, Cin, fh, fw, w, partial, bpart, s);
+        case 6: return run_wgrad<VEC, 6>(dy, x, E_h, E_w, U_h, U_w, Cout, Cin, fh, fw, w, partial, bpart, s);
+        case 7: return run_wgrad<VEC, 7>(dy, x, E_h, E_w, U_h, U_w, Cout, Cin, fh, fw, w, partial, bpart, s);
+        case 8: return run_wgrad<VEC, 8>(dy, x, E_h, E_w, U_h, U_w, Cout, Cin, fh, fw, w, partial, bpart, s);
     }
     return hipErrorInvalidValue;
 }
 
 hipError_t launch_wgrad(const float* dy, const float* x, int F, int E_h, int E_w, int U_h, int U_w, int Cout, int Cin,
-                        int fh, int fw, const WgradPlan& w, float* partial, float* dw, hipStream_t s) {
+                        int fh, int fw, const WgradPlan& w, float* partial, float* dw, float* db, hipStream_t s) {
     (void)F;
     // positions and chunks are 32-bit in the kernel
     if (w.positions + w.tt + kKC >= (1ll << 31) || U_w != E_w + fw - 1 || U_h != E_h + fh - 1)
         return hipErrorInvalidConfiguration;
+    float* bpart = partial + w.partial_floats;
     const bool vec = Cout % 4 == 0 && Cin % 4 == 0;
-    hipError_t e = vec ? dispatch_wgrad<true>(dy, x, E_h, E_w, U_h, U_w, Cout, Cin, fh, fw, w, partial, s)
-                       : dispatch_wgrad<false>(dy, x, E_h, E_w, U_h, U_w, Cout, Cin, fh, fw, w, partial, s);
+    hipError_t e = vec ? dispatch_wgrad<true>(dy, x, E_h, E_w, U_h, U_w, Cout, Cin, fh, fw, w, partial, bpart, s)
+                       : dispatch_wgrad<false>(dy, x, E_h, E_w, U_h, U_w, Cout, Cin, fh, fw, w, partial, bpart, s);
     if (e != hipSuccess) return e;
-    const int64_t n = (int64_t)Cout * Cin * fh * fw;
-    wgrad_reduce_kernel<<<dim3((unsigned)ceil_div64(n, kBT)), kBT, 0, s>>>(partial, w.splits, fh * fw, Cout, Cin, dw);
-    return hipGetLastError();
-}
-
-// ------------------------------------------------------------------ bias gradient
-// Block b sums positions [b*P/nb, (b+1)*P/nb) for every channel (threads stride
-// over channels); the reduce sums the blocks in order.
-__global__ __launch_bounds__(kBT) void bias_partial_kernel(const float* __restrict__ dy, int64_t P, int C, int nb,
-                                                          float* __restrict__ part) {
-    const int b = blockIdx.x;
-    const int64_t p0 = P * b / nb, p1 = P * (b + 1) / nb;
-    for (int c = threadIdx.x; c < C; c += kBT) {
-        float s = 0.f;
-        for (int64_t p = p0; p < p1; ++p) s += dy[p * C + c];
-        part[(int64_t)b * C + c] = s;
-    }
-}
-
-__global__ __launch_bounds__(kBT) void bias_reduce_kernel(const float* __restrict__ part, int nb, int C,
-                                                         float* __restrict__ db) {
-    const int c = blockIdx.x * kBT + threadIdx.x;
-    if (c >= C) return;
-    float s = 0.f;
-    for (int b = 0; b < nb; ++b) s += part[(int64_t)b * C + c];
-    db[c] = s;
-}
-
-int bias_blocks(int64_t P) { return (int)std::max<int64_t>(1, std::min<int64_t>(2048, P / 256)); }
-
-hipError_t launch_bias_grad(const float* dy, int64_t P, int C, float* part, float* db, hipStream_t s) {
-    const int nb = bias_blocks(P);
-    bias_partial_kernel<<<dim3((unsigned)nb), kBT, 0, s>>>(dy, P, C, nb, part);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    bias_reduce_kernel<<<dim3((unsigned)ceil_div64(C, kBT)), kBT, 0, s>>>(part, nb, C, db);
+    const int64_t n = (int64_t)Cout * Cin * fh * fw + Cout;
+    wgrad_reduce_kernel<<<dim3((unsigned)ceil_div64(n, kBT)), kBT, 0, s>>>(partial, bpart, w.splits, fh * fw, Cout,
+                                                                           Cin, dw, db);
     return hipGetLastError();
 }
 

@@ -101,6 +101,7 @@ struct WgradPlan {
     int otiles = 0, itiles = 0, splits = 0;
     int64_t positions = 0;       // F * E_h * U_w: output rows read over the input width
     int64_t nchunks = 0, partial_floats = 0;
+    int64_t bias_partial_floats = 0;   // after the weight partial sums in the same buffer
 };
 
 struct LaunchRec {
@@ -166,9 +167,7 @@ hipError_t launch_pad_grad(const float* in, int F, int E_h, int E_w, int C, int 
                            hipStream_t s);
 WgradPlan wgrad_plan(int F, int E_h, int E_w, int Cout, int Cin, int fh, int fw);
 hipError_t launch_wgrad(const float* dy, const float* x, int F, int E_h, int E_w, int U_h, int U_w, int Cout, int Cin,
-                        int fh, int fw, const WgradPlan& w, float* partial, float* dw, hipStream_t s);
-int bias_blocks(int64_t P);
-hipError_t launch_bias_grad(const float* dy, int64_t P, int C, float* part, float* db, hipStream_t s);
+                        int fh, int fw, const WgradPlan& w, float* partial, float* dw, float* db, hipStream_t s);
 hipError_t launch_crop_to_planar(const float* in, int D_w, int C, int H, int W, float* out, hipStream_t s);
 
 // host-side weight packing for the MFMA kernels (conv_mfma.hip)
