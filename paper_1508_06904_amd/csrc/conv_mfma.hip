@@ -210,39 +210,44 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
         __syncthreads();                 // ... and every other wave's
     };
 
-    // -- prologue: chunk 0 halo and the first weight slice
-    stage_halo(0, halo0);
-    stage_w(0, wbuf0);
-    wait_staged();
-
-    int step = 0;
-    for (int cc = 0; cc < nchunks; ++cc) {
-        const char* halo = (cc & 1) ? halo1 : halo0;
-        for (int th = 0; th < fh; ++th) {
-            for (int tw = 0; tw < fw; ++tw, ++step) {
-                const bool has_next = step + 1 < steps;
-                const bool last_tap = (th == fh - 1) && (tw == fw - 1);
-                // stage the next weight slice (its buffer was last read in the
-                // previous step) and, with a double-buffered halo, the next chunk's
-                // halo; the copies run while the MFMAs below execute
-                if (has_next) {
-                    stage_w(step + 1, (step & 1) ? wbuf0 : wbuf1);
-                    if (last_tap && dbl_halo) stage_halo(cc + 1, (cc & 1) ? halo0 : halo1);
-                }
-                const int tap_off = (th * tap_row + tw) * kPitchBytes;
-                const char* wcur = (step & 1) ? wbuf1 : wbuf0;
-                u32x4 a[MT][2], b[NT][2];
+    if constexpr (BF16) {
+        // Operand B comes straight from the packed weights in global memory
+        // (every workgroup of the N block reads the same slices, which stay in
+        // L2) into registers, one step ahead: no LDS slice and no barrier per
+        // step, only one per chunk for the halo.  Lane (n, half) of MFMA s holds
+        // bytes 32 half + 16 s of row n of a slice, as the halo reads of A do.
+        const char* w_lane = w_nb + (size_t)(wn * 32 * NT + l32) * kChunkBytes + half * 32;
+        auto load_b = [&](int st, u32x4 (&bb)[NT][2]) {
+            const char* src = w_lane + (size_t)st * (Cfg::BN * kChunkBytes);
 #pragma unroll
-                for (int mt = 0; mt < MT; ++mt) {
-                    a[mt][0] = *reinterpret_cast<const u32x4*>(halo + a_off[mt] + tap_off);
-                    a[mt][1] = *reinterpret_cast<const u32x4*>(halo + a_off[mt] + tap_off + 16);
-                }
+            for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
-                for (int nt = 0; nt < NT; ++nt) {
-                    b[nt][0] = *reinterpret_cast<const u32x4*>(wcur + b_off[nt]);
-                    b[nt][1] = *reinterpret_cast<const u32x4*>(wcur + b_off[nt] + 16);
-                }
-                if constexpr (BF16) {
+                for (int s = 0; s < 2; ++s)
+                    bb[nt][s] = *reinterpret_cast<const u32x4*>(src + nt * 32 * kChunkBytes + s * 16);
+        };
+        u32x4 bq[NT][2];
+        load_b(0, bq);
+        stage_halo(0, halo0);
+        wait_staged();
+        int step = 0;
+        for (int cc = 0; cc < nchunks; ++cc) {
+            const char* halo = (cc & 1) ? halo1 : halo0;
+            const bool next_chunk = cc + 1 < nchunks;
+            // the next chunk's halo goes to the other buffer (last read by chunk
+            // cc - 1, which ended with a barrier) while this chunk's taps run
+            if (dbl_halo && next_chunk) stage_halo(cc + 1, (cc & 1) ? halo0 : halo1);
+            for (int th = 0; th < fh; ++th) {
+                for (int tw = 0; tw < fw; ++tw, ++step) {
+                    const bool has_next = step + 1 < steps;
+                    u32x4 bnext[NT][2];
+                    if (has_next) load_b(step + 1, bnext);
+                    const int tap_off = (th * tap_row + tw) * kPitchBytes;
+                    u32x4 a[MT][2];
+#pragma unroll
+                    for (int mt = 0; mt < MT; ++mt) {
+                        a[mt][0] = *reinterpret_cast<const u32x4*>(halo + a_off[mt] + tap_off);
+                        a[mt][1] = *reinterpret_cast<const u32x4*>(halo + a_off[mt] + tap_off + 16);
+                    }
 #pragma unroll
                     for (int s = 0; s < 2; ++s)
 #pragma unroll
@@ -250,27 +255,87 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
 #pragma unroll
                             for (int nt = 0; nt < NT; ++nt)
                                 acc[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                                    as_bf16x8(a[mt][s]), as_bf16x8(b[nt][s]), acc[mt][nt], 0, 0, 0);
-                } else {
+                                    as_bf16x8(a[mt][s]), as_bf16x8(bq[nt][s]), acc[mt][nt], 0, 0, 0);
+                    if (has_next) {
 #pragma unroll
-                    for (int s = 0; s < 8; ++s) {
-#pragma unroll
-                        for (int mt = 0; mt < MT; ++mt) {
-                            const uint32_t aw = a[mt][s >> 2][s & 3];
-#pragma unroll
-                            for (int nt = 0; nt < NT; ++nt) {
-                                const uint32_t bw = b[nt][s >> 2][s & 3];
-                                acc[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(aw), __uint_as_float(bw),
-                                                                                  acc[mt][nt], 0, 0, 0);
-                            }
+                        for (int nt = 0; nt < NT; ++nt) {
+                            bq[nt][0] = bnext[nt][0];
+                            bq[nt][1] = bnext[nt][1];
                         }
                     }
                 }
-                if (has_next && last_tap && !dbl_halo) {
-                    __syncthreads();                   // every wave is done with this chunk's halo
+            }
+            if (next_chunk) {
+                if (!dbl_halo) {
+                    __syncthreads();           // every wave is done with this chunk's halo
                     stage_halo(cc + 1, halo0);
                 }
-                wait_staged();
+                wait_staged();                 // the next chunk's halo has landed for every wave
+            }
+        }
+    } else {
+        // -- prologue: chunk 0 halo and the first weight slice
+        stage_halo(0, halo0);
+        stage_w(0, wbuf0);
+        wait_staged();
+
+        int step = 0;
+        for (int cc = 0; cc < nchunks; ++cc) {
+            const char* halo = (cc & 1) ? halo1 : halo0;
+            for (int th = 0; th < fh; ++th) {
+                for (int tw = 0; tw < fw; ++tw, ++step) {
+                    const bool has_next = step + 1 < steps;
+                    const bool last_tap = (th == fh - 1) && (tw == fw - 1);
+                    // stage the next weight slice (its buffer was last read in the
+                    // previous step) and, with a double-buffered halo, the next chunk's
+                    // halo; the copies run while the MFMAs below execute
+                    if (has_next) {
+                        stage_w(step + 1, (step & 1) ? wbuf0 : wbuf1);
+                        if (last_tap && dbl_halo) stage_halo(cc + 1, (cc & 1) ? halo0 : halo1);
+                    }
+                    const int tap_off = (th * tap_row + tw) * kPitchBytes;
+                    const char* wcur = (step & 1) ? wbuf1 : wbuf0;
+                    u32x4 a[MT][2], b[NT][2];
+    #pragma unroll
+                    for (int mt = 0; mt < MT; ++mt) {
+                        a[mt][0] = *reinterpret_cast<const u32x4*>(halo + a_off[mt] + tap_off);
+                        a[mt][1] = *reinterpret_cast<const u32x4*>(halo + a_off[mt] + tap_off + 16);
+                    }
+    #pragma unroll
+                    for (int nt = 0; nt < NT; ++nt) {
+                        b[nt][0] = *reinterpret_cast<const u32x4*>(wcur + b_off[nt]);
+                        b[nt][1] = *reinterpret_cast<const u32x4*>(wcur + b_off[nt] + 16);
+                    }
+                    if constexpr (BF16) {
+    #pragma unroll
+                        for (int s = 0; s < 2; ++s)
+    #pragma unroll
+                            for (int mt = 0; mt < MT; ++mt)
+    #pragma unroll
+                                for (int nt = 0; nt < NT; ++nt)
+                                    acc[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                                        as_bf16x8(a[mt][s]), as_bf16x8(b[nt][s]), acc[mt][nt], 0, 0, 0);
+                    } else {
+    #pragma unroll
+                        for (int s = 0; s < 8; ++s) {
+    #pragma unroll
+                            for (int mt = 0; mt < MT; ++mt) {
+                                const uint32_t aw = a[mt][s >> 2][s & 3];
+    #pragma unroll
+                                for (int nt = 0; nt < NT; ++nt) {
+                                    const uint32_t bw = b[nt][s >> 2][s & 3];
+                                    acc[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(aw), __uint_as_float(bw),
+                                                                                      acc[mt][nt], 0, 0, 0);
+                                }
+                            }
+                        }
+                    }
+                    if (has_next && last_tap && !dbl_halo) {
+                        __syncthreads();                   // every wave is done with this chunk's halo
+                        stage_halo(cc + 1, halo0);
+                    }
+                    wait_staged();
+                }
             }
         }
     }
@@ -374,18 +439,21 @@ static size_t device_lds_limit() {
     return (size_t)cached;
 }
 
+// LDS bytes of the double-buffered weight slices: binary32 stages them in LDS,
+// bfloat16 reads its operands straight into registers.
+static size_t weight_lds_bytes(bool bf16, int BN) { return bf16 ? 0 : 2 * (size_t)BN * kPitchBytes; }
+
 // Spatial tile TH x TW = BM output samples: the shape that wastes the fewest
 // masked samples on this layer's fragment extent; among those, one whose halo can
 // be double-buffered within the LDS budget of two workgroups per CU, then the
 // smallest halo.
-static Tile pick_tile(int BM, int BN, int Hout, int Wout, int fh, int fw, size_t lds_max) {
+static Tile pick_tile(int BM, size_t wb, int Hout, int Wout, int fh, int fw, size_t lds_max) {
     Tile best{0, 0, 0, 0};
     int64_t best_work = -1, best_halo = -1;
     for (int TW = 8; TW <= BM; TW *= 2) {
         const int TH = BM / TW;
         const int64_t halo_px = (int64_t)(TH + fh - 1) * (TW + fw - 1);
         const size_t halo_b = (size_t)((halo_px * kPitchBytes + 127) / 128) * 128;
-        const size_t wb = 2 * (size_t)BN * kPitchBytes;
         const size_t cap = std::min(lds_max, (size_t)kMaxLds);
         int dbl;
         size_t lds;
@@ -407,8 +475,8 @@ static Tile pick_tile(int BM, int BN, int Hout, int Wout, int fh, int fw, size_t
 // Whether some spatial tile of the variant chosen for `cout` fits an fh x fw
 // filter's halo into LDS (checked against the 64 KB every device offers).
 bool mfma_supports(bool bf16, int cout, int fh, int fw) {
-    const int bn = bf16 ? mfma_bf16_pick_bn(cout) : mfma_f32_pick_bn(cout);
-    return pick_tile(256, bn, 1, 1, fh, fw, 64 * 1024).TH > 0 && pick_tile(256, bn, 64, 64, fh, fw, 64 * 1024).TH > 0;
+    const size_t wb = weight_lds_bytes(bf16, bf16 ? mfma_bf16_pick_bn(cout) : mfma_f32_pick_bn(cout));
+    return pick_tile(256, wb, 1, 1, fh, fw, 64 * 1024).TH > 0 && pick_tile(256, wb, 64, 64, fh, fw, 64 * 1024).TH > 0;
 }
 
 // Dynamic LDS above 64 KB needs a per-kernel opt-in (once per instantiation).
@@ -427,10 +495,9 @@ static hipError_t allow_large_lds(const void* kern, size_t lds) {
 // Flat-mode tile (TH = 1, TW = BM consecutive positions of the flattened
 // fragment batch) for fragments of Hin x Win input samples, or TH = 0 if its
 // single-row halo does not fit.
-static Tile flat_tile(int BM, int BN, int Win, int fh, int fw, size_t lds_max) {
+static Tile flat_tile(int BM, size_t wb, int Win, int fh, int fw, size_t lds_max) {
     const int64_t halo_px = BM + (int64_t)(fh - 1) * Win + fw - 1;
     const size_t halo_b = (size_t)((halo_px * kPitchBytes + 127) / 128) * 128;
-    const size_t wb = 2 * (size_t)BN * kPitchBytes;
     const size_t cap = std::min(lds_max, (size_t)kMaxLds);
     if (2 * halo_b + wb <= cap) return Tile{1, BM, 2 * halo_b + wb, 1};
     if (halo_b + wb <= cap) return Tile{1, BM, halo_b + wb, 0};
@@ -449,14 +516,14 @@ struct LaunchShape {
     int64_t nblocks;    // 0 if no tile fits
 };
 
-static LaunchShape launch_shape(int BM, int BN, int F, int Hin, int Win, int dil_h, int dil_w, int fh, int fw,
+static LaunchShape launch_shape(int BM, size_t wb, int F, int Hin, int Win, int dil_h, int dil_w, int fh, int fw,
                                 int nbs) {
     LaunchShape L{Tile{0, 0, 0, 0}, 0, 0, 0, 0};
     const size_t lds = device_lds_limit();
     if (dil_h * dil_w > 1) {
         const int Hout = Hin - dil_h * (fh - 1), Wout = Win - dil_w * (fw - 1);
         const int Hp = (int)ceil_div64(Hout, dil_h), Wp = (int)ceil_div64(Wout, dil_w);
-        L.t = pick_tile(BM, BN, Hp, Wp, fh, fw, lds);
+        L.t = pick_tile(BM, wb, Hp, Wp, fh, fw, lds);
         if (L.t.TH == 0) return L;
         L.tilesY = (int)ceil_div64(Hp, L.t.TH);
         L.tilesX = (int)ceil_div64(Wp, L.t.TW);
@@ -464,10 +531,10 @@ static LaunchShape launch_shape(int BM, int BN, int F, int Hin, int Win, int dil
         return L;
     }
     const int Hout = Hin - fh + 1, Wout = Win - fw + 1;
-    L.t = pick_tile(BM, BN, Hout, Wout, fh, fw, lds);
+    L.t = pick_tile(BM, wb, Hout, Wout, fh, fw, lds);
     const int64_t flat_len = (int64_t)F * Hin * Win;
     if (flat_len < (1ll << 30)) {
-        const Tile ft = flat_tile(BM, BN, Win, fh, fw, lds);
+        const Tile ft = flat_tile(BM, wb, Win, fh, fw, lds);
         const int64_t work_tiles =
             L.t.TH ? (int64_t)F * ceil_div64(Hout, L.t.TH) * L.t.TH * ceil_div64(Wout, L.t.TW) * L.t.TW : -1;
         const int64_t work_flat = ceil_div64(flat_len, BM) * BM;
@@ -498,10 +565,13 @@ static LaunchShape launch_shape(int BM, int BN, int F, int Hin, int Win, int dil
 // the 64-channel tile is taken.
 PlanConv mfma_launch_variant(const PlanConv& pc, int F, int Hin, int Win, int dil_h, int dil_w) {
     if (!pc.w_alt || pc.impl == CONV_DIRECT) return pc;
-    const LaunchShape a = launch_shape(256, pc.bn, F, Hin, Win, dil_h, dil_w, pc.fh, pc.fw, pc.cout_pad / pc.bn);
+    const bool bf16 = pc.impl == CONV_MFMA_BF16;
+    const LaunchShape a = launch_shape(256, weight_lds_bytes(bf16, pc.bn), F, Hin, Win, dil_h, dil_w, pc.fh, pc.fw,
+                                       pc.cout_pad / pc.bn);
     if (a.nblocks == 0 || a.nblocks >= 512) return pc;
     const LaunchShape b =
-        launch_shape(256, pc.bn_alt, F, Hin, Win, dil_h, dil_w, pc.fh, pc.fw, pc.cout_pad_alt / pc.bn_alt);
+        launch_shape(256, weight_lds_bytes(bf16, pc.bn_alt), F, Hin, Win, dil_h, dil_w, pc.fh, pc.fw,
+                     pc.cout_pad_alt / pc.bn_alt);
     if (b.nblocks == 0) return pc;
     if (a.nblocks > 256 && 11 * ceil_div64(b.nblocks, 256) >= 20 * ceil_div64(a.nblocks, 256)) return pc;
     PlanConv alt = pc;
@@ -518,7 +588,8 @@ static hipError_t run_mfma(const void* in, int F, int Hin, int Win, int dil_h, i
     const bool dilated = dil_h * dil_w > 1;
     if (dilated && F != 1) return hipErrorInvalidValue;   // dilated: one signal, tiled per phase
     const int nbs = pc.cout_pad / Cfg::BN;
-    const LaunchShape L = launch_shape(Cfg::BM, Cfg::BN, F, Hin, Win, dil_h, dil_w, pc.fh, pc.fw, nbs);
+    const LaunchShape L =
+        launch_shape(Cfg::BM, weight_lds_bytes(BF16, Cfg::BN), F, Hin, Win, dil_h, dil_w, pc.fh, pc.fw, nbs);
     if (L.nblocks == 0) return hipErrorInvalidConfiguration;
     if (L.nblocks >= (1ll << 31)) return hipErrorInvalidConfiguration;
     auto kern = conv_mfma_kernel<BF16, Tout, WGM, WGN, MT, NT>;
