@@ -344,12 +344,63 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
     const int n_base = nb * Cfg::BN + wn * 32 * NT;
     const size_t f_off = (size_t)f * Hout * Wout;
     const int frag_px = flat_h * flat_w;
+    // output sample of tile position m: whether it exists, and its index
+    auto out_pos = [&](int m, size_t& o) -> bool {
+        if (flat_w) {
+            const int p = tx0 + m;                 // TH = 1: position in the flat sequence (Win long)
+            const int fr = p / frag_px, r = p - fr * frag_px;
+            const int y = r / flat_w, x = r - y * flat_w;
+            o = ((size_t)fr * Hout + y) * Wout + x;
+            return p < Win && y < Hout && x < Wout;
+        }
+        if (dilated) {
+            const int y = py + dil_h * (ty0 + m / TW), x = px + dil_w * (tx0 + m % TW);
+            o = (size_t)y * Wout + x;
+            return y < Hout && x < Wout;
+        }
+        const int y = ty0 + m / TW, x = tx0 + m % TW;
+        o = f_off + (size_t)y * Wout + x;
+        return y < Hout && x < Wout;
+    };
     int ncol[NT];
     float bn[NT];
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
         ncol[nt] = n_base + nt * 32 + l32;
         bn[nt] = ncol[nt] < Cout ? bias[ncol[nt]] : 0.f;
+    }
+    if constexpr (sizeof(Tout) == 2) {
+        // bfloat16 output: each lane holds one channel of 16 positions, so direct
+        // stores would be 2-byte stores, one instruction per value.  Transpose
+        // through LDS (the halo buffers are free now) into 16-byte units of 8
+        // channels of one position: 8x fewer store instructions.
+        if (Cout % 8 == 0 && ((uintptr_t)out & 15) == 0) {
+            constexpr int WCOLS = 32 * NT;                          // channels of a wave's block
+            uint16_t* st = reinterpret_cast<uint16_t*>(lds) + wave * (32 * WCOLS);
+            __syncthreads();                                        // every wave is done with the halo
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) {
+#pragma unroll
+                for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+                    for (int v = 0; v < 16; ++v) {
+                        const int i = (v >> 2) * 8 + half * 4 + (v & 3);
+                        st[i * WCOLS + nt * 32 + l32] = f32_to_bf16(activate(act, acc[mt][nt][v] + bn[nt]));
+                    }
+                __syncthreads();
+#pragma unroll
+                for (int r = 0; r < WCOLS / 16; ++r) {               // 32 rows x WCOLS / 8 units, 64 per round
+                    const int u = r * 64 + lane;
+                    const int row = u / (WCOLS / 8), c8 = (u % (WCOLS / 8)) * 8;
+                    size_t o;
+                    if (out_pos(wm * 32 * MT + mt * 32 + row, o) && n_base + c8 < Cout)
+                        *reinterpret_cast<u32x4*>(out + o * Cout + n_base + c8) =
+                            *reinterpret_cast<const u32x4*>(st + row * WCOLS + c8);
+                }
+                __syncthreads();                                    // before the next block overwrites st
+            }
+            return;
+        }
     }
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
@@ -360,7 +411,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
             size_t o;
             bool ok;
             if (flat_w) {
-                const int p = tx0 + m;                 // TH = 1: position in the flat sequence (Win long)
+                const int p = tx0 + m;
                 const int fr = p / frag_px, r = p - fr * frag_px;
                 const int y = r / flat_w, x = r - y * flat_w;
                 ok = p < Win && y < Hout && x < Wout;
