@@ -497,8 +497,13 @@ static size_t weight_lds_bytes(bool bf16, int BN) { return bf16 ? 0 : 2 * (size_
 // Spatial tile TH x TW = BM output samples: the shape that wastes the fewest
 // masked samples on this layer's fragment extent; among those, one whose halo can
 // be double-buffered within the LDS budget of two workgroups per CU, then the
-// smallest halo.
-static Tile pick_tile(int BM, size_t wb, int Hout, int Wout, int fh, int fw, size_t lds_max) {
+// smallest halo.  With TW = 8 a 16-lane group of an A read spans two halo rows,
+// whose samples share LDS banks unless the halo row is 8 mod 16 samples long;
+// the bfloat16 kernel, whose steps are short enough for that to show, counts
+// such a tile's work 3 % higher (measured: 8 x 32 -> 16 x 16 tiles make the 3x3
+// layers of the 4K frame 18 % faster, while 16 x 16 tiles with 3.4 % more
+// masked work make its 6x6 layer 4.7 % slower).
+static Tile pick_tile(int BM, size_t wb, int Hout, int Wout, int fh, int fw, size_t lds_max, bool bf16) {
     Tile best{0, 0, 0, 0};
     int64_t best_work = -1, best_halo = -1;
     for (int TW = 8; TW <= BM; TW *= 2) {
@@ -511,7 +516,8 @@ static Tile pick_tile(int BM, size_t wb, int Hout, int Wout, int fh, int fw, siz
         if (2 * halo_b + wb <= cap) { dbl = 1; lds = 2 * halo_b + wb; }
         else if (halo_b + wb <= cap) { dbl = 0; lds = halo_b + wb; }
         else continue;
-        const int64_t work = ceil_div64(Hout, TH) * TH * ceil_div64(Wout, TW) * TW;
+        int64_t work = ceil_div64(Hout, TH) * TH * ceil_div64(Wout, TW) * TW;
+        if (bf16 && TW < 16 && (TW + fw - 1) % 16 != 8) work += work / 32;
         const bool better = best_work < 0 || work < best_work ||
                             (work == best_work && (dbl > best.dbl || (dbl == best.dbl && halo_px < best_halo)));
         if (better) {
@@ -527,7 +533,8 @@ static Tile pick_tile(int BM, size_t wb, int Hout, int Wout, int fh, int fw, siz
 // filter's halo into LDS (checked against the 64 KB every device offers).
 bool mfma_supports(bool bf16, int cout, int fh, int fw) {
     const size_t wb = weight_lds_bytes(bf16, bf16 ? mfma_bf16_pick_bn(cout) : mfma_f32_pick_bn(cout));
-    return pick_tile(256, wb, 1, 1, fh, fw, 64 * 1024).TH > 0 && pick_tile(256, wb, 64, 64, fh, fw, 64 * 1024).TH > 0;
+    return pick_tile(256, wb, 1, 1, fh, fw, 64 * 1024, bf16).TH > 0 &&
+           pick_tile(256, wb, 64, 64, fh, fw, 64 * 1024, bf16).TH > 0;
 }
 
 // Dynamic LDS above 64 KB needs a per-kernel opt-in (once per instantiation).
@@ -567,14 +574,14 @@ struct LaunchShape {
     int64_t nblocks;    // 0 if no tile fits
 };
 
-static LaunchShape launch_shape(int BM, size_t wb, int F, int Hin, int Win, int dil_h, int dil_w, int fh, int fw,
+static LaunchShape launch_shape(int BM, bool bf16, size_t wb, int F, int Hin, int Win, int dil_h, int dil_w, int fh, int fw,
                                 int nbs) {
     LaunchShape L{Tile{0, 0, 0, 0}, 0, 0, 0, 0};
     const size_t lds = device_lds_limit();
     if (dil_h * dil_w > 1) {
         const int Hout = Hin - dil_h * (fh - 1), Wout = Win - dil_w * (fw - 1);
         const int Hp = (int)ceil_div64(Hout, dil_h), Wp = (int)ceil_div64(Wout, dil_w);
-        L.t = pick_tile(BM, wb, Hp, Wp, fh, fw, lds);
+        L.t = pick_tile(BM, wb, Hp, Wp, fh, fw, lds, bf16);
         if (L.t.TH == 0) return L;
         L.tilesY = (int)ceil_div64(Hp, L.t.TH);
         L.tilesX = (int)ceil_div64(Wp, L.t.TW);
@@ -582,7 +589,7 @@ static LaunchShape launch_shape(int BM, size_t wb, int F, int Hin, int Win, int 
         return L;
     }
     const int Hout = Hin - fh + 1, Wout = Win - fw + 1;
-    L.t = pick_tile(BM, wb, Hout, Wout, fh, fw, lds);
+    L.t = pick_tile(BM, wb, Hout, Wout, fh, fw, lds, bf16);
     const int64_t flat_len = (int64_t)F * Hin * Win;
     if (flat_len < (1ll << 30)) {
         const Tile ft = flat_tile(BM, wb, Win, fh, fw, lds);
@@ -617,11 +624,11 @@ static LaunchShape launch_shape(int BM, size_t wb, int F, int Hin, int Win, int 
 PlanConv mfma_launch_variant(const PlanConv& pc, int F, int Hin, int Win, int dil_h, int dil_w) {
     if (!pc.w_alt || pc.impl == CONV_DIRECT) return pc;
     const bool bf16 = pc.impl == CONV_MFMA_BF16;
-    const LaunchShape a = launch_shape(256, weight_lds_bytes(bf16, pc.bn), F, Hin, Win, dil_h, dil_w, pc.fh, pc.fw,
+    const LaunchShape a = launch_shape(256, bf16, weight_lds_bytes(bf16, pc.bn), F, Hin, Win, dil_h, dil_w, pc.fh, pc.fw,
                                        pc.cout_pad / pc.bn);
     if (a.nblocks == 0 || a.nblocks >= 512) return pc;
     const LaunchShape b =
-        launch_shape(256, weight_lds_bytes(bf16, pc.bn_alt), F, Hin, Win, dil_h, dil_w, pc.fh, pc.fw,
+        launch_shape(256, bf16, weight_lds_bytes(bf16, pc.bn_alt), F, Hin, Win, dil_h, dil_w, pc.fh, pc.fw,
                      pc.cout_pad_alt / pc.bn_alt);
     if (b.nblocks == 0) return pc;
     if (a.nblocks > 256 && 11 * ceil_div64(b.nblocks, 256) >= 20 * ceil_div64(a.nblocks, 256)) return pc;
@@ -640,7 +647,7 @@ static hipError_t run_mfma(const void* in, int F, int Hin, int Win, int dil_h, i
     if (dilated && F != 1) return hipErrorInvalidValue;   // dilated: one signal, tiled per phase
     const int nbs = pc.cout_pad / Cfg::BN;
     const LaunchShape L =
-        launch_shape(Cfg::BM, weight_lds_bytes(BF16, Cfg::BN), F, Hin, Win, dil_h, dil_w, pc.fh, pc.fw, nbs);
+        launch_shape(Cfg::BM, BF16, weight_lds_bytes(BF16, Cfg::BN), F, Hin, Win, dil_h, dil_w, pc.fh, pc.fw, nbs);
     if (L.nblocks == 0) return hipErrorInvalidConfiguration;
     if (L.nblocks >= (1ll << 31)) return hipErrorInvalidConfiguration;
     auto kern = conv_mfma_kernel<BF16, Tout, WGM, WGN, MT, NT>;
