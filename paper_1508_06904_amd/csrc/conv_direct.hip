@@ -48,12 +48,27 @@ __global__ __launch_bounds__(256) void conv_direct_kernel(const Tin* __restrict_
         }
     }
     Tout* op = out + p * Cout + og;
+    const bool aligned16 = ((uintptr_t)out & 15) == 0;
     if constexpr (sizeof(Tout) == 4 && COB % 4 == 0) {
-        if (Cout % 4 == 0 && og + COB <= Cout) {   // 16-byte aligned: full vectors
+        if (aligned16 && Cout % 4 == 0 && og + COB <= Cout) {   // 16-byte aligned: full vectors
 #pragma unroll
             for (int o = 0; o < COB; o += 4)
                 *reinterpret_cast<float4*>(op + o) = make_float4(activate(act, acc[o]), activate(act, acc[o + 1]),
                                                                  activate(act, acc[o + 2]), activate(act, acc[o + 3]));
+            return;
+        }
+    }
+    if constexpr (sizeof(Tout) == 2 && COB % 8 == 0) {
+        if (aligned16 && Cout % 8 == 0 && og + COB <= Cout) {   // 8 bfloat16 channels per 16-byte store
+#pragma unroll
+            for (int o = 0; o < COB; o += 8) {
+                uint32_t w[4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    w[e] = (uint32_t)f32_to_bf16(activate(act, acc[o + 2 * e])) |
+                           ((uint32_t)f32_to_bf16(activate(act, acc[o + 2 * e + 1])) << 16);
+                *reinterpret_cast<uint4*>(op + o) = make_uint4(w[0], w[1], w[2], w[3]);
+            }
             return;
         }
     }
