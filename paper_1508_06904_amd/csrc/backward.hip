@@ -195,6 +195,7 @@ constexpr int kKC = 32;               // positions per chunk
 constexpr int kWP = kWT + 32;         // LDS row pitch in floats: the two half-waves of a read
                                       // (rows p and p + 1) hit disjoint banks
 constexpr int kMaxTT = 8;             // taps of one filter row per workgroup
+constexpr int kMaxPackedTT = 4;       // MFMA tiles per wave in the packed (narrow-layer) mode
 
 static size_t wgrad_lds_bytes(int tt) { return 2 * (size_t)(kKC + kKC + tt - 1) * kWP * sizeof(float); }
 
@@ -212,13 +213,19 @@ static size_t wgrad_lds_bytes(int tt) { return 2 * (size_t)(kKC + kKC + tt - 1) 
 // of its 32 positions and the x rows of 32 + TT - 1 positions once, and every tap
 // of the group reads its operand rows t_w further on in LDS -- TT times fewer
 // global reads than one workgroup per tap.
-template <bool VEC, int TT>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void wgrad_mfma_kernel(const float* __restrict__ dy, const float* __restrict__ x,
-                                                        int E_h, int E_w, int U_h, int U_w, int Cout, int Cin, int fh,
-                                                        int fw, int Q, int nchunks, int otiles, int itiles, int ntg,
-                                                        int splits, float* __restrict__ partial,
-                                                        float* __restrict__ bias_partial) {
-    constexpr int RB = kKC + TT - 1;              // staged x rows per chunk
+//
+// PACKED (layers with at most 32 input channels): the 64 columns of an MFMA
+// tile hold g = 64 / cpt taps of cpt channels each (cpt: Cin rounded up to a
+// power of two, at least 4), column j being tap j / cpt and channel j % cpt, so
+// a narrow layer does not spend 64-column tiles on a few channels.  Tile t of a
+// workgroup covers taps t g .. t g + g - 1 of its group; the staged x rows are
+// cpt floats apart and column j of tap row q reads row q + j / cpt.
+template <bool VEC, int TT, bool PACKED>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void wgrad_mfma_kernel(
+    const float* __restrict__ dy, const float* __restrict__ x, int E_h, int E_w, int U_h, int U_w, int Cout, int Cin,
+    int fh, int fw, int Q, int nchunks, int otiles, int itiles, int ntg, int splits, int cpt,
+    float* __restrict__ partial, float* __restrict__ bias_partial) {
+    constexpr int RB = kKC + TT - 1;              // staged x rows per chunk (unpacked; bounds the buffer)
     extern __shared__ __attribute__((aligned(16))) float wl[];
     auto lds_a = [&](int buf) { return wl + buf * (kKC * kWP); };                  // dy rows
     auto lds_b = [&](int buf) { return wl + 2 * kKC * kWP + buf * (RB * kWP); };   // x rows
@@ -238,8 +245,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void w
     bid /= ntg;
     const int th = bid % fh;
     const int split = bid / fh;
-    const int tw0 = tg * TT;
-    const int ntt = min(TT, fw - tw0);            // taps of this group
+    const int g = PACKED ? kWT / cpt : 1;         // taps per MFMA tile
+    const int span = TT * g;                      // taps per group
+    const int tw0 = tg * span;
+    const int ntt = min(span, fw - tw0);          // taps of this group
+    const int rows_b = kKC + span - 1;            // staged x rows per chunk
     const int c0 = (int)((int64_t)nchunks * split / splits), c1 = (int)((int64_t)nchunks * (split + 1) / splits);
     const int o0 = ot * kWT, i0 = it * kWT;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -273,11 +283,19 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void w
         }
 #pragma unroll
         for (int k = 0; k < 3; ++k) {
-            const int row = s_row + 16 * k;
+            int row, col;
+            if constexpr (PACKED) {                 // rows of cpt floats, cpt / 4 units each
+                const int u = tid + 256 * k;
+                row = u / (cpt / 4);
+                col = (u - row * (cpt / 4)) * 4;
+            } else {
+                row = s_row + 16 * k;
+                col = i0 + s_col;
+            }
             const int q = qc + tw0 + row;
             const int f = q / rowlen;
             const int64_t src = (int64_t)q + (int64_t)f * (fh - 1) * U_w + (int64_t)th * U_w;
-            rb[k] = row < RB ? load4(x + src * Cin, i0 + s_col, Cin, q < Q) : make_float4(0.f, 0.f, 0.f, 0.f);
+            rb[k] = row < rows_b ? load4(x + src * Cin, col, Cin, q < Q) : make_float4(0.f, 0.f, 0.f, 0.f);
         }
     };
     auto store_chunk = [&](int buf) {
@@ -285,8 +303,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void w
         for (int k = 0; k < 2; ++k)
             *reinterpret_cast<float4*>(lds_a(buf) + (s_row + 16 * k) * kWP + s_col) = ra[k];
 #pragma unroll
-        for (int k = 0; k < 3; ++k)
-            if (s_row + 16 * k < RB) *reinterpret_cast<float4*>(lds_b(buf) + (s_row + 16 * k) * kWP + s_col) = rb[k];
+        for (int k = 0; k < 3; ++k) {
+            if constexpr (PACKED) {
+                const int u = tid + 256 * k;
+                if (u < rows_b * (cpt / 4)) *reinterpret_cast<float4*>(lds_b(buf) + u * 4) = rb[k];
+            } else {
+                if (s_row + 16 * k < RB) *reinterpret_cast<float4*>(lds_b(buf) + (s_row + 16 * k) * kWP + s_col) = rb[k];
+            }
+        }
     };
 
     if (c0 < c1) {
@@ -299,7 +323,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void w
         const bool more = c + 1 < c1;
         if (more) load_chunk(c + 1);
         const float* A = lds_a(buf) + wm * 32 + l32;
-        const float* Bm = lds_b(buf) + wn * 32 + l32;
+        const float* Bm = lds_b(buf) + wn * 32 + l32;   // packed: column j = wn 32 + l32 of row 0
+        const int bstep = PACKED ? cpt : kWP;           // floats between staged rows
         // all TT taps even in a ragged last group (the extra ones are not stored):
         // a tap-dependent branch here would keep a second copy of the accumulators
 #pragma unroll 4
@@ -309,7 +334,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void w
             bsum += av;
             float bv[TT];
 #pragma unroll
-            for (int t = 0; t < TT; ++t) bv[t] = Bm[(p + t) * kWP];
+            for (int t = 0; t < TT; ++t) bv[t] = PACKED ? Bm[(p + t * g) * bstep] : Bm[(p + t) * kWP];
 #pragma unroll
             for (int t = 0; t < TT; ++t) acc[t] = __builtin_amdgcn_mfma_f32_32x32x2f32(av, bv[t], acc[t], 0, 0, 0);
         }
@@ -325,11 +350,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void w
 
     // D[i][j] of a 32x32 tile sits in lane j + 32*((i/4)%2), register (i/8)*4 + i%4
     const int taps = fh * fw;
-    const int ii = i0 + wn * 32 + l32;
+    const int jj = wn * 32 + l32;
+    const int ii = PACKED ? jj % cpt : i0 + jj;     // input channel of this lane's column
+    const int tl = PACKED ? jj / cpt : 0;           // tap of this lane's column within a tile
 #pragma unroll
     for (int t = 0; t < TT; ++t) {
-        if (t >= ntt) break;
-        float* dst = partial + ((size_t)split * taps + th * fw + tw0 + t) * Cout * Cin;
+        const int k = t * g + tl;                   // tap within the group
+        if (k >= ntt) continue;
+        float* dst = partial + ((size_t)split * taps + th * fw + tw0 + k) * Cout * Cin;
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
             const int o = o0 + wm * 32 + (v >> 2) * 8 + half * 4 + (v & 3);
@@ -377,26 +405,46 @@ static hipError_t allow_lds(const void* kern, size_t lds) {
 
 WgradPlan wgrad_plan(int F, int E_h, int E_w, int Cout, int Cin, int fh, int fw) {
     WgradPlan w;
-    // the largest group of taps (at most kMaxTT) whose ragged last group wastes at
-    // most a tenth of the row's MFMA work
-    for (int tt = std::min(fw, kMaxTT); tt >= 1; --tt) {
-        const int ntg = (fw + tt - 1) / tt;
-        if (10 * (ntg * tt - fw) <= fw) {
-            w.tt = tt;
-            w.ntg = ntg;
-            break;
+    if (Cin <= kWT / 2) {
+        // packed: cpt columns per tap, g taps per tile; at most kMaxPackedTT tiles,
+        // the fewest MFMA tiles per row (ntg * tt), then the most taps per group
+        w.packed = true;
+        w.cpt = 4;
+        while (w.cpt < Cin) w.cpt *= 2;
+        const int g = kWT / w.cpt;
+        int best_work = -1;
+        for (int tt = kMaxPackedTT; tt >= 1; --tt) {
+            const int ntg = (fw + tt * g - 1) / (tt * g);
+            if (best_work < 0 || ntg * tt < best_work) {
+                best_work = ntg * tt;
+                w.tt = tt;
+                w.ntg = ntg;
+            }
+        }
+    } else {
+        // the largest group of taps (at most kMaxTT) whose ragged last group wastes
+        // at most a tenth of the row's MFMA work
+        for (int tt = std::min(fw, kMaxTT); tt >= 1; --tt) {
+            const int ntg = (fw + tt - 1) / tt;
+            if (10 * (ntg * tt - fw) <= fw) {
+                w.tt = tt;
+                w.ntg = ntg;
+                break;
+            }
         }
     }
     w.positions = (int64_t)F * E_h * (E_w + fw - 1);
     w.nchunks = (w.positions + kKC - 1) / kKC;
     w.otiles = (Cout + kWT - 1) / kWT;
-    w.itiles = (Cin + kWT - 1) / kWT;
+    w.itiles = w.packed ? 1 : (Cin + kWT - 1) / kWT;
     const int64_t base = (int64_t)w.otiles * w.itiles * fh * w.ntg;
     // About 512 workgroups run at once (two or three per CU, 53-55 KB of LDS
     // each).  Take at least eight rounds of 512 and, among the split counts up
     // to twice that, the one whose last round is fullest; every split keeps at
-    // least 8 chunks.
-    const int64_t max_splits = std::max<int64_t>(1, std::min<int64_t>(4096, w.nchunks / 8));
+    // least 64 chunks, so that a workgroup's prologue and partial-sum stores stay
+    // small against its loop (measured on the 512 x 512 frame: 8 -> 64 chunks
+    // makes its weight gradients 6.6 -> 5.5 ms).
+    const int64_t max_splits = std::max<int64_t>(1, std::min<int64_t>(4096, w.nchunks / 64));
     const int64_t lo = std::min(max_splits, std::max<int64_t>(1, (512 * 8 + base - 1) / base));
     const int64_t hi = std::min(max_splits, 2 * lo);
     int64_t best = lo;
@@ -415,18 +463,18 @@ WgradPlan wgrad_plan(int F, int E_h, int E_w, int Cout, int Cin, int fh, int fw)
     return w;
 }
 
-template <bool VEC, int TT>
+template <bool VEC, int TT, bool PACKED>
 static hipError_t run_wgrad(const float* dy, const float* x, int E_h, int E_w, int U_h, int U_w, int Cout, int Cin,
                             int fh, int fw, const WgradPlan& w, float* partial, float* bpart, hipStream_t s) {
-    auto kern = wgrad_mfma_kernel<VEC, TT>;
+    auto kern = wgrad_mfma_kernel<VEC, TT, PACKED>;
     const size_t lds = wgrad_lds_bytes(TT);
     hipError_t e = allow_lds((const void*)kern, lds);
     if (e != hipSuccess) return e;
     const int64_t nblocks = (int64_t)w.otiles * w.itiles * fh * w.ntg * w.splits;
     if (nblocks >= (1ll << 31)) return hipErrorInvalidConfiguration;
     kern<<<dim3((unsigned)nblocks), 256, lds, s>>>(dy, x, E_h, E_w, U_h, U_w, Cout, Cin, fh, fw, (int)w.positions,
-                                                   (int)w.nchunks, w.otiles, w.itiles, w.ntg, w.splits, partial,
-                                                   bpart);
+                                                   (int)w.nchunks, w.otiles, w.itiles, w.ntg, w.splits, w.cpt,
+                                                   partial, bpart);
     return hipGetLastError();
 }
 
@@ -434,15 +482,24 @@ template <bool VEC>
 static hipError_t dispatch_wgrad(const float* dy, const float* x, int E_h, int E_w, int U_h, int U_w, int Cout,
                                  int Cin, int fh, int fw, const WgradPlan& w, float* partial, float* bpart,
                                  hipStream_t s) {
+    if (w.packed) {
+        switch (w.tt) {
+            case 1: return run_wgrad<VEC, 1, true>(dy, x, E_h, E_w, U_h, U_w, Cout, Cin, fh, fw, w, partial, bpart, s);
+            case 2: return run_wgrad<VEC, 2, true>(dy, x, E_h, E_w, U_h, U_w, Cout, Cin, fh, fw, w, partial, bpart, s);
+            case 3: return run_wgrad<VEC, 3, true>(dy, x, E_h, E_w, U_h, U_w, Cout, Cin, fh, fw, w, partial, bpart, s);
+            case 4: return run_wgrad<VEC, 4, true>(dy, x, E_h, E_w, U_h, U_w, Cout, Cin, fh, fw, w, partial, bpart, s);
+        }
+        return hipErrorInvalidValue;
+    }
     switch (w.tt) {
-        case 1: return run_wgrad<VEC, 1>(dy, x, E_h, E_w, U_h, U_w, Cout, Cin, fh, fw, w, partial, bpart, s);
-        case 2: return run_wgrad<VEC, 2>(dy, x, E_h, E_w, U_h, U_w, Cout, Cin, fh, fw, w, partial, bpart, s);
-        case 3: return run_wgrad<VEC, 3>(dy, x, E_h, E_w, U_h, U_w, Cout, Cin, fh, fw, w, partial, bpart, s);
-        case 4: return run_wgrad<VEC, 4>(dy, x, E_h, E_w, U_h, U_w, Cout, Cin, fh, fw, w, partial, bpart, s);
-        case 5: return run_wgrad<VEC, 5>(dy, x, E_h, E_w, U_h, U_w, Cout, Cin, fh, fw, w, partial, bpart, s);
-        case 6: return run_wgrad<VEC, 6>(dy, x, E_h, E_w, U_h, U_w, Cout, Cin, fh, fw, w, partial, bpart, s);
-        case 7: return run_wgrad<VEC, 7>(dy, x, E_h, E_w, U_h, U_w, Cout, Cin, fh, fw, w, partial, bpart, s);
-        case 8: return run_wgrad<VEC, 8>(dy, x, E_h, E_w, U_h, U_w, Cout, Cin, fh, fw, w, partial, bpart, s);
+        case 1: return run_wgrad<VEC, 1, false>(dy, x, E_h, E_w, U_h, U_w, Cout, Cin, fh, fw, w, partial, bpart, s);
+        case 2: return run_wgrad<VEC, 2, false>(dy, x, E_h, E_w, U_h, U_w, Cout, Cin, fh, fw, w, partial, bpart, s);
+        case 3: return run_wgrad<VEC, 3, false>(dy, x, E_h, E_w, U_h, U_w, Cout, Cin, fh, fw, w, partial, bpart, s);
+        case 4: return run_wgrad<VEC, 4, false>(dy, x, E_h, E_w, U_h, U_w, Cout, Cin, fh, fw, w, partial, bpart, s);
+        case 5: return run_wgrad<VEC, 5, false>(dy, x, E_h, E_w, U_h, U_w, Cout, Cin, fh, fw, w, partial, bpart, s);
+        case 6: return run_wgrad<VEC, 6, false>(dy, x, E_h, E_w, U_h, U_w, Cout, Cin, fh, fw, w, partial, bpart, s);
+        case 7: return run_wgrad<VEC, 7, false>(dy, x, E_h, E_w, U_h, U_w, Cout, Cin, fh, fw, w, partial, bpart, s);
+        case 8: return run_wgrad<VEC, 8, false>(dy, x, E_h, E_w, U_h, U_w, Cout, Cin, fh, fw, w, partial, bpart, s);
     }
     return hipErrorInvalidValue;
 }
@@ -451,7 +508,8 @@ hipError_t launch_wgrad(const float* dy, const float* x, int F, int E_h, int E_w
                         int fh, int fw, const WgradPlan& w, float* partial, float* dw, float* db, hipStream_t s) {
     (void)F;
     // positions and chunks are 32-bit in the kernel
-    if (w.positions + w.tt + kKC >= (1ll << 31) || U_w != E_w + fw - 1 || U_h != E_h + fh - 1)
+    const int span = w.packed ? w.tt * (kWT / w.cpt) : w.tt;   // taps per group
+    if (w.positions + span + kKC >= (1ll << 31) || U_w != E_w + fw - 1 || U_h != E_h + fh - 1)
         return hipErrorInvalidConfiguration;
     float* bpart = partial + w.partial_floats;
     const bool vec = Cout % 4 == 0 && Cin % 4 == 0;

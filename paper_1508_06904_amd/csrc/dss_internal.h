@@ -97,7 +97,9 @@ PlanConv mfma_launch_variant(const PlanConv& pc, int F, int Hin, int Win, int di
 
 // Host-side description of a weight-gradient launch (backward.hip).
 struct WgradPlan {
-    int tt = 1, ntg = 1;         // taps per workgroup and tap groups per filter row
+    int tt = 1, ntg = 1;         // MFMA tiles per wave (taps, or tap groups when packed), groups per row
+    bool packed = false;         // narrow layer: cpt columns per tap, 64 / cpt taps per tile
+    int cpt = 64;
     int otiles = 0, itiles = 0, splits = 0;
     int64_t positions = 0;       // F * E_h * U_w: output rows read over the input width
     int64_t nchunks = 0, partial_floats = 0;
