@@ -766,7 +766,11 @@ struct BwdLayout {
 
 int64_t align256(int64_t b) { return (b + 255) / 256 * 256; }
 
-dss_status backward_layout(const Chain& ch, int H, int W, bool want_dx, BwdLayout* out) {
+// plan: the plan whose input-gradient convolutions run (their kernels decide
+// whether a zero-bordered copy of the gradient is needed), or NULL for a chain
+// alone (the kernels the chain's plan would choose).
+dss_status backward_layout(const Chain& ch, int H, int W, bool want_dx, BwdLayout* out,
+                           const dss_plan* plan = nullptr) {
     BwdLayout B;
     dss_status s = compute_geometry(ch, DSS_F32, H, W, 0, &B.G);
     if (s != DSS_OK) return s;
@@ -799,8 +803,14 @@ dss_status backward_layout(const Chain& ch, int H, int W, bool want_dx, BwdLayou
             B.flops += 2.0 * f;                           // forward + weight gradient
             if (j > 1 || want_dx) {
                 B.flops += f;                             // input gradient
-                padmax = std::max(padmax, Fin * (lg.E_h + 2 * (c.c_h - 1)) * (int64_t)(lg.E_w + 2 * (c.c_w - 1)) *
-                                              c.cout * 4);
+                // the MFMA kernel reads the gradient with a virtual zero border;
+                // the direct kernel needs it written out
+                const ConvImpl bi = plan && (int)plan->bconvs.size() >= j ? plan->bconvs[j - 1].impl
+                                                                           : choose_impl(c.cout, c.cin, c.c_h, c.c_w,
+                                                                                         DSS_F32);
+                if (bi == CONV_DIRECT)
+                    padmax = std::max(padmax, Fin * (lg.E_h + 2 * (c.c_h - 1)) *
+                                                  (int64_t)(lg.E_w + 2 * (c.c_w - 1)) * c.cout * 4);
             }
             B.wg[j] = wgrad_plan((int)Fin, lg.E_h, lg.E_w, c.cout, c.cin, c.c_h, c.c_w);
             wpmax = std::max(wpmax, (B.wg[j].partial_floats + B.wg[j].bias_partial_floats) * 4);
@@ -856,7 +866,7 @@ extern "C" dss_status dss_plan_backward_geometry(dss_plan_t plan, int32_t H, int
                                                  int64_t* bias_grad_floats, double* flops) {
     if (!plan) return fail(DSS_E_INVALID, "NULL plan");
     BwdLayout B;
-    dss_status s = backward_layout(plan->chain, H, W, with_signal_grad != 0, &B);
+    dss_status s = backward_layout(plan->chain, H, W, with_signal_grad != 0, &B, plan);
     if (s != DSS_OK) return s;
     return backward_geometry_out(B, workspace_bytes, weight_grad_floats, bias_grad_floats, flops);
 }
@@ -870,7 +880,7 @@ extern "C" dss_status dss_backward_dense(dss_plan_t plan, const void* signal, in
     if (plan->dtype != DSS_F32) return fail(DSS_E_UNSUPPORTED, "the backward pass is implemented for binary32 plans");
     const Chain& ch = plan->chain;
     BwdLayout B;
-    dss_status s = backward_layout(ch, H, W, grad_signal != nullptr, &B);
+    dss_status s = backward_layout(ch, H, W, grad_signal != nullptr, &B, plan);
     if (s != DSS_OK) return s;
     if (!workspace) return fail(DSS_E_INVALID, "NULL workspace (need %lld bytes)", (long long)B.total);
     if (workspace_bytes < B.total)
@@ -957,16 +967,21 @@ extern "C" dss_status dss_backward_dense(dss_plan_t plan, const void* signal, in
         });
         if (e != hipSuccess) return hip_fail(e, "wgrad launch");
         if (j == 1 && !grad_signal) break;
+        // input gradient: the full convolution of the output gradient with the
+        // transposed, flipped filters, i.e. a valid convolution over the gradient
+        // with a zero border of fh - 1 x fw - 1 samples
         const int ph = c.c_h - 1, pw = c.c_w - 1;
-        e = T.run("pad_grad", j, 0.0, 0.0, [&] {
-            return launch_pad_grad(gb[cur], Fin, lg.E_h, lg.E_w, c.cout, ph, pw, padb, stream);
-        });
-        if (e != hipSuccess) return hip_fail(e, "pad_grad launch");
+        const PlanConv bpc = mfma_launch_variant(plan->bconvs[j - 1], Fin, lg.E_h, lg.E_w, 1, 1, ph, pw);
+        if (bpc.impl != CONV_MFMA_F32) {
+            e = T.run("pad_grad", j, 0.0, 0.0, [&] {
+                return launch_pad_grad(gb[cur], Fin, lg.E_h, lg.E_w, c.cout, ph, pw, padb, stream);
+            });
+            if (e != hipSuccess) return hip_fail(e, "pad_grad launch");
+        }
         const int Hp = lg.E_h + 2 * ph, Wp = lg.E_w + 2 * pw;
-        const PlanConv bpc = mfma_launch_variant(plan->bconvs[j - 1], Fin, Hp, Wp, 1, 1);
         e = T.run(dgrad_name(bpc), j, fl, 0.0, [&]() -> hipError_t {
             if (bpc.impl == CONV_MFMA_F32)
-                return launch_conv_mfma_f32(padb, Fin, Hp, Wp, 1, 1, bpc, gb[cur ^ 1], stream);
+                return launch_conv_mfma_f32_padded(gb[cur], Fin, lg.E_h, lg.E_w, ph, pw, bpc, gb[cur ^ 1], stream);
             return launch_conv_direct(DSS_F32, DSS_F32, padb, Fin, Hp, Wp, 1, 1, c.cout, bpc, gb[cur ^ 1], stream);
         });
         if (e != hipSuccess) return hip_fail(e, "input-gradient conv launch");

@@ -83,7 +83,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
     Tout* __restrict__ out,            // [F][Hout][Wout][Cout]
     int Hout, int Wout, int TH, int TW, int tilesY, int tilesX, int nbs, int dbl_halo,
     int flat_h, int flat_w,             // flat mode: input fragments of flat_h x flat_w (0: spatial tiles)
-    int dil_h, int dil_w) {             // dilated mode (> 1): taps dil apart on one signal, tiled by phase
+    int dil_h, int dil_w,               // dilated mode (> 1): taps dil apart on one signal, tiled by phase
+    int pad_h, int pad_w) {             // spatial tiles: a zero border of pad samples around every fragment
     using Cfg = MfmaCfg<BF16, WGM, WGN, MT, NT>;
     constexpr int THREADS = Cfg::THREADS;
     constexpr int WSLOTS = Cfg::WSLOTS;
@@ -165,7 +166,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
     const size_t f_base = dilated ? ((size_t)py * Win + px) * row_bytes : (size_t)f * Hin * Win * row_bytes;
     const int lim_h = dilated ? (Hin - py + dil_h - 1) / dil_h : Hin;   // samples of this phase / fragment
     const int lim_w = dilated ? (Win - px + dil_w - 1) / dil_w : Win;
-    const char* in_tile = in + f_base + (size_t)ty0 * row_step + (size_t)tx0 * col_step;
+    // top-left input sample of the tile's halo (negative inside the zero border)
+    const int hy0 = ty0 - pad_h, hx0 = tx0 - pad_w;
+    const char* in_f = in + f_base;
     const int taps = fh * fw;
     const int steps = nchunks * taps;
     const char* w_nb = wp + (size_t)nb * steps * (Cfg::BN * kChunkBytes);
@@ -186,15 +189,17 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
         w_off[r] = (S >= WSLOTS || q == 4) ? kPad : n * kChunkBytes + q * 16;
     }
     auto stage_halo = [&](int cc, char* dst) {
-        const char* src_c = in_tile + (size_t)cc * kChunkBytes;
+        const char* src_c = in_f + (size_t)cc * kChunkBytes;
         const int c_base = cc * Cfg::CC;
         for (int r0 = 0; r0 < halo_slots; r0 += THREADS) {
             const int S = r0 + tid;
             const int px = S / kSlotsPerRow, q = S - px * kSlotsPerRow;
             if (S < halo_slots && q < 4) {
                 const int dy = px / HW, dx = px - dy * HW;
-                const bool ok = ty0 + dy < lim_h && tx0 + dx < lim_w && c_base + q * (16 / Cfg::ES) < Cin;
-                dma16(ok ? src_c + (size_t)dy * row_step + (size_t)dx * col_step + q * 16 : zero,
+                const int yy = hy0 + dy, xx = hx0 + dx;
+                const bool ok = (unsigned)yy < (unsigned)lim_h && (unsigned)xx < (unsigned)lim_w &&
+                                c_base + q * (16 / Cfg::ES) < Cin;
+                dma16(ok ? src_c + (size_t)yy * row_step + (size_t)xx * col_step + q * 16 : zero,
                       dst + (r0 + wave * 64) * 16);
             }
         }
@@ -574,8 +579,10 @@ struct LaunchShape {
     int64_t nblocks;    // 0 if no tile fits
 };
 
+// Hin x Win: the fragment extent including any zero border (which rules out the
+// flat reading, allow_flat = false).
 static LaunchShape launch_shape(int BM, bool bf16, size_t wb, int F, int Hin, int Win, int dil_h, int dil_w, int fh, int fw,
-                                int nbs) {
+                                int nbs, bool allow_flat = true) {
     LaunchShape L{Tile{0, 0, 0, 0}, 0, 0, 0, 0};
     const size_t lds = device_lds_limit();
     if (dil_h * dil_w > 1) {
@@ -591,7 +598,7 @@ static LaunchShape launch_shape(int BM, bool bf16, size_t wb, int F, int Hin, in
     const int Hout = Hin - fh + 1, Wout = Win - fw + 1;
     L.t = pick_tile(BM, wb, Hout, Wout, fh, fw, lds, bf16);
     const int64_t flat_len = (int64_t)F * Hin * Win;
-    if (flat_len < (1ll << 30)) {
+    if (allow_flat && flat_len < (1ll << 30)) {
         const Tile ft = flat_tile(BM, wb, Win, fh, fw, lds);
         const int64_t work_tiles =
             L.t.TH ? (int64_t)F * ceil_div64(Hout, L.t.TH) * L.t.TH * ceil_div64(Wout, L.t.TW) * L.t.TW : -1;
@@ -621,15 +628,19 @@ static LaunchShape launch_shape(int BM, bool bf16, size_t wb, int F, int Hin, in
 // tile against ceil(blocks64 / 256) of half the work each.  A lone workgroup
 // per CU (one wave per SIMD) hides no MFMA latency, so up to 256 workgroups
 // the 64-channel tile is taken.
-PlanConv mfma_launch_variant(const PlanConv& pc, int F, int Hin, int Win, int dil_h, int dil_w) {
+PlanConv mfma_launch_variant(const PlanConv& pc, int F, int Hin, int Win, int dil_h, int dil_w, int pad_h,
+                             int pad_w) {
     if (!pc.w_alt || pc.impl == CONV_DIRECT) return pc;
     const bool bf16 = pc.impl == CONV_MFMA_BF16;
+    const bool flat = pad_h == 0 && pad_w == 0;
+    Hin += 2 * pad_h;
+    Win += 2 * pad_w;
     const LaunchShape a = launch_shape(256, bf16, weight_lds_bytes(bf16, pc.bn), F, Hin, Win, dil_h, dil_w, pc.fh, pc.fw,
-                                       pc.cout_pad / pc.bn);
+                                       pc.cout_pad / pc.bn, flat);
     if (a.nblocks == 0 || a.nblocks >= 512) return pc;
     const LaunchShape b =
         launch_shape(256, bf16, weight_lds_bytes(bf16, pc.bn_alt), F, Hin, Win, dil_h, dil_w, pc.fh, pc.fw,
-                     pc.cout_pad_alt / pc.bn_alt);
+                     pc.cout_pad_alt / pc.bn_alt, flat);
     if (b.nblocks == 0) return pc;
     if (a.nblocks > 256 && 11 * ceil_div64(b.nblocks, 256) >= 20 * ceil_div64(a.nblocks, 256)) return pc;
     PlanConv alt = pc;
@@ -640,55 +651,62 @@ PlanConv mfma_launch_variant(const PlanConv& pc, int F, int Hin, int Win, int di
 }
 
 template <bool BF16, typename Tout, int WGM, int WGN, int MT, int NT>
-static hipError_t run_mfma(const void* in, int F, int Hin, int Win, int dil_h, int dil_w, const PlanConv& pc,
-                           void* out, hipStream_t s) {
+static hipError_t run_mfma(const void* in, int F, int Hin, int Win, int dil_h, int dil_w, int pad_h, int pad_w,
+                           const PlanConv& pc, void* out, hipStream_t s) {
     using Cfg = MfmaCfg<BF16, WGM, WGN, MT, NT>;
     const bool dilated = dil_h * dil_w > 1;
+    const bool padded = pad_h > 0 || pad_w > 0;
     if (dilated && F != 1) return hipErrorInvalidValue;   // dilated: one signal, tiled per phase
+    if (padded && (dilated || pad_h < 0 || pad_w < 0)) return hipErrorInvalidValue;
     const int nbs = pc.cout_pad / Cfg::BN;
-    const LaunchShape L =
-        launch_shape(Cfg::BM, BF16, weight_lds_bytes(BF16, Cfg::BN), F, Hin, Win, dil_h, dil_w, pc.fh, pc.fw, nbs);
+    const LaunchShape L = launch_shape(Cfg::BM, BF16, weight_lds_bytes(BF16, Cfg::BN), F, Hin + 2 * pad_h,
+                                       Win + 2 * pad_w, dil_h, dil_w, pc.fh, pc.fw, nbs, !padded);
     if (L.nblocks == 0) return hipErrorInvalidConfiguration;
     if (L.nblocks >= (1ll << 31)) return hipErrorInvalidConfiguration;
     auto kern = conv_mfma_kernel<BF16, Tout, WGM, WGN, MT, NT>;
     hipError_t e = allow_large_lds((const void*)kern, L.t.lds);
     if (e != hipSuccess) return e;
     const int nchunks = pc.cin_pad / Cfg::CC;
-    const int Hout = Hin - dil_h * (pc.fh - 1), Wout = Win - dil_w * (pc.fw - 1);
+    const int Hout = Hin + 2 * pad_h - dil_h * (pc.fh - 1), Wout = Win + 2 * pad_w - dil_w * (pc.fw - 1);
     if (L.flat) {
         // one "fragment" of 1 x (F * Hin * Win) samples for the staging and the tile grid
         const int flat_len = (int)((int64_t)F * Hin * Win);   // below 2^30 in flat mode
         kern<<<dim3((unsigned)L.nblocks), Cfg::THREADS, L.t.lds, s>>>(
             (const char*)in, 1, flat_len, pc.cin, (const char*)pc.w, pc.b, pc.fh, pc.fw, pc.cout, pc.act, nchunks,
-            (Tout*)out, Hout, Wout, 1, L.t.TW, 1, L.tilesX, nbs, L.t.dbl, Hin, Win, 1, 1);
+            (Tout*)out, Hout, Wout, 1, L.t.TW, 1, L.tilesX, nbs, L.t.dbl, Hin, Win, 1, 1, 0, 0);
         return hipGetLastError();
     }
     kern<<<dim3((unsigned)L.nblocks), Cfg::THREADS, L.t.lds, s>>>(
         (const char*)in, Hin, Win, pc.cin, (const char*)pc.w, pc.b, pc.fh, pc.fw, pc.cout, pc.act, nchunks,
-        (Tout*)out, Hout, Wout, L.t.TH, L.t.TW, L.tilesY, L.tilesX, nbs, L.t.dbl, 0, 0, dil_h, dil_w);
+        (Tout*)out, Hout, Wout, L.t.TH, L.t.TW, L.tilesY, L.tilesX, nbs, L.t.dbl, 0, 0, dil_h, dil_w, pad_h, pad_w);
     return hipGetLastError();
 }
 
 template <bool BF16, typename Tout>
-static hipError_t dispatch_bn(const void* in, int F, int Hin, int Win, int dh, int dw, const PlanConv& pc, void* out,
-                              hipStream_t s) {
+static hipError_t dispatch_bn(const void* in, int F, int Hin, int Win, int dh, int dw, int ph, int pw,
+                              const PlanConv& pc, void* out, hipStream_t s) {
     switch (pc.bn) {
-        case 128: return run_mfma<BF16, Tout, 2, 2, 4, 2>(in, F, Hin, Win, dh, dw, pc, out, s);
-        case 64: return run_mfma<BF16, Tout, 4, 1, 2, 2>(in, F, Hin, Win, dh, dw, pc, out, s);
-        case 32: return run_mfma<BF16, Tout, 4, 1, 2, 1>(in, F, Hin, Win, dh, dw, pc, out, s);
+        case 128: return run_mfma<BF16, Tout, 2, 2, 4, 2>(in, F, Hin, Win, dh, dw, ph, pw, pc, out, s);
+        case 64: return run_mfma<BF16, Tout, 4, 1, 2, 2>(in, F, Hin, Win, dh, dw, ph, pw, pc, out, s);
+        case 32: return run_mfma<BF16, Tout, 4, 1, 2, 1>(in, F, Hin, Win, dh, dw, ph, pw, pc, out, s);
     }
     return hipErrorInvalidValue;
 }
 
 hipError_t launch_conv_mfma_f32(const float* in, int F, int Hin, int Win, int dil_h, int dil_w, const PlanConv& pc,
                                 float* out, hipStream_t s) {
-    return dispatch_bn<false, float>(in, F, Hin, Win, dil_h, dil_w, pc, out, s);
+    return dispatch_bn<false, float>(in, F, Hin, Win, dil_h, dil_w, 0, 0, pc, out, s);
+}
+
+hipError_t launch_conv_mfma_f32_padded(const float* in, int F, int Hin, int Win, int pad_h, int pad_w,
+                                       const PlanConv& pc, float* out, hipStream_t s) {
+    return dispatch_bn<false, float>(in, F, Hin, Win, 1, 1, pad_h, pad_w, pc, out, s);
 }
 
 hipError_t launch_conv_mfma_bf16(dss_dtype tout, const uint16_t* in, int F, int Hin, int Win, int dil_h, int dil_w,
                                  const PlanConv& pc, void* out, hipStream_t s) {
-    if (tout == DSS_F32) return dispatch_bn<true, float>(in, F, Hin, Win, dil_h, dil_w, pc, out, s);
-    return dispatch_bn<true, uint16_t>(in, F, Hin, Win, dil_h, dil_w, pc, out, s);
+    if (tout == DSS_F32) return dispatch_bn<true, float>(in, F, Hin, Win, dil_h, dil_w, 0, 0, pc, out, s);
+    return dispatch_bn<true, uint16_t>(in, F, Hin, Win, dil_h, dil_w, 0, 0, pc, out, s);
 }
 
 }  // namespace dss

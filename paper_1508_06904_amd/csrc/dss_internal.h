@@ -93,7 +93,8 @@ struct PlanConv {
 };
 
 // The variant a launch over F fragments of Hin x Win (taps dil apart) should use.
-PlanConv mfma_launch_variant(const PlanConv& pc, int F, int Hin, int Win, int dil_h, int dil_w);
+PlanConv mfma_launch_variant(const PlanConv& pc, int F, int Hin, int Win, int dil_h, int dil_w, int pad_h = 0,
+                             int pad_w = 0);
 
 // Host-side description of a weight-gradient launch (backward.hip).
 struct WgradPlan {
@@ -142,6 +143,10 @@ hipError_t launch_conv_mfma_f32(const float* in, int F, int Hin, int Win, int di
                                 const PlanConv& pc, float* out, hipStream_t s);
 hipError_t launch_conv_mfma_bf16(dss_dtype tout, const uint16_t* in, int F, int Hin, int Win, int dil_h,
                                  int dil_w, const PlanConv& pc, void* out, hipStream_t s);
+// As launch_conv_mfma_f32 over fragments with a zero border of pad_h x pad_w
+// samples that is not stored (output (Hin + 2 pad_h - fh + 1) x (Win + 2 pad_w - fw + 1)).
+hipError_t launch_conv_mfma_f32_padded(const float* in, int F, int Hin, int Win, int pad_h, int pad_w,
+                                       const PlanConv& pc, float* out, hipStream_t s);
 hipError_t launch_pool_frag(dss_dtype dt, const void* in, int S_h, int S_w, int E_h, int E_w, int C,
                             int k_h, int k_w, void* out, hipStream_t s);
 hipError_t launch_patch_pack(dss_dtype dt, const void* in, int C, int H, int W, int O_w, int64_t first, int count,
