@@ -98,6 +98,8 @@ def summarize(recs, steps):
             e["tflops"] = d["flops"] / d["ms"] / 1e9
         if d["bytes"] > 0:
             e["gbs"] = d["bytes"] / d["ms"] / 1e6
+            if d["flops"] == 0:                       # HBM-bound data movement: pooling, Frag, Defrag
+                e["frac_of_hbm_peak"] = e["gbs"] / PEAK_HBM_GBS
         out.append((e, d))
     return out
 
@@ -352,11 +354,20 @@ def calibrate_copy(n=4, nbytes=1 << 30):
     src = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda")
     dst = torch.empty_like(src)
     torch.cuda.synchronize()
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    start.record()
     for _ in range(n):
         dst.copy_(src)
+    end.record()
     torch.cuda.synchronize()
+    ms = start.elapsed_time(end) / n
+    # the achievable streaming rate of a plain copy, the practical ceiling the
+    # HBM-bound kernels are compared with (besides the 8 TB/s peak)
     print(json.dumps({"calibration": "device copy", "bytes_read_per_launch": nbytes,
-                      "bytes_written_per_launch": nbytes, "launches": n}), flush=True)
+                      "bytes_written_per_launch": nbytes, "launches": n, "ms_per_launch": ms,
+                      "gbs": 2 * nbytes / ms / 1e6, "frac_of_hbm_peak": 2 * nbytes / ms / 1e6 / PEAK_HBM_GBS}),
+          flush=True)
 
 
 def cpu_baseline_backward(w, g, target_s):
