@@ -71,6 +71,33 @@ def test_backward_random_chain(name):
     check_all(gpu_backward(plan, w.x, G), ob.dense_backward(w.layers, w.x, G), name)
 
 
+# Layers with at most 32 input channels take the packed weight-gradient mode
+# (several taps share the 64 MFMA columns); these chains give it one channel,
+# channel counts that are not powers of two, wide filters split into several tap
+# groups, and ragged last groups (filter widths 7, 9, 11, 13 and 5 against group
+# capacities of 16, 16, 6, 16 and 6 taps).
+NARROW = {
+    "2d_narrow": ([("conv", 1, 8, 3, 7, "relu"), ("pool", 2, 2), ("conv", 8, 12, 2, 9, "tanh"),
+                   ("conv", 12, 3, 2, 2, "none")], 1, 2),
+    "1d_narrow": ([("conv", 5, 24, 1, 13, "relu"), ("pool", 1, 3), ("conv", 24, 32, 1, 11, "relu"),
+                   ("conv", 32, 2, 1, 5, "none")], 5, 1),
+}
+
+
+@pytest.mark.parametrize("name", list(NARROW))
+def test_backward_narrow_layers(name):
+    arch, C, nd = NARROW[name]
+    w0 = wl.custom(arch, C, 1, 1, seed=1)
+    B = oracle.receptive_field(w0.layers)
+    H = 1 if nd == 1 else B[0] + 40
+    W = B[1] + (3000 if nd == 1 else 100)
+    w = wl.custom(arch, C, H, W, seed=21, value_kind="normal")
+    G = np.random.default_rng(22).standard_normal((w.layers[-1]["cout"], H - B[0] + 1, W - B[1] + 1))
+    plan = dss.Plan(w.layers, nd, C)
+    log("backward %s on %s" % (name, w.x.shape))
+    check_all(gpu_backward(plan, w.x, G), ob.dense_backward(w.layers, w.x, G), name)
+
+
 @pytest.mark.parametrize("kernel", ["mfma", "direct"])
 def test_backward_exact_integer_chain(kernel, monkeypatch):
     if kernel == "direct":
