@@ -70,7 +70,11 @@ static ConvImpl choose_impl(int cin, int cout, int fh, int fw, dss_dtype dt) {
     // kernel for every convolution of plans created afterwards.
     const char* force = getenv("DSS_CONV_KERNEL");
     if (force && std::strcmp(force, "direct") == 0) return CONV_DIRECT;
-    if (cin < 16) return CONV_DIRECT;
+    // few input channels (first layers), or few output channels in binary32
+    // (final projections, where a 32-channel MFMA tile would be mostly idle; the
+    // LDS-staged direct kernel streams them faster; with bfloat16 inputs the
+    // MFMA tile still wins)
+    if (cin < 16 || (cout <= 8 && dt == DSS_F32)) return CONV_DIRECT;
     if (dt == DSS_F32 && cin % 4 == 0 && mfma_supports(false, cout, fh, fw)) return CONV_MFMA_F32;
     if (dt == DSS_BF16 && cin % 8 == 0 && mfma_supports(true, cout, fh, fw)) return CONV_MFMA_BF16;
     return CONV_DIRECT;
@@ -436,7 +440,8 @@ const char* conv_name(const PlanConv& pc, dss_dtype tout) {
                                                                    : "conv_mfma_bf16_n32_f32out";
             return pc.bn == 128 ? "conv_mfma_bf16_n128" : pc.bn == 64 ? "conv_mfma_bf16_n64" : "conv_mfma_bf16_n32";
         default:
-            return "conv_direct";
+            // the direct kernel's LDS-staged form for few outputs and many inputs
+            return pc.cin >= 16 && pc.cout_pad <= 8 ? "conv_narrow" : "conv_direct";
     }
 }
 

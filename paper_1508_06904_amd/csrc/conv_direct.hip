@@ -7,13 +7,50 @@
 // tap order).  In the dilated fashion (appendix, Definition "dilate") tap
 // (t_h, t_w) reads sample (y + dil_h t_h, x + dil_w t_w) of a single signal.
 // Used for the layers that do not suit the MFMA implicit GEMM: the first layer
-// (few input channels) and the final projections (few output channels).  One thread computes COB consecutive output channels of one output
-// sample; the weight reads are uniform across the wavefront and go through the
-// scalar cache.  Accumulation is binary32 (bfloat16 activations are widened).
+// (few input channels) and the final projections (few output channels, where
+// an MFMA tile of 32 channels would be mostly idle).  One thread computes COB
+// consecutive output channels of one output sample; the weight reads are
+// uniform across the wavefront and go through the scalar cache.  Accumulation
+// is binary32 (bfloat16 activations are widened).
 #include "dev_common.h"
 #include "dss_internal.h"
 
 namespace dss {
+
+// COB activated outputs of sample p (channels og .. og + COB - 1), as 16-byte
+// vectors where the channel block is whole and aligned.
+template <typename Tout, int COB>
+__device__ __forceinline__ void store_outputs(Tout* __restrict__ out, int64_t p, int Cout, int og, int act,
+                                              const float (&acc)[COB]) {
+    Tout* op = out + p * Cout + og;
+    const bool aligned16 = ((uintptr_t)out & 15) == 0;
+    if constexpr (sizeof(Tout) == 4 && COB % 4 == 0) {
+        if (aligned16 && Cout % 4 == 0 && og + COB <= Cout) {   // 16-byte aligned: full vectors
+#pragma unroll
+            for (int o = 0; o < COB; o += 4)
+                *reinterpret_cast<float4*>(op + o) = make_float4(activate(act, acc[o]), activate(act, acc[o + 1]),
+                                                                 activate(act, acc[o + 2]), activate(act, acc[o + 3]));
+            return;
+        }
+    }
+    if constexpr (sizeof(Tout) == 2 && COB % 8 == 0) {
+        if (aligned16 && Cout % 8 == 0 && og + COB <= Cout) {   // 8 bfloat16 channels per 16-byte store
+#pragma unroll
+            for (int o = 0; o < COB; o += 8) {
+                uint32_t w[4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    w[e] = (uint32_t)f32_to_bf16(activate(act, acc[o + 2 * e])) |
+                           ((uint32_t)f32_to_bf16(activate(act, acc[o + 2 * e + 1])) << 16);
+                *reinterpret_cast<uint4*>(op + o) = make_uint4(w[0], w[1], w[2], w[3]);
+            }
+            return;
+        }
+    }
+#pragma unroll
+    for (int o = 0; o < COB; ++o)
+        if (og + o < Cout) store_elem(op + o, activate(act, acc[o]));
+}
 
 template <typename Tin, typename Tout, int COB, int VEC>
 __global__ __launch_bounds__(256) void conv_direct_kernel(const Tin* __restrict__ in, int Hin, int Win, int Cin,
@@ -47,40 +84,163 @@ __global__ __launch_bounds__(256) void conv_direct_kernel(const Tin* __restrict_
             }
         }
     }
-    Tout* op = out + p * Cout + og;
-    const bool aligned16 = ((uintptr_t)out & 15) == 0;
-    if constexpr (sizeof(Tout) == 4 && COB % 4 == 0) {
-        if (aligned16 && Cout % 4 == 0 && og + COB <= Cout) {   // 16-byte aligned: full vectors
+    store_outputs<Tout, COB>(out, p, Cout, og, act, acc);
+}
+
+// Few output channels (at most 8) and many input channels (the final
+// projections): the plain kernel above reads a whole channel vector per thread,
+// so each load instruction touches one cache line per lane.  Here a workgroup
+// takes a TH x TW tile of output samples (TH TW = 256, one per thread); per chunk
+// of KC input channels the tile's halo of (TH + dil_h (fh - 1)) x
+// (TW + dil_w (fw - 1)) samples is read with 16-byte loads into registers (the
+// next chunk's loads are issued before this chunk's arithmetic), stored to LDS
+// as binary32 with a KC + 4 float pitch (16-byte reads of consecutive samples
+// hit disjoint banks), and every thread accumulates its sample from there.  The
+// weights of a chunk, taps x KC x COB values read uniformly, go through the
+// scalar cache: KC = 32 for 1x1 filters, 16 for wider ones.
+constexpr int kNMaxUnits = 8;  // 16-byte staging units per thread and chunk
+
+template <typename Tin, typename Tout, int COB, int KC>
+__global__ __launch_bounds__(256) void conv_narrow_kernel(const Tin* __restrict__ in, int Hin, int Win, int Cin,
+                                                         const float* __restrict__ w, const float* __restrict__ bias,
+                                                         int fh, int fw, int dil_h, int dil_w, int Cout, int CoutP,
+                                                         int act, Tout* __restrict__ out, int Hout, int Wout, int TH,
+                                                         int TW, int tilesY, int tilesX) {
+    constexpr int kNC = KC, kNP = KC + 4;
+    constexpr int EPU = 16 / sizeof(Tin);              // channels per 16-byte unit
+    constexpr int UPS = kNC / EPU;                     // units per sample and chunk
+    extern __shared__ __attribute__((aligned(16))) float sm[];
+    const int tiles = tilesY * tilesX;
+    const int f = blockIdx.x / tiles, tr = blockIdx.x - f * tiles;
+    const int ty0 = (tr / tilesX) * TH, tx0 = (tr % tilesX) * TW;
+    const int og = blockIdx.y * COB;
+    const int HWd = TW + dil_w * (fw - 1);
+    const int nunits = (TH + dil_h * (fh - 1)) * HWd * UPS;
+    const int tid = threadIdx.x;
+    const int ly = tid / TW, lx = tid - ly * TW;
+    const int y = ty0 + ly, x = tx0 + lx;
+    const bool active = y < Hout && x < Wout;
+    const Tin* in_f = in + (size_t)f * Hin * Win * Cin;
+    const bool vec = Cin % EPU == 0;
+    float acc[COB];
 #pragma unroll
-            for (int o = 0; o < COB; o += 4)
-                *reinterpret_cast<float4*>(op + o) = make_float4(activate(act, acc[o]), activate(act, acc[o + 1]),
-                                                                 activate(act, acc[o + 2]), activate(act, acc[o + 3]));
-            return;
-        }
-    }
-    if constexpr (sizeof(Tout) == 2 && COB % 8 == 0) {
-        if (aligned16 && Cout % 8 == 0 && og + COB <= Cout) {   // 8 bfloat16 channels per 16-byte store
+    for (int o = 0; o < COB; ++o) acc[o] = bias[og + o];
+
+    uint4 ru[kNMaxUnits];
+    auto load_chunk = [&](int c0) {
 #pragma unroll
-            for (int o = 0; o < COB; o += 8) {
-                uint32_t w[4];
+        for (int k = 0; k < kNMaxUnits; ++k) {
+            const int u = tid + 256 * k;
+            ru[k] = make_uint4(0u, 0u, 0u, 0u);
+            if (u >= nunits) continue;
+            const int si = u / UPS, q = u - si * UPS;
+            const int hy = si / HWd, hx = si - hy * HWd;
+            const int gy = ty0 + hy, gx = tx0 + hx, c = c0 + EPU * q;
+            if (gy >= Hin || gx >= Win || c >= Cin) continue;
+            const Tin* src = in_f + ((size_t)gy * Win + gx) * Cin + c;
+            if (vec) {
+                ru[k] = *reinterpret_cast<const uint4*>(src);
+            } else {
+                Tin t[EPU];
 #pragma unroll
-                for (int e = 0; e < 4; ++e)
-                    w[e] = (uint32_t)f32_to_bf16(activate(act, acc[o + 2 * e])) |
-                           ((uint32_t)f32_to_bf16(activate(act, acc[o + 2 * e + 1])) << 16);
-                *reinterpret_cast<uint4*>(op + o) = make_uint4(w[0], w[1], w[2], w[3]);
+                for (int e = 0; e < EPU; ++e) t[e] = c + e < Cin ? src[e] : Tin(0);
+                ru[k] = __builtin_bit_cast(uint4, t);
             }
-            return;
+        }
+    };
+    auto store_chunk = [&]() {
+#pragma unroll
+        for (int k = 0; k < kNMaxUnits; ++k) {
+            const int u = tid + 256 * k;
+            if (u >= nunits) continue;
+            const int si = u / UPS, q = u - si * UPS;
+            float* dst = sm + si * kNP + EPU * q;
+            if constexpr (sizeof(Tin) == 4) {
+                *reinterpret_cast<uint4*>(dst) = ru[k];
+            } else {
+                const uint32_t wv[4] = {ru[k].x, ru[k].y, ru[k].z, ru[k].w};
+#pragma unroll
+                for (int h = 0; h < 2; ++h)
+                    *reinterpret_cast<float4*>(dst + 4 * h) = make_float4(
+                        __uint_as_float(wv[2 * h] << 16), __uint_as_float(wv[2 * h] & 0xffff0000u),
+                        __uint_as_float(wv[2 * h + 1] << 16), __uint_as_float(wv[2 * h + 1] & 0xffff0000u));
+            }
+        }
+    };
+
+    load_chunk(0);
+    for (int c0 = 0; c0 < Cin; c0 += kNC) {
+        __syncthreads();                               // the previous chunk has been used
+        store_chunk();
+        __syncthreads();
+        if (c0 + kNC < Cin) load_chunk(c0 + kNC);      // in flight during the arithmetic below
+        if (!active) continue;
+        const int cn = min(kNC, Cin - c0);
+        for (int th = 0; th < fh; ++th) {
+            for (int tw = 0; tw < fw; ++tw) {
+                const float* sp = sm + ((ly + th * dil_h) * HWd + lx + tw * dil_w) * kNP;
+                const float* wr = w + ((size_t)(th * fw + tw) * Cin + c0) * CoutP + og;
+                if (cn == kNC) {
+#pragma unroll
+                    for (int q = 0; q < kNC / 4; ++q) {
+                        const float4 v4 = *reinterpret_cast<const float4*>(sp + 4 * q);
+                        const float v[4] = {v4.x, v4.y, v4.z, v4.w};
+#pragma unroll
+                        for (int e = 0; e < 4; ++e)
+#pragma unroll
+                            for (int o = 0; o < COB; ++o) acc[o] = fmaf(v[e], wr[(4 * q + e) * CoutP + o], acc[o]);
+                    }
+                } else {
+                    for (int c = 0; c < cn; ++c)
+#pragma unroll
+                        for (int o = 0; o < COB; ++o) acc[o] = fmaf(sp[c], wr[c * CoutP + o], acc[o]);
+                }
+            }
         }
     }
-#pragma unroll
-    for (int o = 0; o < COB; ++o)
-        if (og + o < Cout) store_elem(op + o, activate(act, acc[o]));
+    if (active) store_outputs<Tout, COB>(out, ((int64_t)f * Hout + y) * Wout + x, Cout, og, act, acc);
+}
+
+// Tile of the narrow kernel: the width (16 .. 256, a power of two) that computes
+// the fewest masked samples among those whose halo fits 64 KB of LDS and the
+// staging registers; TH = 0 if none does.
+static void narrow_tile(int Hout, int Wout, int fh, int fw, int dh, int dw, int kc, int units_per_sample, int& TH,
+                        int& TW, size_t& lds) {
+    TH = TW = 0;
+    int64_t best = -1;
+    for (int tw = 16; tw <= 256; tw *= 2) {
+        const int th = 256 / tw;
+        const int64_t samples = (int64_t)(th + dh * (fh - 1)) * (tw + dw * (fw - 1));
+        const size_t l = (size_t)samples * (kc + 4) * sizeof(float);
+        if (l > 64 * 1024 || samples * units_per_sample > 256 * kNMaxUnits) continue;
+        const int64_t work = ceil_div64(Hout, th) * th * ceil_div64(Wout, tw) * tw;
+        if (best < 0 || work < best) {
+            best = work;
+            TH = th;
+            TW = tw;
+            lds = l;
+        }
+    }
 }
 
 template <typename Tin, typename Tout, int COB>
 static void run_direct(const void* in, int F, int Hin, int Win, int dh, int dw, int Cin, const PlanConv& pc, void* out,
                        hipStream_t s) {
     const int Hout = Hin - dh * (pc.fh - 1), Wout = Win - dw * (pc.fw - 1);
+    const int kc = pc.fh * pc.fw == 1 ? 32 : 16;
+    if (Cin >= 16 && pc.cout_pad <= 8) {
+        int TH, TW;
+        size_t lds = 0;
+        narrow_tile(Hout, Wout, pc.fh, pc.fw, dh, dw, kc, kc / (16 / (int)sizeof(Tin)), TH, TW, lds);
+        const int tilesY = (int)ceil_div64(Hout, TH > 0 ? TH : 1), tilesX = (int)ceil_div64(Wout, TW > 0 ? TW : 1);
+        if (TH > 0 && (int64_t)F * tilesY * tilesX < (1ll << 31)) {
+            const dim3 grid((unsigned)((int64_t)F * tilesY * tilesX), (unsigned)(pc.cout_pad / COB));
+            auto kern = kc == 32 ? conv_narrow_kernel<Tin, Tout, COB, 32> : conv_narrow_kernel<Tin, Tout, COB, 16>;
+            kern<<<grid, 256, lds, s>>>((const Tin*)in, Hin, Win, Cin, (const float*)pc.w, pc.b, pc.fh, pc.fw, dh, dw,
+                                        pc.cout, pc.cout_pad, pc.act, (Tout*)out, Hout, Wout, TH, TW, tilesY, tilesX);
+            return;
+        }
+    }
     const int64_t npix = (int64_t)F * Hout * Wout;
     const dim3 grid((unsigned)ceil_div64(npix, 256), (unsigned)(pc.cout_pad / COB));
     const int vec_ok = (Cin % 4 == 0);

@@ -324,6 +324,8 @@ def test_timing_records():
     # the 128-channel layer runs the 64-channel tile here: at this size the 128-channel
     # tile would give too few workgroups to fill the GPU
     assert "conv_mfma_f32_n64" in names and "conv_mfma_f32_n32" in names and "pool_frag" in names
+    # the final 1x1 projection to 2 channels runs the LDS-staged direct kernel
+    assert names[-2] == "conv_narrow"
     g = plan.geometry(120, 130)
     assert sum(r["flops"] for r in recs) == pytest.approx(g["conv_flops"], rel=1e-9)
     assert all(r["ms"] >= 0 for r in recs)
