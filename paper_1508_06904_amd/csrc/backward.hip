@@ -19,8 +19,10 @@
 //                      strided network's max-pool gradient uses too.
 //  act_backward        dy = g * act'(a) for a convolution without a pool.
 //  pad_grad            zero border of fh-1 x fw-1 around every fragment: the input
-//                      gradient is then a valid convolution with the transposed,
-//                      flipped filters (the forward convolution kernels run it).
+//                      gradient is a valid convolution of the bordered gradient
+//                      with the transposed, flipped filters.  The MFMA convolution
+//                      reads the border virtually; this copy feeds the direct
+//                      kernel (input gradients into few channels).
 //  wgrad_mfma          dW[o][i][t] = sum_p dy[p][o] x[p + t][i]: per tap a GEMM
 //                      over all output positions p of all fragments (MFMA
 //                      32x32x2 binary32); a workgroup takes the taps of one

@@ -16,10 +16,18 @@
 // K loop: input channels in chunks of 64 bytes per sample (16 binary32 or 32
 // bfloat16 channels) x filter taps.  For each chunk the input halo tile
 // (TH + fh - 1) x (TW + fw - 1) x chunk is staged in LDS once and reused by all
-// fh * fw taps; the weight slice of one (chunk, tap) pair, BN x chunk, is
-// double-buffered in LDS while the previous slice feeds the MFMAs.  Sample and
-// weight rows use an 80-byte LDS pitch so that the 32-byte operand reads of a
-// wavefront spread over all banks.
+// fh * fw taps (double-buffered across chunks when two workgroups still fit a
+// CU).  The weight slice of one (chunk, tap) pair, BN x chunk: binary32 stages it
+// double-buffered in LDS (a step is 64 MFMA issues, long enough to hide the copy
+// and its barrier); bfloat16, whose steps are 8x shorter, loads each lane's B
+// operands from global memory straight into registers one step ahead, with one
+// barrier per chunk.  Sample and weight rows use an 80-byte LDS pitch so that
+// the 32-byte operand reads of a wavefront spread over all banks.
+//
+// Spatial tiles may read a virtual zero border of pad_h x pad_w samples around
+// every fragment (the input gradient of the backward pass); small fragments can
+// instead be read as one flat sequence, and the dilated fashion tiles one signal
+// by phase (see the kernel's parameters).
 //
 // K-index assignment inside one MFMA issue: lane half h (lanes 32h..32h+31)
 // holds input channels h*8 + s (binary32, issue s of 8) or h*16 + 8s .. +7
@@ -27,7 +35,8 @@
 // every product pairs an input sample with its own weight.
 //
 // Epilogue: + bias, activation, masked store (edge tiles, padded channels) in
-// the channels-last output layout; binary32 or bfloat16 (round to nearest even).
+// the channels-last output layout; binary32, or bfloat16 (round to nearest even)
+// transposed through LDS into 16-byte stores of 8 channels.
 #include <algorithm>
 
 #include <mutex>
