@@ -301,8 +301,12 @@ dss_status dss_eval_dilate(dss_plan_t plan, const void* signal, int32_t H, int32
  * algorithmic convolution flops (forward + weight gradient + input gradient) of
  * dss_backward_dense on an H x W signal, for a layer list (host only) or a plan.
  * with_signal_grad: nonzero if the gradient with respect to the signal is wanted
- * (it adds the first layer's input-gradient convolution).  Output pointers may be
- * NULL.  Errors as dss_chain_geometry. */
+ * (it adds the first layer's input-gradient convolution).  The workspace
+ * depends on the kernels chosen for the input gradients (a zero-bordered copy
+ * of the gradient only for those that run on the direct kernel): the plan form
+ * is exact for its plan, the layer-list form assumes the choice a plan created
+ * at the same time would make.  Output pointers may be NULL.  Errors as
+ * dss_chain_geometry. */
 dss_status dss_chain_backward_geometry(const dss_layer* layers, int32_t n_layers, int32_t ndim,
                                        int32_t in_channels, int32_t H, int32_t W,
                                        int32_t with_signal_grad, int64_t* workspace_bytes,
