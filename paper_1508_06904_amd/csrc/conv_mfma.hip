@@ -20,7 +20,7 @@
 // CU).  The weight slice of one (chunk, tap) pair, BN x chunk: binary32 stages it
 // double-buffered in LDS (a step is 64 MFMA issues, long enough to hide the copy
 // and its barrier); bfloat16, whose steps are 8x shorter, loads each lane's B
-// operands from global memory straight into registers one step ahead, with one
+// operands from global memory straight into registers two steps ahead, with one
 // barrier per chunk.  Sample and weight rows use an 80-byte LDS pitch so that
 // the 32-byte operand reads of a wavefront spread over all banks.
 //
@@ -57,6 +57,7 @@ constexpr int kChunkBytes = 64;     // bytes of one channel chunk per sample
 constexpr int kMaxLds = 78 * 1024;  // two workgroups per CU (160 KB of LDS)
 constexpr int kXcds = 8;            // accelerator complex dies of an MI355X
 constexpr int kGroup = 16;          // neighbouring tiles scheduled together
+constexpr int kBf16Block = 2048;    // bytes of 32 weight rows x 32 bfloat16 channels
 
 template <bool BF16, int WGM, int WGN, int MT, int NT>
 struct MfmaCfg {
@@ -86,7 +87,7 @@ template <bool BF16, typename Tout, int WGM, int WGN, int MT, int NT>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void conv_mfma_kernel(
     const char* __restrict__ in,       // [F][Hin][Win][Cin] of BF16 ? bfloat16 : binary32
     int Hin, int Win, int Cin,
-    const char* __restrict__ wp,       // packed [nb][chunk][th][tw][BN][chunk channels]
+    const char* __restrict__ wp,       // packed [nb][chunk][th][tw][BN][chunk channels] (bfloat16: slices in lane order)
     const float* __restrict__ bias,    // [Cout_pad]
     int fh, int fw, int Cout, int act, int nchunks,
     Tout* __restrict__ out,            // [F][Hout][Wout][Cout]
@@ -227,66 +228,120 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
     if constexpr (BF16) {
         // Operand B comes straight from the packed weights in global memory
         // (every workgroup of the N block reads the same slices, which stay in
-        // L2) into registers, one step ahead: no LDS slice and no barrier per
+        // L2) into registers, two steps ahead: no LDS slice and no barrier per
         // step, only one per chunk for the halo.  Lane (n, half) of MFMA s holds
-        // bytes 32 half + 16 s of row n of a slice, as the halo reads of A do.
-        const char* w_lane = w_nb + (size_t)(wn * 32 * NT + l32) * kChunkBytes + half * 32;
+        // bytes 32 half + 16 s of row n of a slice, as the halo reads of A do; the
+        // slices are packed in lane order (see mfma_bf16_pack), so each load
+        // instruction reads one contiguous kilobyte.
+        const char* w_lane = w_nb + (size_t)(wn * NT) * kBf16Block + lane * 16;
         auto load_b = [&](int st, u32x4 (&bb)[NT][2]) {
             const char* src = w_lane + (size_t)st * (Cfg::BN * kChunkBytes);
 #pragma unroll
             for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
                 for (int s = 0; s < 2; ++s)
-                    bb[nt][s] = *reinterpret_cast<const u32x4*>(src + nt * 32 * kChunkBytes + s * 16);
+                    bb[nt][s] = *reinterpret_cast<const u32x4*>(src + nt * kBf16Block + s * (kBf16Block / 2));
         };
-        u32x4 bq[NT][2];
-        load_b(0, bq);
+        // One step: this tap's A operands from the halo, then 16 MFMAs with the B
+        // operands bb.  The compiler interleaves the reads with the MFMAs; issuing
+        // all eight reads ahead of the first MFMA measured 5 % slower.
+        auto mma_step = [&](const char* halo, int tap_off, const u32x4 (&bb)[NT][2]) {
+            u32x4 a[2][MT];
+#pragma unroll
+            for (int s = 0; s < 2; ++s)
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt)
+                    a[s][mt] = *reinterpret_cast<const u32x4*>(halo + a_off[mt] + tap_off + 16 * s);
+#pragma unroll
+            for (int s = 0; s < 2; ++s)
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+                    for (int nt = 0; nt < NT; ++nt)
+                        acc[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                            as_bf16x8(a[s][mt]), as_bf16x8(bb[nt][s]), acc[mt][nt], 0, 0, 0);
+        };
+        // The next chunk's halo is staged by the same copies as stage_halo, but
+        // issued as inline assembly.  To the compiler, LDS-DMA completes out of
+        // order with ordinary loads, so with one in flight that it knows of,
+        // every wait for a B operand would become a wait for all loads; unseen,
+        // they leave those waits partial.  The hardware counts them in issue order
+        // with the B loads (a partial wait that the compiler computes without
+        // them still covers its own loads), and the full wait before the chunk's
+        // closing barrier drains them.  M0 (the LDS destination) is saved and
+        // restored around each copy.
+        const uint32_t lds_base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)lds;
+        auto stage_halo_unseen = [&](int cn, char* dst) {
+            const char* src_c = in_f + (size_t)cn * kChunkBytes;
+            const int c_base = cn * Cfg::CC;
+            const uint32_t dst_lds = lds_base + (uint32_t)(dst - lds);
+            for (int r0 = 0; r0 < halo_slots; r0 += THREADS) {
+                const int S = r0 + tid;
+                const int px = S / kSlotsPerRow, q = S - px * kSlotsPerRow;
+                if (S < halo_slots && q < 4) {
+                    const int dy = px / HW, dx = px - dy * HW;
+                    const int yy = hy0 + dy, xx = hx0 + dx;
+                    const bool ok = (unsigned)yy < (unsigned)lim_h && (unsigned)xx < (unsigned)lim_w &&
+                                    c_base + q * (16 / Cfg::ES) < Cin;
+                    const char* src = ok ? src_c + (size_t)yy * row_step + (size_t)xx * col_step + q * 16 : zero;
+                    const uint32_t m0v = __builtin_amdgcn_readfirstlane(dst_lds + (uint32_t)(r0 + wave * 64) * 16);
+                    uint32_t saved;
+                    asm volatile(
+                        "s_mov_b32 %0, m0\n\t"
+                        "s_mov_b32 m0, %2\n\t"
+                        "s_nop 0\n\t"
+                        "global_load_lds_dwordx4 %1, off\n\t"
+                        "s_mov_b32 m0, %0"
+                        : "=&s"(saved)
+                        : "v"(src), "s"(m0v)
+                        : "memory");
+                }
+            }
+        };
+        // B operands two steps ahead in three register sets whose roles rotate
+        // with the step, over all steps of all chunks in threes, so no register
+        // copy waits for a load (the loads past the last step repeat the last
+        // slice).  A chunk ends inside the rotation: its closing drain and barrier
+        // leave the next chunk's halo in place, and the copies of the one after
+        // it go out.
+        u32x4 bA[NT][2], bB[NT][2], bC[NT][2];
+        load_b(0, bA);
+        load_b(min(1, steps - 1), bB);
         stage_halo(0, halo0);
         wait_staged();
-        int step = 0;
-        for (int cc = 0; cc < nchunks; ++cc) {
-            const char* halo = (cc & 1) ? halo1 : halo0;
-            const bool next_chunk = cc + 1 < nchunks;
-            // the next chunk's halo goes to the other buffer (last read by chunk
-            // cc - 1, which ended with a barrier) while this chunk's taps run
-            if (dbl_halo && next_chunk) stage_halo(cc + 1, (cc & 1) ? halo0 : halo1);
-            for (int th = 0; th < fh; ++th) {
-                for (int tw = 0; tw < fw; ++tw, ++step) {
-                    const bool has_next = step + 1 < steps;
-                    u32x4 bnext[NT][2];
-                    if (has_next) load_b(step + 1, bnext);
-                    const int tap_off = (th * tap_row + tw) * kPitchBytes;
-                    u32x4 a[MT][2];
-#pragma unroll
-                    for (int mt = 0; mt < MT; ++mt) {
-                        a[mt][0] = *reinterpret_cast<const u32x4*>(halo + a_off[mt] + tap_off);
-                        a[mt][1] = *reinterpret_cast<const u32x4*>(halo + a_off[mt] + tap_off + 16);
-                    }
-#pragma unroll
-                    for (int s = 0; s < 2; ++s)
-#pragma unroll
-                        for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-                            for (int nt = 0; nt < NT; ++nt)
-                                acc[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                                    as_bf16x8(a[mt][s]), as_bf16x8(bq[nt][s]), acc[mt][nt], 0, 0, 0);
-                    if (has_next) {
-#pragma unroll
-                        for (int nt = 0; nt < NT; ++nt) {
-                            bq[nt][0] = bnext[nt][0];
-                            bq[nt][1] = bnext[nt][1];
-                        }
-                    }
+        if (dbl_halo && nchunks > 1) stage_halo_unseen(1, halo1);
+        int step = 0, cc = 0, th = 0, tw = 0;   // step, chunk and tap of the next step
+        const char* halo = halo0;
+        auto next_chunk = [&]() {
+            if (++cc >= nchunks) return;
+            if (!dbl_halo) {
+                __syncthreads();               // every wave is done with the previous chunk's halo
+                stage_halo(cc, halo0);
+            }
+            wait_staged();                     // chunk cc's halo has landed, for every wave
+            halo = (cc & 1) ? halo1 : halo0;
+            // chunk cc + 1 goes to the buffer of chunk cc - 1, which every wave is done with
+            if (dbl_halo && cc + 1 < nchunks) stage_halo_unseen(cc + 1, (cc & 1) ? halo0 : halo1);
+        };
+        auto sub_step = [&](const u32x4 (&bb)[NT][2], u32x4 (&bl)[NT][2]) {
+            load_b(min(step + 2, steps - 1), bl);
+            mma_step(halo, (th * tap_row + tw) * kPitchBytes, bb);
+            ++step;
+            if (++tw == fw) {
+                tw = 0;
+                if (++th == fh) {
+                    th = 0;
+                    next_chunk();
                 }
             }
-            if (next_chunk) {
-                if (!dbl_halo) {
-                    __syncthreads();           // every wave is done with this chunk's halo
-                    stage_halo(cc + 1, halo0);
-                }
-                wait_staged();                 // the next chunk's halo has landed for every wave
-            }
+        };
+        while (step + 2 < steps) {
+            sub_step(bA, bC);
+            sub_step(bB, bA);
+            sub_step(bC, bB);
         }
+        if (step < steps) sub_step(bA, bC);
+        if (step < steps) sub_step(bB, bA);
     } else {
         // -- prologue: chunk 0 halo and the first weight slice
         stage_halo(0, halo0);
@@ -481,8 +536,29 @@ static void pack_weights(const PlanConv& pc, int cc, const float* w, E* dst, Con
 void mfma_f32_pack(const PlanConv& pc, const float* w, float* dst) {
     pack_weights(pc, 16, w, dst, [](float v) { return v; });
 }
+// bfloat16: the same slices, each in the order the kernel's lanes load them.
+// Row n = 32 g + r and channel c = 16 half + 8 s + e of a slice go to element
+// ((2 g + s) * 64 + 32 half + r) * 8 + e: the 16-byte operand of lane
+// 32 half + r for MFMA s of 32-row block g, so the 64 lanes of one load read
+// 1 KB of consecutive bytes.
 void mfma_bf16_pack(const PlanConv& pc, const float* w, uint16_t* dst) {
-    pack_weights(pc, 32, w, dst, [](float v) { return host_f32_to_bf16(v); });
+    constexpr int cc = 32;
+    static_assert(cc * 2 == kChunkBytes && 32 * cc * 2 == kBf16Block, "bfloat16 slice layout");
+    const int nbs = pc.cout_pad / pc.bn, nch = pc.cin_pad / cc;
+    const size_t slice = (size_t)pc.bn * cc;
+    size_t base = 0;
+    for (int nb = 0; nb < nbs; ++nb)
+        for (int ch = 0; ch < nch; ++ch)
+            for (int th = 0; th < pc.fh; ++th)
+                for (int tw = 0; tw < pc.fw; ++tw, base += slice)
+                    for (int nl = 0; nl < pc.bn; ++nl)
+                        for (int cl = 0; cl < cc; ++cl) {
+                            const int o = nb * pc.bn + nl, i = ch * cc + cl;
+                            float v = 0.f;
+                            if (o < pc.cout && i < pc.cin) v = w[(((size_t)o * pc.cin + i) * pc.fh + th) * pc.fw + tw];
+                            const int g = nl / 32, r = nl % 32, hf = cl / 16, s = (cl / 8) % 2, e = cl % 8;
+                            dst[base + ((size_t)(2 * g + s) * 64 + 32 * hf + r) * 8 + e] = host_f32_to_bf16(v);
+                        }
 }
 
 struct Tile {
