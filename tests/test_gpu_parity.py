@@ -169,6 +169,25 @@ def test_random_chain_bf16(name):
     assert_close(out, ref, BF16_TOL, name)
 
 
+# The bfloat16 kernel runs its steps (input-channel chunk x filter tap) in
+# threes over rotating operand registers, with a chunk change inside the
+# rotation: step counts of every residue mod 3, one to three chunks, the single-
+# buffered halo of a 7x7 filter, and small pooled fragments (flat tiles).
+BF16_STEP_CASES = [(cin, f, pool) for cin in (24, 40, 80) for f in (1, 2, 5, 7) for pool in (False,)] + \
+                  [(40, 6, False), (40, 3, True), (80, 5, True), (24, 1, True)]
+
+
+@pytest.mark.parametrize("cin,f,pool", BF16_STEP_CASES)
+def test_bf16_step_rotation(cin, f, pool):
+    arch = ([("pool", 2, 2)] if pool else []) + [("conv", cin, 136, f, f, "relu")]
+    H, W = (2 * f + 23, 2 * f + 37) if pool else (f + 29, f + 70)
+    w = wl.custom(arch, cin, H, W, seed=cin + f, dtype="bf16")
+    log("bf16 conv %dx%d cin=%d pool=%s on %s" % (f, f, cin, pool, w.x.shape))
+    out, _ = gpu_dense(w.layers, w.x, 2, "bf16")
+    ref = oracle.eval_stride(oracle_layers(w.layers, "bf16"), w.x)
+    assert_close(out, ref, BF16_TOL, "bf16 %dx%d cin=%d" % (f, f, cin))
+
+
 def test_direct_and_mfma_agree(direct_conv):
     """Both convolution kernels on the same chain agree to rounding."""
     arch, C, nd = CHAINS["2d_mfma_mixed"]
