@@ -75,8 +75,8 @@ static ConvImpl choose_impl(int cin, int cout, int fh, int fw, dss_dtype dt) {
     // LDS-staged direct kernel streams them faster; with bfloat16 inputs the
     // MFMA tile still wins)
     if (cin < 16 || (cout <= 8 && dt == DSS_F32)) return CONV_DIRECT;
-    if (dt == DSS_F32 && cin % 4 == 0 && mfma_supports(false, cout, fh, fw)) return CONV_MFMA_F32;
-    if (dt == DSS_BF16 && cin % 8 == 0 && mfma_supports(true, cout, fh, fw)) return CONV_MFMA_BF16;
+    if (dt == DSS_F32 && cin % 4 == 0 && mfma_supports(false, fh, fw)) return CONV_MFMA_F32;
+    if (dt == DSS_BF16 && cin % 8 == 0 && mfma_supports(true, fh, fw)) return CONV_MFMA_BF16;
     return CONV_DIRECT;
 }
 

@@ -8,21 +8,19 @@
 // workgroup), N = output channels, K = fh * fw * Cin.
 //
 // Workgroup = 4 wavefronts of 64 lanes; each wave owns a (32*MT) x (32*NT) block
-// of the output tile (128 x 64 for the wide layers: per MFMA K step a lane reads
-// 16 bytes of A per 32 rows and of B per 32 columns from LDS, so the wider the
-// wave tile the fewer LDS bytes per flop), computed with 32x32 MFMA tiles:
+// of the output tile (128 x 64 for the wide layers: the wider the wave tile, the
+// fewer operand bytes per flop), computed with 32x32 MFMA tiles:
 //   binary32:  v_mfma_f32_32x32x2_f32   (K = 2 per issue)
 //   bfloat16:  v_mfma_f32_32x32x16_bf16 (K = 16 per issue), binary32 accumulation
 // K loop: input channels in chunks of 64 bytes per sample (16 binary32 or 32
-// bfloat16 channels) x filter taps.  For each chunk the input halo tile
-// (TH + fh - 1) x (TW + fw - 1) x chunk is staged in LDS once and reused by all
-// fh * fw taps (double-buffered across chunks when two workgroups still fit a
-// CU).  The weight slice of one (chunk, tap) pair, BN x chunk: binary32 stages it
-// double-buffered in LDS (a step is 64 MFMA issues, long enough to hide the copy
-// and its barrier); bfloat16, whose steps are 8x shorter, loads each lane's B
-// operands from global memory straight into registers two steps ahead, with one
-// barrier per chunk.  Sample and weight rows use an 80-byte LDS pitch so that
-// the 32-byte operand reads of a wavefront spread over all banks.
+// bfloat16 channels) x filter taps; a step is one (chunk, tap) pair.  For each
+// chunk the input halo tile (TH + fh - 1) x (TW + fw - 1) x chunk is staged in
+// LDS once and read by all fh * fw taps (A operands; double-buffered across
+// chunks when two workgroups still fit a CU).  The weights of a step, BN x
+// chunk, go from global memory (L2-resident: every workgroup of an N block reads
+// the same slices) straight into each lane's B registers two steps ahead: no
+// LDS copy, one barrier per chunk.  Halo samples use an 80-byte LDS pitch so
+// that the 32-byte operand reads of a wavefront spread over all banks.
 //
 // Spatial tiles may read a virtual zero border of pad_h x pad_w samples around
 // every fragment (the input gradient of the backward pass); small fragments can
@@ -57,7 +55,7 @@ constexpr int kChunkBytes = 64;     // bytes of one channel chunk per sample
 constexpr int kMaxLds = 78 * 1024;  // two workgroups per CU (160 KB of LDS)
 constexpr int kXcds = 8;            // accelerator complex dies of an MI355X
 constexpr int kGroup = 16;          // neighbouring tiles scheduled together
-constexpr int kBf16Block = 2048;    // bytes of 32 weight rows x 32 bfloat16 channels
+constexpr int kSliceBlock = 2048;   // bytes of 32 weight rows x one 64-byte channel chunk
 
 template <bool BF16, int WGM, int WGN, int MT, int NT>
 struct MfmaCfg {
@@ -66,7 +64,6 @@ struct MfmaCfg {
     static constexpr int BM = 32 * MT * WGM;            // output samples per workgroup
     static constexpr int BN = 32 * NT * WGN;            // output channels per workgroup
     static constexpr int THREADS = 64 * WGM * WGN;
-    static constexpr int WSLOTS = BN * kSlotsPerRow;    // 16-byte LDS slots of one weight slice
 };
 
 // 16 zero bytes: the source of every staged unit that lies outside the fragment
@@ -97,7 +94,6 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
     int pad_h, int pad_w) {             // spatial tiles: a zero border of pad samples around every fragment
     using Cfg = MfmaCfg<BF16, WGM, WGN, MT, NT>;
     constexpr int THREADS = Cfg::THREADS;
-    constexpr int WSLOTS = Cfg::WSLOTS;
     extern __shared__ __attribute__((aligned(16))) char lds[];
 
     const int tid = threadIdx.x;
@@ -142,8 +138,6 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
     const int halo_bytes = ((halo_px * kPitchBytes + 127) / 128) * 128;
     char* halo0 = lds;
     char* halo1 = dbl_halo ? lds + halo_bytes : lds;
-    char* wbuf0 = lds + (dbl_halo ? 2 : 1) * halo_bytes;
-    char* wbuf1 = wbuf0 + Cfg::BN * kPitchBytes;
 
     // per-lane operand offsets (bytes) inside the halo / weight slice
     int a_off[MT];
@@ -152,9 +146,6 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
         const int m = wm * 32 * MT + mt * 32 + l32;
         a_off[mt] = ((m / TW) * HW + (m % TW)) * kPitchBytes + half * 32;
     }
-    int b_off[NT];
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt) b_off[nt] = (wn * 32 * NT + nt * 32 + l32) * kPitchBytes + half * 32;
 
     floatx16 acc[MT][NT];
 #pragma unroll
@@ -186,18 +177,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
 
     // Staging: LDS slot S (16 bytes) of the halo holds quad S % 5 of halo sample
     // S / 5 (slot 4 of every sample is padding and is never written); lane l of
-    // wave w stages slot r * THREADS + w * 64 + l in round r.  Weight slots map to
-    // the same source offsets in every step, so they are computed once (kPad: a
-    // padding slot, nothing to stage); the halo mapping is recomputed per chunk.
-    constexpr int kPad = -1;
-    constexpr int kWRounds = (WSLOTS + THREADS - 1) / THREADS;
-    int w_off[kWRounds];
-#pragma unroll
-    for (int r = 0; r < kWRounds; ++r) {
-        const int S = r * THREADS + tid;
-        const int n = S / kSlotsPerRow, q = S - n * kSlotsPerRow;
-        w_off[r] = (S >= WSLOTS || q == 4) ? kPad : n * kChunkBytes + q * 16;
-    }
+    // wave w stages slot r * THREADS + w * 64 + l in round r.
     auto stage_halo = [&](int cc, char* dst) {
         const char* src_c = in_f + (size_t)cc * kChunkBytes;
         const int c_base = cc * Cfg::CC;
@@ -214,44 +194,39 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
             }
         }
     };
-    auto stage_w = [&](int st, char* dst) {
-        const char* src = w_nb + (size_t)st * (Cfg::BN * kChunkBytes);
-#pragma unroll
-        for (int r = 0; r < kWRounds; ++r)
-            if (w_off[r] != kPad) dma16(src + w_off[r], dst + (r * THREADS + wave * 64) * 16);
-    };
     auto wait_staged = [] {
         __builtin_amdgcn_s_waitcnt(0);   // this wave's copies have landed in LDS
         __syncthreads();                 // ... and every other wave's
     };
 
-    if constexpr (BF16) {
-        // Operand B comes straight from the packed weights in global memory
-        // (every workgroup of the N block reads the same slices, which stay in
-        // L2) into registers, two steps ahead: no LDS slice and no barrier per
-        // step, only one per chunk for the halo.  Lane (n, half) of MFMA s holds
-        // bytes 32 half + 16 s of row n of a slice, as the halo reads of A do; the
-        // slices are packed in lane order (see mfma_bf16_pack), so each load
-        // instruction reads one contiguous kilobyte.
-        const char* w_lane = w_nb + (size_t)(wn * NT) * kBf16Block + lane * 16;
-        auto load_b = [&](int st, u32x4 (&bb)[NT][2]) {
-            const char* src = w_lane + (size_t)st * (Cfg::BN * kChunkBytes);
+    // Operand B comes straight from the packed weights in global memory
+    // (every workgroup of the N block reads the same slices, which stay in
+    // L2) into registers, two steps ahead: no LDS slice and no barrier per
+    // step, only one per chunk for the halo.  Lane (n, half) holds bytes
+    // 32 half .. 32 half + 31 of row n of a slice (two 16-byte loads), as its
+    // halo reads of A do; the slices are packed in lane order (see
+    // pack_lane_order), so each load instruction reads one contiguous kilobyte.
+    const char* w_lane = w_nb + (size_t)(wn * NT) * kSliceBlock + lane * 16;
+    auto load_b = [&](int st, u32x4 (&bb)[NT][2]) {
+        const char* src = w_lane + (size_t)st * (Cfg::BN * kChunkBytes);
 #pragma unroll
-            for (int nt = 0; nt < NT; ++nt)
-#pragma unroll
-                for (int s = 0; s < 2; ++s)
-                    bb[nt][s] = *reinterpret_cast<const u32x4*>(src + nt * kBf16Block + s * (kBf16Block / 2));
-        };
-        // One step: this tap's A operands from the halo, then 16 MFMAs with the B
-        // operands bb.  The compiler interleaves the reads with the MFMAs; issuing
-        // all eight reads ahead of the first MFMA measured 5 % slower.
-        auto mma_step = [&](const char* halo, int tap_off, const u32x4 (&bb)[NT][2]) {
-            u32x4 a[2][MT];
+        for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
             for (int s = 0; s < 2; ++s)
+                bb[nt][s] = *reinterpret_cast<const u32x4*>(src + nt * kSliceBlock + s * (kSliceBlock / 2));
+    };
+    // One step: this tap's A operands from the halo, then the step's MFMAs with
+    // the B operands bb (per wave 16 bfloat16 or 64 binary32 issues).  The
+    // compiler interleaves the reads with the MFMAs; issuing all eight reads
+    // ahead of the first MFMA measured 5 % slower (bfloat16).
+    auto mma_step = [&](const char* halo, int tap_off, const u32x4 (&bb)[NT][2]) {
+        u32x4 a[2][MT];
 #pragma unroll
-                for (int mt = 0; mt < MT; ++mt)
-                    a[s][mt] = *reinterpret_cast<const u32x4*>(halo + a_off[mt] + tap_off + 16 * s);
+        for (int s = 0; s < 2; ++s)
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt)
+                a[s][mt] = *reinterpret_cast<const u32x4*>(halo + a_off[mt] + tap_off + 16 * s);
+        if constexpr (BF16) {
 #pragma unroll
             for (int s = 0; s < 2; ++s)
 #pragma unroll
@@ -260,154 +235,99 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
                     for (int nt = 0; nt < NT; ++nt)
                         acc[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
                             as_bf16x8(a[s][mt]), as_bf16x8(bb[nt][s]), acc[mt][nt], 0, 0, 0);
-        };
-        // The next chunk's halo is staged by the same copies as stage_halo, but
-        // issued as inline assembly.  To the compiler, LDS-DMA completes out of
-        // order with ordinary loads, so with one in flight that it knows of,
-        // every wait for a B operand would become a wait for all loads; unseen,
-        // they leave those waits partial.  The hardware counts them in issue order
-        // with the B loads (a partial wait that the compiler computes without
-        // them still covers its own loads), and the full wait before the chunk's
-        // closing barrier drains them.  M0 (the LDS destination) is saved and
-        // restored around each copy.
-        const uint32_t lds_base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)lds;
-        auto stage_halo_unseen = [&](int cn, char* dst) {
-            const char* src_c = in_f + (size_t)cn * kChunkBytes;
-            const int c_base = cn * Cfg::CC;
-            const uint32_t dst_lds = lds_base + (uint32_t)(dst - lds);
-            for (int r0 = 0; r0 < halo_slots; r0 += THREADS) {
-                const int S = r0 + tid;
-                const int px = S / kSlotsPerRow, q = S - px * kSlotsPerRow;
-                if (S < halo_slots && q < 4) {
-                    const int dy = px / HW, dx = px - dy * HW;
-                    const int yy = hy0 + dy, xx = hx0 + dx;
-                    const bool ok = (unsigned)yy < (unsigned)lim_h && (unsigned)xx < (unsigned)lim_w &&
-                                    c_base + q * (16 / Cfg::ES) < Cin;
-                    const char* src = ok ? src_c + (size_t)yy * row_step + (size_t)xx * col_step + q * 16 : zero;
-                    const uint32_t m0v = __builtin_amdgcn_readfirstlane(dst_lds + (uint32_t)(r0 + wave * 64) * 16);
-                    uint32_t saved;
-                    asm volatile(
-                        "s_mov_b32 %0, m0\n\t"
-                        "s_mov_b32 m0, %2\n\t"
-                        "s_nop 0\n\t"
-                        "global_load_lds_dwordx4 %1, off\n\t"
-                        "s_mov_b32 m0, %0"
-                        : "=&s"(saved)
-                        : "v"(src), "s"(m0v)
-                        : "memory");
-                }
-            }
-        };
-        // B operands two steps ahead in three register sets whose roles rotate
-        // with the step, over all steps of all chunks in threes, so no register
-        // copy waits for a load (the loads past the last step repeat the last
-        // slice).  A chunk ends inside the rotation: its closing drain and barrier
-        // leave the next chunk's halo in place, and the copies of the one after
-        // it go out.
-        u32x4 bA[NT][2], bB[NT][2], bC[NT][2];
-        load_b(0, bA);
-        load_b(min(1, steps - 1), bB);
-        stage_halo(0, halo0);
-        wait_staged();
-        if (dbl_halo && nchunks > 1) stage_halo_unseen(1, halo1);
-        int step = 0, cc = 0, th = 0, tw = 0;   // step, chunk and tap of the next step
-        const char* halo = halo0;
-        auto next_chunk = [&]() {
-            if (++cc >= nchunks) return;
-            if (!dbl_halo) {
-                __syncthreads();               // every wave is done with the previous chunk's halo
-                stage_halo(cc, halo0);
-            }
-            wait_staged();                     // chunk cc's halo has landed, for every wave
-            halo = (cc & 1) ? halo1 : halo0;
-            // chunk cc + 1 goes to the buffer of chunk cc - 1, which every wave is done with
-            if (dbl_halo && cc + 1 < nchunks) stage_halo_unseen(cc + 1, (cc & 1) ? halo0 : halo1);
-        };
-        auto sub_step = [&](const u32x4 (&bb)[NT][2], u32x4 (&bl)[NT][2]) {
-            load_b(min(step + 2, steps - 1), bl);
-            mma_step(halo, (th * tap_row + tw) * kPitchBytes, bb);
-            ++step;
-            if (++tw == fw) {
-                tw = 0;
-                if (++th == fh) {
-                    th = 0;
-                    next_chunk();
-                }
-            }
-        };
-        while (step + 2 < steps) {
-            sub_step(bA, bC);
-            sub_step(bB, bA);
-            sub_step(bC, bB);
+        } else {
+#pragma unroll
+            for (int s = 0; s < 8; ++s)
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+                    for (int nt = 0; nt < NT; ++nt)
+                        acc[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x2f32(
+                            __uint_as_float(a[s >> 2][mt][s & 3]), __uint_as_float(bb[nt][s >> 2][s & 3]),
+                            acc[mt][nt], 0, 0, 0);
         }
-        if (step < steps) sub_step(bA, bC);
-        if (step < steps) sub_step(bB, bA);
-    } else {
-        // -- prologue: chunk 0 halo and the first weight slice
-        stage_halo(0, halo0);
-        stage_w(0, wbuf0);
-        wait_staged();
-
-        int step = 0;
-        for (int cc = 0; cc < nchunks; ++cc) {
-            const char* halo = (cc & 1) ? halo1 : halo0;
-            for (int th = 0; th < fh; ++th) {
-                for (int tw = 0; tw < fw; ++tw, ++step) {
-                    const bool has_next = step + 1 < steps;
-                    const bool last_tap = (th == fh - 1) && (tw == fw - 1);
-                    // stage the next weight slice (its buffer was last read in the
-                    // previous step) and, with a double-buffered halo, the next chunk's
-                    // halo; the copies run while the MFMAs below execute
-                    if (has_next) {
-                        stage_w(step + 1, (step & 1) ? wbuf0 : wbuf1);
-                        if (last_tap && dbl_halo) stage_halo(cc + 1, (cc & 1) ? halo0 : halo1);
-                    }
-                    const int tap_off = (th * tap_row + tw) * kPitchBytes;
-                    const char* wcur = (step & 1) ? wbuf1 : wbuf0;
-                    u32x4 a[MT][2], b[NT][2];
-    #pragma unroll
-                    for (int mt = 0; mt < MT; ++mt) {
-                        a[mt][0] = *reinterpret_cast<const u32x4*>(halo + a_off[mt] + tap_off);
-                        a[mt][1] = *reinterpret_cast<const u32x4*>(halo + a_off[mt] + tap_off + 16);
-                    }
-    #pragma unroll
-                    for (int nt = 0; nt < NT; ++nt) {
-                        b[nt][0] = *reinterpret_cast<const u32x4*>(wcur + b_off[nt]);
-                        b[nt][1] = *reinterpret_cast<const u32x4*>(wcur + b_off[nt] + 16);
-                    }
-                    if constexpr (BF16) {
-    #pragma unroll
-                        for (int s = 0; s < 2; ++s)
-    #pragma unroll
-                            for (int mt = 0; mt < MT; ++mt)
-    #pragma unroll
-                                for (int nt = 0; nt < NT; ++nt)
-                                    acc[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                                        as_bf16x8(a[mt][s]), as_bf16x8(b[nt][s]), acc[mt][nt], 0, 0, 0);
-                    } else {
-    #pragma unroll
-                        for (int s = 0; s < 8; ++s) {
-    #pragma unroll
-                            for (int mt = 0; mt < MT; ++mt) {
-                                const uint32_t aw = a[mt][s >> 2][s & 3];
-    #pragma unroll
-                                for (int nt = 0; nt < NT; ++nt) {
-                                    const uint32_t bw = b[nt][s >> 2][s & 3];
-                                    acc[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(aw), __uint_as_float(bw),
-                                                                                      acc[mt][nt], 0, 0, 0);
-                                }
-                            }
-                        }
-                    }
-                    if (has_next && last_tap && !dbl_halo) {
-                        __syncthreads();                   // every wave is done with this chunk's halo
-                        stage_halo(cc + 1, halo0);
-                    }
-                    wait_staged();
-                }
+    };
+    // The next chunk's halo is staged by the same copies as stage_halo, but
+    // issued as inline assembly.  To the compiler, LDS-DMA completes out of
+    // order with ordinary loads, so with one in flight that it knows of,
+    // every wait for a B operand would become a wait for all loads; unseen,
+    // they leave those waits partial.  The hardware counts them in issue order
+    // with the B loads (a partial wait that the compiler computes without
+    // them still covers its own loads), and the full wait before the chunk's
+    // closing barrier drains them.  M0 (the LDS destination) is saved and
+    // restored around each copy.
+    const uint32_t lds_base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)lds;
+    auto stage_halo_unseen = [&](int cn, char* dst) {
+        const char* src_c = in_f + (size_t)cn * kChunkBytes;
+        const int c_base = cn * Cfg::CC;
+        const uint32_t dst_lds = lds_base + (uint32_t)(dst - lds);
+        for (int r0 = 0; r0 < halo_slots; r0 += THREADS) {
+            const int S = r0 + tid;
+            const int px = S / kSlotsPerRow, q = S - px * kSlotsPerRow;
+            if (S < halo_slots && q < 4) {
+                const int dy = px / HW, dx = px - dy * HW;
+                const int yy = hy0 + dy, xx = hx0 + dx;
+                const bool ok = (unsigned)yy < (unsigned)lim_h && (unsigned)xx < (unsigned)lim_w &&
+                                c_base + q * (16 / Cfg::ES) < Cin;
+                const char* src = ok ? src_c + (size_t)yy * row_step + (size_t)xx * col_step + q * 16 : zero;
+                const uint32_t m0v = __builtin_amdgcn_readfirstlane(dst_lds + (uint32_t)(r0 + wave * 64) * 16);
+                uint32_t saved;
+                asm volatile(
+                    "s_mov_b32 %0, m0\n\t"
+                    "s_mov_b32 m0, %2\n\t"
+                    "s_nop 0\n\t"
+                    "global_load_lds_dwordx4 %1, off\n\t"
+                    "s_mov_b32 m0, %0"
+                    : "=&s"(saved)
+                    : "v"(src), "s"(m0v)
+                    : "memory");
             }
         }
+    };
+    // B operands two steps ahead in three register sets whose roles rotate
+    // with the step, over all steps of all chunks in threes, so no register
+    // copy waits for a load (the loads past the last step repeat the last
+    // slice).  A chunk ends inside the rotation: its closing drain and barrier
+    // leave the next chunk's halo in place, and the copies of the one after
+    // it go out.
+    u32x4 bA[NT][2], bB[NT][2], bC[NT][2];
+    load_b(0, bA);
+    load_b(min(1, steps - 1), bB);
+    stage_halo(0, halo0);
+    wait_staged();
+    if (dbl_halo && nchunks > 1) stage_halo_unseen(1, halo1);
+    int step = 0, cc = 0, th = 0, tw = 0;   // step, chunk and tap of the next step
+    const char* halo = halo0;
+    auto next_chunk = [&]() {
+        if (++cc >= nchunks) return;
+        if (!dbl_halo) {
+            __syncthreads();               // every wave is done with the previous chunk's halo
+            stage_halo(cc, halo0);
+        }
+        wait_staged();                     // chunk cc's halo has landed, for every wave
+        halo = (cc & 1) ? halo1 : halo0;
+        // chunk cc + 1 goes to the buffer of chunk cc - 1, which every wave is done with
+        if (dbl_halo && cc + 1 < nchunks) stage_halo_unseen(cc + 1, (cc & 1) ? halo0 : halo1);
+    };
+    auto sub_step = [&](const u32x4 (&bb)[NT][2], u32x4 (&bl)[NT][2]) {
+        load_b(min(step + 2, steps - 1), bl);
+        mma_step(halo, (th * tap_row + tw) * kPitchBytes, bb);
+        ++step;
+        if (++tw == fw) {
+            tw = 0;
+            if (++th == fh) {
+                th = 0;
+                next_chunk();
+            }
+        }
+    };
+    while (step + 2 < steps) {
+        sub_step(bA, bC);
+        sub_step(bB, bA);
+        sub_step(bC, bB);
     }
+    if (step < steps) sub_step(bA, bC);
+    if (step < steps) sub_step(bB, bA);
 
     // -- epilogue: D[i][j] of a 32x32 tile sits in lane j + 32*((i/4)%2), register (i/8)*4 + i%4
     const int n_base = nb * Cfg::BN + wn * 32 * NT;
@@ -514,36 +434,15 @@ static size_t packed_elems(const PlanConv& pc, int cc) {
 size_t mfma_f32_packed_floats(const PlanConv& pc) { return packed_elems(pc, 16); }
 size_t mfma_bf16_packed_elems(const PlanConv& pc) { return packed_elems(pc, 32); }
 
-// Packed weight layout: [nb][chunk][th][tw][n in BN][c in chunk], so that the
-// slice of one (chunk, tap) pair is one contiguous BN x 64-byte block.
-template <typename E, typename Conv>
-static void pack_weights(const PlanConv& pc, int cc, const float* w, E* dst, Conv conv) {
-    const int nbs = pc.cout_pad / pc.bn, nch = pc.cin_pad / cc;
-    size_t idx = 0;
-    for (int nb = 0; nb < nbs; ++nb)
-        for (int ch = 0; ch < nch; ++ch)
-            for (int th = 0; th < pc.fh; ++th)
-                for (int tw = 0; tw < pc.fw; ++tw)
-                    for (int nl = 0; nl < pc.bn; ++nl)
-                        for (int cl = 0; cl < cc; ++cl, ++idx) {
-                            const int o = nb * pc.bn + nl, i = ch * cc + cl;
-                            float v = 0.f;
-                            if (o < pc.cout && i < pc.cin) v = w[(((size_t)o * pc.cin + i) * pc.fh + th) * pc.fw + tw];
-                            dst[idx] = conv(v);
-                        }
-}
-
-void mfma_f32_pack(const PlanConv& pc, const float* w, float* dst) {
-    pack_weights(pc, 16, w, dst, [](float v) { return v; });
-}
-// bfloat16: the same slices, each in the order the kernel's lanes load them.
-// Row n = 32 g + r and channel c = 16 half + 8 s + e of a slice go to element
-// ((2 g + s) * 64 + 32 half + r) * 8 + e: the 16-byte operand of lane
-// 32 half + r for MFMA s of 32-row block g, so the 64 lanes of one load read
+// Each slice in the order the kernel's lanes load it: row n = 32 g + r and the
+// channel at byte offset cb = 32 half + 16 s + b of the row's 64-byte chunk go to
+// byte ((2 g + s) * 64 + 32 half + r) * 16 + b, the 16-byte operand of lane
+// 32 half + r for load s of 32-row block g, so the 64 lanes of one load read
 // 1 KB of consecutive bytes.
-void mfma_bf16_pack(const PlanConv& pc, const float* w, uint16_t* dst) {
-    constexpr int cc = 32;
-    static_assert(cc * 2 == kChunkBytes && 32 * cc * 2 == kBf16Block, "bfloat16 slice layout");
+template <typename E, typename Conv>
+static void pack_lane_order(const PlanConv& pc, const float* w, E* dst, Conv conv) {
+    constexpr int cc = kChunkBytes / (int)sizeof(E);
+    static_assert(32 * kChunkBytes == kSliceBlock, "slice layout");
     const int nbs = pc.cout_pad / pc.bn, nch = pc.cin_pad / cc;
     const size_t slice = (size_t)pc.bn * cc;
     size_t base = 0;
@@ -556,9 +455,17 @@ void mfma_bf16_pack(const PlanConv& pc, const float* w, uint16_t* dst) {
                             const int o = nb * pc.bn + nl, i = ch * cc + cl;
                             float v = 0.f;
                             if (o < pc.cout && i < pc.cin) v = w[(((size_t)o * pc.cin + i) * pc.fh + th) * pc.fw + tw];
-                            const int g = nl / 32, r = nl % 32, hf = cl / 16, s = (cl / 8) % 2, e = cl % 8;
-                            dst[base + ((size_t)(2 * g + s) * 64 + 32 * hf + r) * 8 + e] = host_f32_to_bf16(v);
+                            const int g = nl / 32, r = nl % 32, cb = cl * (int)sizeof(E);
+                            const int hf = cb / 32, s = (cb / 16) % 2, b = cb % 16;
+                            dst[base + (((size_t)(2 * g + s) * 64 + 32 * hf + r) * 16 + b) / sizeof(E)] = conv(v);
                         }
+}
+
+void mfma_f32_pack(const PlanConv& pc, const float* w, float* dst) {
+    pack_lane_order(pc, w, dst, [](float v) { return v; });
+}
+void mfma_bf16_pack(const PlanConv& pc, const float* w, uint16_t* dst) {
+    pack_lane_order(pc, w, dst, [](float v) { return host_f32_to_bf16(v); });
 }
 
 struct Tile {
@@ -580,9 +487,6 @@ static size_t device_lds_limit() {
     return (size_t)cached;
 }
 
-// LDS bytes of the double-buffered weight slices: binary32 stages them in LDS,
-// bfloat16 reads its operands straight into registers.
-static size_t weight_lds_bytes(bool bf16, int BN) { return bf16 ? 0 : 2 * (size_t)BN * kPitchBytes; }
 
 // Spatial tile TH x TW = BM output samples: the shape that wastes the fewest
 // masked samples on this layer's fragment extent; among those, one whose halo can
@@ -593,7 +497,7 @@ static size_t weight_lds_bytes(bool bf16, int BN) { return bf16 ? 0 : 2 * (size_
 // such a tile's work 3 % higher (measured: 8 x 32 -> 16 x 16 tiles make the 3x3
 // layers of the 4K frame 18 % faster, while 16 x 16 tiles with 3.4 % more
 // masked work make its 6x6 layer 4.7 % slower).
-static Tile pick_tile(int BM, size_t wb, int Hout, int Wout, int fh, int fw, size_t lds_max, bool bf16) {
+static Tile pick_tile(int BM, int Hout, int Wout, int fh, int fw, size_t lds_max, bool bf16) {
     Tile best{0, 0, 0, 0};
     int64_t best_work = -1, best_halo = -1;
     for (int TW = 8; TW <= BM; TW *= 2) {
@@ -603,8 +507,8 @@ static Tile pick_tile(int BM, size_t wb, int Hout, int Wout, int fh, int fw, siz
         const size_t cap = std::min(lds_max, (size_t)kMaxLds);
         int dbl;
         size_t lds;
-        if (2 * halo_b + wb <= cap) { dbl = 1; lds = 2 * halo_b + wb; }
-        else if (halo_b + wb <= cap) { dbl = 0; lds = halo_b + wb; }
+        if (2 * halo_b <= cap) { dbl = 1; lds = 2 * halo_b; }
+        else if (halo_b <= cap) { dbl = 0; lds = halo_b; }
         else continue;
         int64_t work = ceil_div64(Hout, TH) * TH * ceil_div64(Wout, TW) * TW;
         if (bf16 && TW < 16 && (TW + fw - 1) % 16 != 8) work += work / 32;
@@ -619,12 +523,10 @@ static Tile pick_tile(int BM, size_t wb, int Hout, int Wout, int fh, int fw, siz
     return best;
 }
 
-// Whether some spatial tile of the variant chosen for `cout` fits an fh x fw
-// filter's halo into LDS (checked against the 64 KB every device offers).
-bool mfma_supports(bool bf16, int cout, int fh, int fw) {
-    const size_t wb = weight_lds_bytes(bf16, bf16 ? mfma_bf16_pick_bn(cout) : mfma_f32_pick_bn(cout));
-    return pick_tile(256, wb, 1, 1, fh, fw, 64 * 1024, bf16).TH > 0 &&
-           pick_tile(256, wb, 64, 64, fh, fw, 64 * 1024, bf16).TH > 0;
+// Whether some spatial tile fits an fh x fw filter's halo into LDS (checked
+// against the 64 KB every device offers).
+bool mfma_supports(bool bf16, int fh, int fw) {
+    return pick_tile(256, 1, 1, fh, fw, 64 * 1024, bf16).TH > 0 && pick_tile(256, 64, 64, fh, fw, 64 * 1024, bf16).TH > 0;
 }
 
 // Dynamic LDS above 64 KB needs a per-kernel opt-in (once per instantiation).
@@ -643,12 +545,12 @@ static hipError_t allow_large_lds(const void* kern, size_t lds) {
 // Flat-mode tile (TH = 1, TW = BM consecutive positions of the flattened
 // fragment batch) for fragments of Hin x Win input samples, or TH = 0 if its
 // single-row halo does not fit.
-static Tile flat_tile(int BM, size_t wb, int Win, int fh, int fw, size_t lds_max) {
+static Tile flat_tile(int BM, int Win, int fh, int fw, size_t lds_max) {
     const int64_t halo_px = BM + (int64_t)(fh - 1) * Win + fw - 1;
     const size_t halo_b = (size_t)((halo_px * kPitchBytes + 127) / 128) * 128;
     const size_t cap = std::min(lds_max, (size_t)kMaxLds);
-    if (2 * halo_b + wb <= cap) return Tile{1, BM, 2 * halo_b + wb, 1};
-    if (halo_b + wb <= cap) return Tile{1, BM, halo_b + wb, 0};
+    if (2 * halo_b <= cap) return Tile{1, BM, 2 * halo_b, 1};
+    if (halo_b <= cap) return Tile{1, BM, halo_b, 0};
     return Tile{0, 0, 0, 0};
 }
 
@@ -666,14 +568,14 @@ struct LaunchShape {
 
 // Hin x Win: the fragment extent including any zero border (which rules out the
 // flat reading, allow_flat = false).
-static LaunchShape launch_shape(int BM, bool bf16, size_t wb, int F, int Hin, int Win, int dil_h, int dil_w, int fh, int fw,
+static LaunchShape launch_shape(int BM, bool bf16, int F, int Hin, int Win, int dil_h, int dil_w, int fh, int fw,
                                 int nbs, bool allow_flat = true) {
     LaunchShape L{Tile{0, 0, 0, 0}, 0, 0, 0, 0};
     const size_t lds = device_lds_limit();
     if (dil_h * dil_w > 1) {
         const int Hout = Hin - dil_h * (fh - 1), Wout = Win - dil_w * (fw - 1);
         const int Hp = (int)ceil_div64(Hout, dil_h), Wp = (int)ceil_div64(Wout, dil_w);
-        L.t = pick_tile(BM, wb, Hp, Wp, fh, fw, lds, bf16);
+        L.t = pick_tile(BM, Hp, Wp, fh, fw, lds, bf16);
         if (L.t.TH == 0) return L;
         L.tilesY = (int)ceil_div64(Hp, L.t.TH);
         L.tilesX = (int)ceil_div64(Wp, L.t.TW);
@@ -681,10 +583,10 @@ static LaunchShape launch_shape(int BM, bool bf16, size_t wb, int F, int Hin, in
         return L;
     }
     const int Hout = Hin - fh + 1, Wout = Win - fw + 1;
-    L.t = pick_tile(BM, wb, Hout, Wout, fh, fw, lds, bf16);
+    L.t = pick_tile(BM, Hout, Wout, fh, fw, lds, bf16);
     const int64_t flat_len = (int64_t)F * Hin * Win;
     if (allow_flat && flat_len < (1ll << 30)) {
-        const Tile ft = flat_tile(BM, wb, Win, fh, fw, lds);
+        const Tile ft = flat_tile(BM, Win, fh, fw, lds);
         const int64_t work_tiles =
             L.t.TH ? (int64_t)F * ceil_div64(Hout, L.t.TH) * L.t.TH * ceil_div64(Wout, L.t.TW) * L.t.TW : -1;
         const int64_t work_flat = ceil_div64(flat_len, BM) * BM;
@@ -720,11 +622,11 @@ PlanConv mfma_launch_variant(const PlanConv& pc, int F, int Hin, int Win, int di
     const bool flat = pad_h == 0 && pad_w == 0;
     Hin += 2 * pad_h;
     Win += 2 * pad_w;
-    const LaunchShape a = launch_shape(256, bf16, weight_lds_bytes(bf16, pc.bn), F, Hin, Win, dil_h, dil_w, pc.fh, pc.fw,
+    const LaunchShape a = launch_shape(256, bf16, F, Hin, Win, dil_h, dil_w, pc.fh, pc.fw,
                                        pc.cout_pad / pc.bn, flat);
     if (a.nblocks == 0 || a.nblocks >= 512) return pc;
     const LaunchShape b =
-        launch_shape(256, bf16, weight_lds_bytes(bf16, pc.bn_alt), F, Hin, Win, dil_h, dil_w, pc.fh, pc.fw,
+        launch_shape(256, bf16, F, Hin, Win, dil_h, dil_w, pc.fh, pc.fw,
                      pc.cout_pad_alt / pc.bn_alt, flat);
     if (b.nblocks == 0) return pc;
     if (a.nblocks > 256 && 11 * ceil_div64(b.nblocks, 256) >= 20 * ceil_div64(a.nblocks, 256)) return pc;
@@ -744,7 +646,7 @@ static hipError_t run_mfma(const void* in, int F, int Hin, int Win, int dil_h, i
     if (dilated && F != 1) return hipErrorInvalidValue;   // dilated: one signal, tiled per phase
     if (padded && (dilated || pad_h < 0 || pad_w < 0)) return hipErrorInvalidValue;
     const int nbs = pc.cout_pad / Cfg::BN;
-    const LaunchShape L = launch_shape(Cfg::BM, BF16, weight_lds_bytes(BF16, Cfg::BN), F, Hin + 2 * pad_h,
+    const LaunchShape L = launch_shape(Cfg::BM, BF16, F, Hin + 2 * pad_h,
                                        Win + 2 * pad_w, dil_h, dil_w, pc.fh, pc.fw, nbs, !padded);
     if (L.nblocks == 0) return hipErrorInvalidConfiguration;
     if (L.nblocks >= (1ll << 31)) return hipErrorInvalidConfiguration;

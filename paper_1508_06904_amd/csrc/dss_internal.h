@@ -178,7 +178,7 @@ hipError_t launch_wgrad(const float* dy, const float* x, int F, int E_h, int E_w
 hipError_t launch_crop_to_planar(const float* in, int D_w, int C, int H, int W, float* out, hipStream_t s);
 
 // host-side weight packing for the MFMA kernels (conv_mfma.hip)
-bool mfma_supports(bool bf16, int cout, int fh, int fw);
+bool mfma_supports(bool bf16, int fh, int fw);
 int mfma_f32_pick_bn(int cout);
 int mfma_bf16_pick_bn(int cout);
 size_t mfma_f32_packed_floats(const PlanConv& pc);
