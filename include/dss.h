@@ -45,7 +45,7 @@ typedef enum dss_status {
     DSS_E_INVALID = 1,      /* bad argument: NULL pointer, bad descriptor, channel mismatch */
     DSS_E_SHAPE = 2,        /* extents do not fit: signal smaller than the receptive field,
                                fragment extents not divisible by the pool size, too small workspace */
-    DSS_E_UNSUPPORTED = 3,  /* valid request outside what this build implements */
+    DSS_E_UNSUPPORTED = 3,  /* valid request outside what the library implements */
     DSS_E_NOMEM = 4,        /* device allocation failed */
     DSS_E_HIP = 5           /* a HIP runtime call or kernel launch failed */
 } dss_status;
