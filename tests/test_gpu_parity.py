@@ -169,23 +169,28 @@ def test_random_chain_bf16(name):
     assert_close(out, ref, BF16_TOL, name)
 
 
-# The bfloat16 kernel runs its steps (input-channel chunk x filter tap) in
-# threes over rotating operand registers, with a chunk change inside the
-# rotation: step counts of every residue mod 3, one to three chunks, the single-
-# buffered halo of a 7x7 filter, and small pooled fragments (flat tiles).
-BF16_STEP_CASES = [(cin, f, pool) for cin in (24, 40, 80) for f in (1, 2, 5, 7) for pool in (False,)] + \
-                  [(40, 6, False), (40, 3, True), (80, 5, True), (24, 1, True)]
+# The MFMA kernel runs its steps (input-channel chunk x filter tap) in threes
+# over rotating weight-operand registers, with a chunk change inside the
+# rotation: step counts of every residue mod 3, one to three chunks (16 binary32
+# or 32 bfloat16 channels each), the single-buffered halo of a 7x7 filter, and
+# small pooled fragments (flat tiles).
+STEP_CASES = [(cin, f, pool) for cin in (1, 2, 3) for f in (1, 2, 5, 7) for pool in (False,)] + \
+             [(2, 6, False), (2, 3, True), (3, 5, True), (1, 1, True)]
 
 
-@pytest.mark.parametrize("cin,f,pool", BF16_STEP_CASES)
-def test_bf16_step_rotation(cin, f, pool):
+@pytest.mark.parametrize("chunks,f,pool", STEP_CASES)
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_mfma_step_rotation(dtype, chunks, f, pool):
+    # input channels in `chunks` chunks, the last one ragged where the MFMA kernel's
+    # 16-byte staging allows it (at least 16 channels, multiples of 4 / 8)
+    cin = {"f32": {1: 16, 2: 28, 3: 44}, "bf16": {1: 24, 2: 56, 3: 88}}[dtype][chunks]
     arch = ([("pool", 2, 2)] if pool else []) + [("conv", cin, 136, f, f, "relu")]
     H, W = (2 * f + 23, 2 * f + 37) if pool else (f + 29, f + 70)
-    w = wl.custom(arch, cin, H, W, seed=cin + f, dtype="bf16")
-    log("bf16 conv %dx%d cin=%d pool=%s on %s" % (f, f, cin, pool, w.x.shape))
-    out, _ = gpu_dense(w.layers, w.x, 2, "bf16")
-    ref = oracle.eval_stride(oracle_layers(w.layers, "bf16"), w.x)
-    assert_close(out, ref, BF16_TOL, "bf16 %dx%d cin=%d" % (f, f, cin))
+    w = wl.custom(arch, cin, H, W, seed=cin + f, dtype=dtype)
+    log("%s conv %dx%d cin=%d pool=%s on %s" % (dtype, f, f, cin, pool, w.x.shape))
+    out, _ = gpu_dense(w.layers, w.x, 2, dtype)
+    ref = oracle.eval_stride(oracle_layers(w.layers, dtype), w.x)
+    assert_close(out, ref, BF16_TOL if dtype == "bf16" else F32_TOL, "%s %dx%d cin=%d" % (dtype, f, f, cin))
 
 
 def test_direct_and_mfma_agree(direct_conv):
