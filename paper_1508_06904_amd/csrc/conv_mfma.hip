@@ -376,7 +376,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
                         const int i = (v >> 2) * 8 + half * 4 + (v & 3);
                         st[i * WCOLS + nt * 32 + l32] = f32_to_bf16(activate(act, acc[mt][nt][v] + bn[nt]));
                     }
-                __syncthreads();
+                // st is this wave's own region and LDS executes a wave's operations
+                // in order: no workgroup barrier between the stores and the loads
+                __builtin_amdgcn_wave_barrier();
 #pragma unroll
                 for (int r = 0; r < WCOLS / 16; ++r) {               // 32 rows x WCOLS / 8 units, 64 per round
                     const int u = r * 64 + lane;
@@ -386,7 +388,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
                         *reinterpret_cast<u32x4*>(out + o * Cout + n_base + c8) =
                             *reinterpret_cast<const u32x4*>(st + row * WCOLS + c8);
                 }
-                __syncthreads();                                    // before the next block overwrites st
+                __builtin_amdgcn_wave_barrier();
             }
             return;
         }
@@ -646,9 +648,15 @@ static hipError_t run_mfma(const void* in, int F, int Hin, int Win, int dil_h, i
     if (dilated && F != 1) return hipErrorInvalidValue;   // dilated: one signal, tiled per phase
     if (padded && (dilated || pad_h < 0 || pad_w < 0)) return hipErrorInvalidValue;
     const int nbs = pc.cout_pad / Cfg::BN;
-    const LaunchShape L = launch_shape(Cfg::BM, BF16, F, Hin + 2 * pad_h,
-                                       Win + 2 * pad_w, dil_h, dil_w, pc.fh, pc.fw, nbs, !padded);
+    LaunchShape L = launch_shape(Cfg::BM, BF16, F, Hin + 2 * pad_h, Win + 2 * pad_w, dil_h, dil_w, pc.fh, pc.fw, nbs,
+                                 !padded);
     if (L.nblocks == 0) return hipErrorInvalidConfiguration;
+    // A single channel chunk reads one halo: the second buffer would only halve
+    // the workgroups that fit a CU.
+    if (pc.cin_pad == Cfg::CC && L.t.dbl) {
+        L.t.dbl = 0;
+        L.t.lds /= 2;
+    }
     if (L.nblocks >= (1ll << 31)) return hipErrorInvalidConfiguration;
     auto kern = conv_mfma_kernel<BF16, Tout, WGM, WGN, MT, NT>;
     hipError_t e = allow_large_lds((const void*)kern, L.t.lds);
