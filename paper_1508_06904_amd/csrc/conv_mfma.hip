@@ -177,22 +177,41 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
 
     // Staging: LDS slot S (16 bytes) of the halo holds quad S % 5 of halo sample
     // S / 5 (slot 4 of every sample is padding and is never written); lane l of
-    // wave w stages slot r * THREADS + w * 64 + l in round r.
+    // wave w stages slot r * THREADS + w * 64 + l in round r.  A round moves S on
+    // by THREADS = 51 * 5 + 1 slots, i.e. 51 samples and one quad, so the sample's
+    // halo row and column are divided out once and then advanced by additions.
+    static_assert(THREADS % kSlotsPerRow == 1, "the slot walk assumes THREADS = 1 mod 5");
+    constexpr int kPxStep = THREADS / kSlotsPerRow;
+    const int px_first = tid / kSlotsPerRow, q_first = tid - px_first * kSlotsPerRow;
+    const int dy_first = px_first / HW, dx_first = px_first - dy_first * HW;
+    const int dy_step = kPxStep / HW, dx_step = kPxStep - dy_step * HW;
+    // fn(r0, q, yy, xx) for every staged slot of this thread: round base r0, quad
+    // q, input sample (yy, xx) of the fragment / phase (negative in the border)
+    auto for_each_slot = [&](auto&& fn) {
+        int q = q_first, dy = dy_first, dx = dx_first;
+        for (int r0 = 0; r0 < halo_slots; r0 += THREADS) {
+            if (r0 + tid < halo_slots && q < 4) fn(r0, q, hy0 + dy, hx0 + dx);
+            dy += dy_step;
+            dx += dx_step;
+            if (++q == kSlotsPerRow) {
+                q = 0;
+                ++dx;
+            }
+            if (dx >= HW) {
+                dx -= HW;
+                ++dy;
+            }
+        }
+    };
     auto stage_halo = [&](int cc, char* dst) {
         const char* src_c = in_f + (size_t)cc * kChunkBytes;
         const int c_base = cc * Cfg::CC;
-        for (int r0 = 0; r0 < halo_slots; r0 += THREADS) {
-            const int S = r0 + tid;
-            const int px = S / kSlotsPerRow, q = S - px * kSlotsPerRow;
-            if (S < halo_slots && q < 4) {
-                const int dy = px / HW, dx = px - dy * HW;
-                const int yy = hy0 + dy, xx = hx0 + dx;
-                const bool ok = (unsigned)yy < (unsigned)lim_h && (unsigned)xx < (unsigned)lim_w &&
-                                c_base + q * (16 / Cfg::ES) < Cin;
-                dma16(ok ? src_c + (size_t)yy * row_step + (size_t)xx * col_step + q * 16 : zero,
-                      dst + (r0 + wave * 64) * 16);
-            }
-        }
+        for_each_slot([&](int r0, int q, int yy, int xx) {
+            const bool ok = (unsigned)yy < (unsigned)lim_h && (unsigned)xx < (unsigned)lim_w &&
+                            c_base + q * (16 / Cfg::ES) < Cin;
+            dma16(ok ? src_c + (size_t)yy * row_step + (size_t)xx * col_step + q * 16 : zero,
+                  dst + (r0 + wave * 64) * 16);
+        });
     };
     auto wait_staged = [] {
         __builtin_amdgcn_s_waitcnt(0);   // this wave's copies have landed in LDS
@@ -261,28 +280,22 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
         const char* src_c = in_f + (size_t)cn * kChunkBytes;
         const int c_base = cn * Cfg::CC;
         const uint32_t dst_lds = lds_base + (uint32_t)(dst - lds);
-        for (int r0 = 0; r0 < halo_slots; r0 += THREADS) {
-            const int S = r0 + tid;
-            const int px = S / kSlotsPerRow, q = S - px * kSlotsPerRow;
-            if (S < halo_slots && q < 4) {
-                const int dy = px / HW, dx = px - dy * HW;
-                const int yy = hy0 + dy, xx = hx0 + dx;
-                const bool ok = (unsigned)yy < (unsigned)lim_h && (unsigned)xx < (unsigned)lim_w &&
-                                c_base + q * (16 / Cfg::ES) < Cin;
-                const char* src = ok ? src_c + (size_t)yy * row_step + (size_t)xx * col_step + q * 16 : zero;
-                const uint32_t m0v = __builtin_amdgcn_readfirstlane(dst_lds + (uint32_t)(r0 + wave * 64) * 16);
-                uint32_t saved;
-                asm volatile(
-                    "s_mov_b32 %0, m0\n\t"
-                    "s_mov_b32 m0, %2\n\t"
-                    "s_nop 0\n\t"
-                    "global_load_lds_dwordx4 %1, off\n\t"
-                    "s_mov_b32 m0, %0"
-                    : "=&s"(saved)
-                    : "v"(src), "s"(m0v)
-                    : "memory");
-            }
-        }
+        for_each_slot([&](int r0, int q, int yy, int xx) {
+            const bool ok = (unsigned)yy < (unsigned)lim_h && (unsigned)xx < (unsigned)lim_w &&
+                            c_base + q * (16 / Cfg::ES) < Cin;
+            const char* src = ok ? src_c + (size_t)yy * row_step + (size_t)xx * col_step + q * 16 : zero;
+            const uint32_t m0v = __builtin_amdgcn_readfirstlane(dst_lds + (uint32_t)(r0 + wave * 64) * 16);
+            uint32_t saved;
+            asm volatile(
+                "s_mov_b32 %0, m0\n\t"
+                "s_mov_b32 m0, %2\n\t"
+                "s_nop 0\n\t"
+                "global_load_lds_dwordx4 %1, off\n\t"
+                "s_mov_b32 m0, %0"
+                : "=&s"(saved)
+                : "v"(src), "s"(m0v)
+                : "memory");
+        });
     };
     // B operands two steps ahead in three register sets whose roles rotate
     // with the step, over all steps of all chunks in threes, so no register
@@ -331,6 +344,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
 
     // -- epilogue: D[i][j] of a 32x32 tile sits in lane j + 32*((i/4)%2), register (i/8)*4 + i%4
     const int n_base = nb * Cfg::BN + wn * 32 * NT;
+    const int tw_log2 = __builtin_ctz(TW);   // spatial and dilated tiles are 2^k samples wide
     const size_t f_off = (size_t)f * Hout * Wout;
     const int frag_px = flat_h * flat_w;
     // output sample of tile position m: whether it exists, and its index
@@ -343,11 +357,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
             return p < Win && y < Hout && x < Wout;
         }
         if (dilated) {
-            const int y = py + dil_h * (ty0 + m / TW), x = px + dil_w * (tx0 + m % TW);
+            const int y = py + dil_h * (ty0 + (m >> tw_log2)), x = px + dil_w * (tx0 + (m & (TW - 1)));
             o = (size_t)y * Wout + x;
             return y < Hout && x < Wout;
         }
-        const int y = ty0 + m / TW, x = tx0 + m % TW;
+        const int y = ty0 + (m >> tw_log2), x = tx0 + (m & (TW - 1));
         o = f_off + (size_t)y * Wout + x;
         return y < Hout && x < Wout;
     };
@@ -408,11 +422,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
                 ok = p < Win && y < Hout && x < Wout;
                 o = ((size_t)fr * Hout + y) * Wout + x;
             } else if (dilated) {
-                const int y = py + dil_h * (ty0 + m / TW), x = px + dil_w * (tx0 + m % TW);
+                const int y = py + dil_h * (ty0 + (m >> tw_log2)), x = px + dil_w * (tx0 + (m & (TW - 1)));
                 ok = y < Hout && x < Wout;
                 o = (size_t)y * Wout + x;
             } else {
-                const int y = ty0 + m / TW, x = tx0 + m % TW;
+                const int y = ty0 + (m >> tw_log2), x = tx0 + (m & (TW - 1));
                 ok = y < Hout && x < Wout;
                 o = f_off + (size_t)y * Wout + x;
             }
