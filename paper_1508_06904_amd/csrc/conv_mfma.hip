@@ -38,6 +38,7 @@
 #include <algorithm>
 
 #include <mutex>
+#include <type_traits>
 #include <vector>
 
 #include "dev_common.h"
@@ -372,71 +373,82 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
         ncol[nt] = n_base + nt * 32 + l32;
         bn[nt] = ncol[nt] < Cout ? bias[ncol[nt]] : 0.f;
     }
-    if constexpr (sizeof(Tout) == 2) {
-        // bfloat16 output: each lane holds one channel of 16 positions, so direct
-        // stores would be 2-byte stores, one instruction per value.  Transpose
-        // through LDS (the halo buffers are free now) into 16-byte units of 8
-        // channels of one position: 8x fewer store instructions.
-        if (Cout % 8 == 0 && ((uintptr_t)out & 15) == 0) {
-            constexpr int WCOLS = 32 * NT;                          // channels of a wave's block
-            uint16_t* st = reinterpret_cast<uint16_t*>(lds) + wave * (32 * WCOLS);
-            __syncthreads();                                        // every wave is done with the halo
+    // The stores of one activation (a compile-time constant, so the per-value
+    // code has no branch on it).
+    auto store_tile = [&](auto act_c) {
+        constexpr int ACT = decltype(act_c)::value;
+        if constexpr (sizeof(Tout) == 2) {
+            // bfloat16 output: each lane holds one channel of 16 positions, so direct
+            // stores would be 2-byte stores, one instruction per value.  Transpose
+            // through LDS (the halo buffers are free now) into 16-byte units of 8
+            // channels of one position: 8x fewer store instructions.
+            if (Cout % 8 == 0 && ((uintptr_t)out & 15) == 0) {
+                constexpr int WCOLS = 32 * NT;                          // channels of a wave's block
+                uint16_t* st = reinterpret_cast<uint16_t*>(lds) + wave * (32 * WCOLS);
+                __syncthreads();                                        // every wave is done with the halo
 #pragma unroll
-            for (int mt = 0; mt < MT; ++mt) {
+                for (int mt = 0; mt < MT; ++mt) {
+#pragma unroll
+                    for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+                        for (int v = 0; v < 16; ++v) {
+                            const int i = (v >> 2) * 8 + half * 4 + (v & 3);
+                            st[i * WCOLS + nt * 32 + l32] = f32_to_bf16(activate(ACT, acc[mt][nt][v] + bn[nt]));
+                        }
+                    // st is this wave's own region and LDS executes a wave's operations
+                    // in order: no workgroup barrier between the stores and the loads
+                    __builtin_amdgcn_wave_barrier();
+#pragma unroll
+                    for (int r = 0; r < WCOLS / 16; ++r) {               // 32 rows x WCOLS / 8 units, 64 per round
+                        const int u = r * 64 + lane;
+                        const int row = u / (WCOLS / 8), c8 = (u % (WCOLS / 8)) * 8;
+                        size_t o;
+                        if (out_pos(wm * 32 * MT + mt * 32 + row, o) && n_base + c8 < Cout)
+                            *reinterpret_cast<u32x4*>(out + o * Cout + n_base + c8) =
+                                *reinterpret_cast<const u32x4*>(st + row * WCOLS + c8);
+                    }
+                    __builtin_amdgcn_wave_barrier();
+                }
+                return;
+            }
+        }
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const int i = (v >> 2) * 8 + half * 4 + (v & 3);
+                const int m = wm * 32 * MT + mt * 32 + i;
+                size_t o;
+                bool ok;
+                if (flat_w) {
+                    const int p = tx0 + m;
+                    const int fr = p / frag_px, r = p - fr * frag_px;
+                    const int y = r / flat_w, x = r - y * flat_w;
+                    ok = p < Win && y < Hout && x < Wout;
+                    o = ((size_t)fr * Hout + y) * Wout + x;
+                } else if (dilated) {
+                    const int y = py + dil_h * (ty0 + (m >> tw_log2)), x = px + dil_w * (tx0 + (m & (TW - 1)));
+                    ok = y < Hout && x < Wout;
+                    o = (size_t)y * Wout + x;
+                } else {
+                    const int y = ty0 + (m >> tw_log2), x = tx0 + (m & (TW - 1));
+                    ok = y < Hout && x < Wout;
+                    o = f_off + (size_t)y * Wout + x;
+                }
+                if (!ok) continue;
 #pragma unroll
                 for (int nt = 0; nt < NT; ++nt)
-#pragma unroll
-                    for (int v = 0; v < 16; ++v) {
-                        const int i = (v >> 2) * 8 + half * 4 + (v & 3);
-                        st[i * WCOLS + nt * 32 + l32] = f32_to_bf16(activate(act, acc[mt][nt][v] + bn[nt]));
-                    }
-                // st is this wave's own region and LDS executes a wave's operations
-                // in order: no workgroup barrier between the stores and the loads
-                __builtin_amdgcn_wave_barrier();
-#pragma unroll
-                for (int r = 0; r < WCOLS / 16; ++r) {               // 32 rows x WCOLS / 8 units, 64 per round
-                    const int u = r * 64 + lane;
-                    const int row = u / (WCOLS / 8), c8 = (u % (WCOLS / 8)) * 8;
-                    size_t o;
-                    if (out_pos(wm * 32 * MT + mt * 32 + row, o) && n_base + c8 < Cout)
-                        *reinterpret_cast<u32x4*>(out + o * Cout + n_base + c8) =
-                            *reinterpret_cast<const u32x4*>(st + row * WCOLS + c8);
-                }
-                __builtin_amdgcn_wave_barrier();
+                    if (ncol[nt] < Cout)
+                        store_elem(out + o * Cout + ncol[nt], activate(ACT, acc[mt][nt][v] + bn[nt]));
             }
-            return;
         }
-    }
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-            const int i = (v >> 2) * 8 + half * 4 + (v & 3);
-            const int m = wm * 32 * MT + mt * 32 + i;
-            size_t o;
-            bool ok;
-            if (flat_w) {
-                const int p = tx0 + m;
-                const int fr = p / frag_px, r = p - fr * frag_px;
-                const int y = r / flat_w, x = r - y * flat_w;
-                ok = p < Win && y < Hout && x < Wout;
-                o = ((size_t)fr * Hout + y) * Wout + x;
-            } else if (dilated) {
-                const int y = py + dil_h * (ty0 + (m >> tw_log2)), x = px + dil_w * (tx0 + (m & (TW - 1)));
-                ok = y < Hout && x < Wout;
-                o = (size_t)y * Wout + x;
-            } else {
-                const int y = ty0 + (m >> tw_log2), x = tx0 + (m & (TW - 1));
-                ok = y < Hout && x < Wout;
-                o = f_off + (size_t)y * Wout + x;
-            }
-            if (!ok) continue;
-#pragma unroll
-            for (int nt = 0; nt < NT; ++nt)
-                if (ncol[nt] < Cout)
-                    store_elem(out + o * Cout + ncol[nt], activate(act, acc[mt][nt][v] + bn[nt]));
-        }
-    }
+    };
+    if (act == 1)
+        store_tile(std::integral_constant<int, 1>{});
+    else if (act == 2)
+        store_tile(std::integral_constant<int, 2>{});
+    else
+        store_tile(std::integral_constant<int, 0>{});
 }
 
 // ------------------------------------------------------------------ host side
