@@ -188,7 +188,8 @@ dss_status dss_plan_layer_geometry(dss_plan_t plan, int32_t H, int32_t W, int32_
  *   workspace  device scratch of at least dss_geometry.workspace_bytes bytes
  *              (256-byte aligned), owned by the caller and not read afterwards
  *   stream     HIP stream for every launch
- * Concurrent evaluations of one plan are allowed if each uses its own workspace.
+ * Concurrent evaluations of one plan are allowed if each uses its own workspace
+ * and the plan's timing is off (timed evaluations append to one record list).
  * Errors: DSS_E_INVALID (NULL pointers), DSS_E_SHAPE (signal smaller than the
  * receptive field, workspace too small), DSS_E_HIP (launch failure). */
 dss_status dss_eval_dense(dss_plan_t plan, const void* signal, int32_t H, int32_t W, float* out,
@@ -379,7 +380,8 @@ typedef struct dss_launch_record {
  * evaluations of this plan, and discards the records collected so far (after
  * waiting for their events).  Timing adds two event records per launch on the
  * evaluation stream and is off by default.  Records accumulate over all timed
- * evaluations until the next call of this function. */
+ * evaluations until the next call of this function; timed evaluations of one
+ * plan must not run concurrently from several host threads. */
 dss_status dss_plan_set_timing(dss_plan_t plan, int32_t enable);
 
 /* Waits for the events of the collected records and copies up to `cap` of

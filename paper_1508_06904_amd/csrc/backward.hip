@@ -33,8 +33,6 @@
 //  crop_to_planar      transpose of Stuff: the stuffed input's gradient cropped
 //                      to the signal and written planar.
 #include <algorithm>
-#include <mutex>
-#include <vector>
 
 #include "dev_common.h"
 #include "dss_internal.h"
@@ -393,18 +391,6 @@ __global__ __launch_bounds__(kBT) void wgrad_reduce_kernel(const float* __restri
     dw[p] = s;                                   // [o][i][th][tw] with tap = th * fw + tw
 }
 
-static hipError_t allow_lds(const void* kern, size_t lds) {
-    if (lds <= 64 * 1024) return hipSuccess;
-    static std::mutex mu;
-    static std::vector<const void*> done;
-    std::lock_guard<std::mutex> lock(mu);
-    for (const void* k : done)
-        if (k == kern) return hipSuccess;
-    hipError_t e = hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    if (e == hipSuccess) done.push_back(kern);
-    return e;
-}
-
 WgradPlan wgrad_plan(int F, int E_h, int E_w, int Cout, int Cin, int fh, int fw) {
     WgradPlan w;
     if (Cin <= kWT / 2) {
@@ -470,7 +456,7 @@ static hipError_t run_wgrad(const float* dy, const float* x, int E_h, int E_w, i
                             int fh, int fw, const WgradPlan& w, float* partial, float* bpart, hipStream_t s) {
     auto kern = wgrad_mfma_kernel<VEC, TT, PACKED>;
     const size_t lds = wgrad_lds_bytes(TT);
-    hipError_t e = allow_lds((const void*)kern, lds);
+    hipError_t e = allow_dynamic_lds((const void*)kern, lds);
     if (e != hipSuccess) return e;
     const int64_t nblocks = (int64_t)w.otiles * w.itiles * fh * w.ntg * w.splits;
     if (nblocks >= (1ll << 31)) return hipErrorInvalidConfiguration;

@@ -37,9 +37,7 @@
 // transposed through LDS into 16-byte stores of 8 channels.
 #include <algorithm>
 
-#include <mutex>
 #include <type_traits>
-#include <vector>
 
 #include "dev_common.h"
 #include "dss_internal.h"
@@ -502,20 +500,6 @@ struct Tile {
     int dbl;    // halo double-buffered
 };
 
-// Largest dynamic LDS allocation per workgroup on the current device.
-static size_t device_lds_limit() {
-    static int cached = -1;
-    if (cached < 0) {
-        int dev = 0, v = 0;
-        if (hipGetDevice(&dev) != hipSuccess ||
-            hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess)
-            v = 64 * 1024;
-        cached = v;
-    }
-    return (size_t)cached;
-}
-
-
 // Spatial tile TH x TW = BM output samples: the shape that wastes the fewest
 // masked samples on this layer's fragment extent; among those, one whose halo can
 // be double-buffered within the LDS budget of two workgroups per CU, then the
@@ -555,19 +539,6 @@ static Tile pick_tile(int BM, int Hout, int Wout, int fh, int fw, size_t lds_max
 // against the 64 KB every device offers).
 bool mfma_supports(bool bf16, int fh, int fw) {
     return pick_tile(256, 1, 1, fh, fw, 64 * 1024, bf16).TH > 0 && pick_tile(256, 64, 64, fh, fw, 64 * 1024, bf16).TH > 0;
-}
-
-// Dynamic LDS above 64 KB needs a per-kernel opt-in (once per instantiation).
-static hipError_t allow_large_lds(const void* kern, size_t lds) {
-    if (lds <= 64 * 1024) return hipSuccess;
-    static std::mutex mu;
-    static std::vector<const void*> done;
-    std::lock_guard<std::mutex> lock(mu);
-    for (const void* k : done)
-        if (k == kern) return hipSuccess;
-    hipError_t e = hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kMaxLds);
-    if (e == hipSuccess) done.push_back(kern);
-    return e;
 }
 
 // Flat-mode tile (TH = 1, TW = BM consecutive positions of the flattened
@@ -685,7 +656,7 @@ static hipError_t run_mfma(const void* in, int F, int Hin, int Win, int dil_h, i
     }
     if (L.nblocks >= (1ll << 31)) return hipErrorInvalidConfiguration;
     auto kern = conv_mfma_kernel<BF16, Tout, WGM, WGN, MT, NT>;
-    hipError_t e = allow_large_lds((const void*)kern, L.t.lds);
+    hipError_t e = allow_dynamic_lds((const void*)kern, L.t.lds);
     if (e != hipSuccess) return e;
     const int nchunks = pc.cin_pad / Cfg::CC;
     const int Hout = Hin + 2 * pad_h - dil_h * (pc.fh - 1), Wout = Win + 2 * pad_w - dil_w * (pc.fw - 1);

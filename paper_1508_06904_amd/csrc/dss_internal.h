@@ -178,6 +178,11 @@ hipError_t launch_wgrad(const float* dy, const float* x, int F, int E_h, int E_w
 hipError_t launch_crop_to_planar(const float* in, int D_w, int C, int H, int W, float* out, hipStream_t s);
 
 // host-side weight packing for the MFMA kernels (conv_mfma.hip)
+// Largest dynamic LDS allocation of a workgroup on the current device.
+size_t device_lds_limit();
+// Lets kern use `bytes` of dynamic LDS on the current device (an opt-in is
+// needed above 64 KB; kept per device and kernel).
+hipError_t allow_dynamic_lds(const void* kern, size_t bytes);
 bool mfma_supports(bool bf16, int fh, int fw);
 int mfma_f32_pick_bn(int cout);
 int mfma_bf16_pick_bn(int cout);
