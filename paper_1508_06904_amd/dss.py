@@ -250,7 +250,8 @@ class Plan:
 
     def workspace(self, H, W, device=None, ell=0):
         """A device workspace (uint8 tensor) large enough for an H x W signal at
-        mixed level ell; reused across calls."""
+        mixed level ell; one buffer per plan, reused by every call that passes no
+        workspace, so calls that run concurrently pass workspaces of their own."""
         import torch
         need = self.geometry(H, W, ell)["workspace_bytes"]
         if self._ws is None or self._ws.numel() < need:

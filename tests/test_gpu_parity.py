@@ -337,6 +337,48 @@ def test_run_twice_bit_identical():
     np.testing.assert_array_equal(a, b)
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_concurrent_evaluations_one_plan(dtype):
+    """Two host threads evaluate one plan at the same time, each on its own
+    stream with its own workspace (the concurrency the C ABI allows when timing
+    is off): every result equals the serial evaluation bit for bit."""
+    import threading
+    import torch
+    arch, C, nd = CHAINS["2d_mfma_mixed"]
+    H, W = 90, 84
+    sig = [wl.custom(arch, C, H, W, seed=s) for s in (21, 22)]
+    plan = dss.Plan(sig[0].layers, nd, C, dtype)
+    xs = [to_device(w.x, dtype) for w in sig]
+    serial = [plan.eval_dense(x) for x in xs]
+    torch.cuda.synchronize()
+    serial = [s.cpu() for s in serial]
+    need = plan.geometry(H, W)["workspace_bytes"]
+    spaces = [torch.empty(need, dtype=torch.uint8, device="cuda") for _ in xs]
+    outs = [torch.empty(s.shape, dtype=torch.float32, device="cuda") for s in serial]
+    streams = [torch.cuda.Stream() for _ in xs]
+    torch.cuda.synchronize()
+    errors = []
+
+    def run(i):
+        try:
+            for _ in range(4):
+                plan.eval_dense(xs[i], out=outs[i], workspace=spaces[i], stream=streams[i])
+            streams[i].synchronize()
+        except Exception as e:   # reported by the main thread
+            errors.append(e)
+
+    threads = [threading.Thread(target=run, args=(i,)) for i in range(len(xs))]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join(timeout=120)
+    assert not any(t.is_alive() for t in threads)
+    assert not errors, errors
+    torch.cuda.synchronize()
+    for i in range(len(xs)):
+        assert torch.equal(outs[i].cpu(), serial[i]), i
+
+
 def test_timing_records():
     w = wl.make("c3_512", H=120, W=130, widths=(16, 32, 64, 128))
     plan = dss.Plan.from_workload(w)
