@@ -30,6 +30,17 @@ def test_library_exports_every_declared_function():
     assert L.dss_version().decode().count(".") == 2
 
 
+def test_missing_library_fails_loudly(monkeypatch, tmp_path):
+    """Without libdss.so the binding raises at its first call: there is no
+    fallback path that could compute anything."""
+    monkeypatch.setattr(dss, "_lib", None)
+    monkeypatch.setattr(dss, "LIB_PATH", str(tmp_path / "libdss.so"))
+    with pytest.raises(dss.DssError, match="does not exist"):
+        dss.lib()
+    with pytest.raises(dss.DssError):
+        dss.Plan.from_workload(wl.make("c1_64x64"))
+
+
 def test_status_strings():
     L = dss.lib()
     for s in range(6):
