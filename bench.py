@@ -62,6 +62,50 @@ WORKLOAD_TEXT = {
 }
 
 
+# The workloads measured besides the headline (HD frame) in a default run, the
+# fewest timed steps for each (the small ones run well under a millisecond), and
+# the oracle's time budget on each (the 64x64 frame is checked in full).
+EXTRA_CONFIGS = ("c1_64x64", "c2_1d_1m", "c3_512", "c5_4k")
+MIN_STEPS = {"c1_64x64": 500, "c2_1d_1m": 200, "c3_512": 100}
+EXTRA_CPU_SECONDS = {"c1_64x64": 6.0, "c2_1d_1m": 16.0, "c3_512": 6.0, "c5_4k": 8.0}
+
+
+def host_cpu_info():
+    """The host the oracle runs on: logical CPUs, the ones this process may use,
+    physical cores and the CPU model (from /proc/cpuinfo)."""
+    info = {"nproc": os.cpu_count()}
+    try:
+        info["affinity_cpus"] = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        pass
+    try:
+        cores, model, phys = set(), None, None
+        for line in open("/proc/cpuinfo"):
+            k, _, v = line.partition(":")
+            k, v = k.strip(), v.strip()
+            if k == "model name" and model is None:
+                model = v
+            elif k == "physical id":
+                phys = v
+            elif k == "core id":
+                cores.add((phys, v))
+        info["physical_cores"] = len(cores) or None
+        info["cpu_model"] = model
+    except OSError:
+        pass
+    return info
+
+
+def child_processes():
+    """Processes this benchmark left running (there should be none)."""
+    try:
+        import psutil
+        return [{"pid": c.pid, "name": c.name(), "cmdline": " ".join(c.cmdline())[:200]}
+                for c in psutil.Process().children(recursive=True)]
+    except Exception as e:   # psutil missing or the process table unreadable
+        return [{"error": str(e)}]
+
+
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
@@ -112,7 +156,11 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--config", default="c4_hd", choices=sorted(WORKLOAD_TEXT))
+    ap.add_argument("--config", default=None, choices=sorted(WORKLOAD_TEXT),
+                    help="headline workload (default c4_hd, plus per-workload entries for the other four)")
+    ap.add_argument("--configs", default=None,
+                    help="comma-separated workloads measured after the headline into the 'configs' key "
+                         "(default: the other four named workloads when --config is not given; '' for none)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target length of the oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--ell", type=int, default=0,
@@ -127,6 +175,8 @@ def main():
                     help="EvalSlide vs patch-by-patch EvalStride on the paper's 240x320 family, L = 1..15")
     ap.add_argument("--sweep-layers", default="1-15", help="range of L for --sweep, e.g. 1-15 or 12")
     args = ap.parse_args()
+    args.config_given = args.config is not None
+    args.config = args.config or "c4_hd"
     if args.calibrate_copy:
         return calibrate_copy()
 
@@ -136,17 +186,41 @@ def main():
               "build (multi-GPU sharding is a design note only); run with --gpus 1", file=sys.stderr)
         sys.exit(2)
 
+    import torch
+
+    torch.cuda.set_device(0)
+    if args.sweep:
+        return sweep(args)
+    record = measure(args, args.config, args.steps, args.warmup, args.cpu_seconds, args.no_cpu_baseline)
+    extra = [c for c in args.configs.split(",") if c] if args.configs is not None else \
+        ([] if args.config_given or args.ell or args.backward or args.fashion != "slide"
+         else [c for c in EXTRA_CONFIGS if c != args.config])
+    if extra:
+        record["configs"] = {}
+        for c in extra:
+            steps = max(args.steps, MIN_STEPS.get(c, 0))
+            r = measure(argparse.Namespace(ell=0, fashion="slide", backward=False), c, steps, args.warmup,
+                        EXTRA_CPU_SECONDS.get(c, 6.0), args.no_cpu_baseline)
+            record["configs"][c] = {k: r[k] for k in ("value", "unit", "ms_per_step", "ms_per_step_median", "steps",
+                                                      "dtype", "config", "roofline", "conv_aggregate", "breakdown",
+                                                      "cpu_baseline") if k in r}
+            if "parity_spot_check" in r:
+                record["configs"][c]["parity_spot_check"] = r["parity_spot_check"]
+    record["children_at_exit"] = child_processes()
+    print(json.dumps(record), flush=True)
+
+
+def measure(args, name, steps, warmup, cpu_seconds, no_cpu):
+    """One workload: `warmup` untimed steps, then `steps` timed steps twice
+    (plain, then with per-launch events); the record of its JSON line."""
     import numpy as np
     import torch
 
     from paper_1508_06904_amd import dss, workloads as wl
 
-    torch.cuda.set_device(0)
-    if args.sweep:
-        return sweep(args)
     t0 = time.time()
-    w = wl.make(args.config)
-    log("workload %s %s generated in %.1fs" % (args.config, w.x.shape, time.time() - t0))
+    w = wl.make(name)
+    log("workload %s %s generated in %.1fs" % (name, w.x.shape, time.time() - t0))
     plan = dss.Plan.from_workload(w)
     C, H, W = w.x.shape
     ell = args.ell
@@ -189,7 +263,7 @@ def main():
         else:
             plan.eval_mixed(x, ell, out=out, workspace=ws)
 
-    for i in range(args.warmup):
+    for i in range(warmup):
         step()
         torch.cuda.synchronize()
         log("warmup %d done" % i)
@@ -199,16 +273,16 @@ def main():
         event pair around every kernel launch (the per-kernel durations of the
         roofline and the breakdown)."""
         plan.set_timing(instrumented)
-        evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+        evs = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
         torch.cuda.synchronize()
         t0 = time.perf_counter()
         evs[0].record()
-        for i in range(args.steps):
+        for i in range(steps):
             step()
             evs[i + 1].record()
         torch.cuda.synchronize()
         wall = time.perf_counter() - t0
-        per = sorted(evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps))
+        per = sorted(evs[i].elapsed_time(evs[i + 1]) for i in range(steps))
         med = per[len(per) // 2] if len(per) % 2 else 0.5 * (per[len(per) // 2 - 1] + per[len(per) // 2])
         recs = plan.timings() if instrumented else None
         plan.set_timing(False)
@@ -218,33 +292,33 @@ def main():
     # (on small workloads an event pair per launch costs as much as the launch)
     ms_total, ms_median, wall_s, _ = timed(False)
     ms_total_inst, _, _, recs = timed(True)
-    ms_per_step = ms_total / args.steps
+    ms_per_step = ms_total / steps
     log("timed %d steps: %.3f ms/step (host wall %.3f ms/step); with per-launch events %.3f ms/step" % (
-        args.steps, ms_per_step, 1e3 * wall_s / args.steps, ms_total_inst / args.steps))
+        steps, ms_per_step, 1e3 * wall_s / steps, ms_total_inst / steps))
 
-    kernels = summarize(recs, args.steps)
+    kernels = summarize(recs, steps)
     breakdown = [e for e, _ in kernels]
     dom, domd = kernels[0]
     if domd["flops"] > 0:
         ach = (domd["flops"] / domd["n"]) / (domd["ms"] / domd["n"]) / 1e9
         peak = PEAK_TFLOPS[w.dtype]
         roof = {"bound": "mfma", "kernel": dom["kernel"], "achieved": ach, "peak": peak, "unit": "TFLOP/s",
-                "frac": ach / peak, "traffic": profiled_traffic(dom["kernel"], args.config if ell == 0 and args.fashion == "slide"
+                "frac": ach / peak, "traffic": profiled_traffic(dom["kernel"], name if ell == 0 and args.fashion == "slide"
                                            and not args.backward
-                                           else "%s_%s%d%s" % (args.config, args.fashion, ell,
+                                           else "%s_%s%d%s" % (name, args.fashion, ell,
                                                                "_backward" if args.backward else "")),
                 "traffic_unit": "bytes per launch (HBM, rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
                 "per_launch": {"flops": domd["flops"] / domd["n"], "avg_ms": domd["ms"] / domd["n"],
-                               "launches_per_step": domd["n"] / args.steps}}
+                               "launches_per_step": domd["n"] / steps}}
     else:
         ach = (domd["bytes"] / domd["n"]) / (domd["ms"] / domd["n"]) / 1e6
         roof = {"bound": "hbm", "kernel": dom["kernel"], "achieved": ach, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                 "frac": ach / PEAK_HBM_GBS, "traffic": None,
                 "per_launch": {"bytes": domd["bytes"] / domd["n"], "avg_ms": domd["ms"] / domd["n"]}}
-    conv_ms = sum(d["ms"] for e, d in kernels if d["flops"] > 0) / args.steps
+    conv_ms = sum(d["ms"] for e, d in kernels if d["flops"] > 0) / steps
     conv_tflops = g["conv_flops"] / (conv_ms * 1e9) if conv_ms > 0 else None
 
-    config = {"workload": args.config + ": " + WORKLOAD_TEXT[args.config], "input": [C, H, W],
+    config = {"workload": name + ": " + WORKLOAD_TEXT[name], "input": [C, H, W],
               "windows_per_step": windows, "receptive_field": [g["B_h"], g["B_w"]],
               "k_star": [g["K_h"], g["K_w"]], "conv_gflop_per_step": g["conv_flops"] / 1e9}
     if args.fashion == "dilate":
@@ -262,11 +336,11 @@ def main():
         "value": windows / (ms_per_step / 1e3),
         "unit": "windows/s",
         "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
+        "steps": steps,
+        "warmup": warmup,
         "ms_per_step": ms_per_step,
         "ms_per_step_median": ms_median,
-        "ms_per_step_with_launch_events": ms_total_inst / args.steps,
+        "ms_per_step_with_launch_events": ms_total_inst / steps,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -280,11 +354,17 @@ def main():
         "cpu_baseline": None,
     }
 
-    if not args.no_cpu_baseline and args.backward:
-        record["cpu_baseline"] = cpu_baseline_backward(w, g, args.cpu_seconds)
-    elif not args.no_cpu_baseline:
-        record["cpu_baseline"], record["parity_spot_check"] = cpu_baseline(w, g, out, args.cpu_seconds)
-    print(json.dumps(record), flush=True)
+    if not no_cpu and args.backward:
+        record["cpu_baseline"] = cpu_baseline_backward(w, g, cpu_seconds)
+    elif not no_cpu:
+        record["cpu_baseline"], record["parity_spot_check"] = cpu_baseline(w, g, out, cpu_seconds)
+    del plan, out, x
+    if "ws" in locals():
+        del ws
+    torch.cuda.empty_cache()
+    return record
+
+
 
 
 def sweep(args, H=240, W=320, maps=128, ws_budget=48e9):
@@ -414,7 +494,7 @@ def cpu_baseline_backward(w, g, target_s):
         run(first, min(16, n - first))
     cpu_s = time.perf_counter() - t
     log("cpu baseline (backward): %d windows in %.1fs" % (n, cpu_s))
-    return {"value": n / cpu_s, "unit": "windows/s", "cores": cores, "kind": "oracle",
+    return {"value": n / cpu_s, "unit": "windows/s", "cores": cores, "kind": "oracle", "host": host_cpu_info(),
             "sample": "%d seeded windows of the frame (corners, edges, fragment phases); float64 window-by-window "
                       "backpropagation through the strided network" % n, "seconds": cpu_s}
 
@@ -442,12 +522,20 @@ def cpu_baseline(w, g, out, target_s):
     t = time.perf_counter()
     oracle.eval_stride(layers, w.x, windows=(sh * si[:nprobe], sw * sj[:nprobe]))
     probe_s = time.perf_counter() - t
-    n = int(max(nprobe, min(4096, target_s / max(probe_s, 1e-6) * nprobe)))
-    if n > len(si):
-        reps = -(-n // max(1, len(si))) + 1
-        si, sj = wl.sample_windows(g["out_h"], g["out_w"], Gh, Gw, per_phase=reps, seed=1)
-    n = min(n, len(si))
-    si, sj = si[:n], sj[:n]
+    windows = g["out_h"] * g["out_w"]
+    full = windows * probe_s / nprobe <= target_s
+    if full:
+        # the whole frame fits the time budget: every window
+        ii, jj = np.meshgrid(np.arange(g["out_h"]), np.arange(g["out_w"]), indexing="ij")
+        si, sj = ii.reshape(-1), jj.reshape(-1)
+        n = len(si)
+    else:
+        n = int(max(nprobe, min(4096, target_s / max(probe_s, 1e-6) * nprobe)))
+        if n > len(si):
+            reps = -(-n // max(1, len(si))) + 1
+            si, sj = wl.sample_windows(g["out_h"], g["out_w"], Gh, Gw, per_phase=reps, seed=1)
+        n = min(n, len(si))
+        si, sj = si[:n], sj[:n]
     log("cpu baseline: %d windows on %d threads (probe %.2fs for %d)" % (n, threads, probe_s, nprobe))
     t = time.perf_counter()
     ref = oracle.eval_stride(layers, w.x, windows=(sh * si, sw * sj))
@@ -455,13 +543,13 @@ def cpu_baseline(w, g, out, target_s):
     got = out[:, si, sj].T.cpu().numpy().astype(np.float64) if hasattr(out, "cpu") else out
     err = float(np.abs(got - ref).max() / max(np.abs(ref).max(), 1e-300))
     H, W = w.x.shape[1:]
-    windows = g["out_h"] * g["out_w"]
+    sample = ("every window (%d) of the %dx%d frame" % (n, H, W) if full else
+              "%d seeded windows of the %dx%d frame covering every fragment phase (i mod %d, j mod %d) "
+              "plus corners and edge midpoints%s" % (n, H, W, Gh, Gw, "" if sh == sw == 1 else
+                                                      " of the output grid (window spacing %dx%d)" % (sh, sw)))
     base = {"value": n / cpu_s, "unit": "windows/s", "cores": threads, "kind": "oracle",
-            "sample": "%d seeded windows of the %dx%d frame covering every fragment phase (i mod %d, j mod %d) "
-                      "plus corners and edge midpoints%s; fp64 EvalStride per window"
-                      % (n, H, W, Gh, Gw, "" if sh == sw == 1 else
-                         " of the output grid (window spacing %dx%d)" % (sh, sw)),
-            "seconds": cpu_s, "extrapolated_full_frame_s": windows * cpu_s / n}
+            "sample": sample + "; fp64 EvalStride per window, plain C with OpenMP over windows",
+            "seconds": cpu_s, "extrapolated_full_frame_s": windows * cpu_s / n, "host": host_cpu_info()}
     tol = 2e-2 if w.dtype == "bf16" else 1e-4
     spot = {"windows": n, "max_abs_err_over_max_abs_oracle": err, "tolerance": tol, "pass": err <= tol}
     log("cpu baseline %.2f windows/s; parity spot check %.3e (tol %.0e)" % (base["value"], err, tol))

@@ -25,6 +25,16 @@
  *    every output buffer untouched.
  *  - A 1-D signal is a 2-D one with height 1 (ndim = 1 requires H = 1, filter
  *    heights fh = 1 and pool heights kh = 1).
+ *  - Workspaces.  Every evaluation entry point takes device scratch memory as
+ *    (workspace, workspace_bytes).  A caller's workspace must hold at least the
+ *    bytes the matching geometry query reports and be 256-byte aligned; it is
+ *    not read after the call's work completes.  workspace == NULL selects the
+ *    plan's own workspace instead (workspace_bytes is then ignored): allocated on
+ *    the plan's first request, grown to the largest request seen (growing first
+ *    waits for the whole device, then frees and reallocates), freed by
+ *    dss_plan_destroy.  Evaluations that pass NULL share that one buffer, so
+ *    they must not run concurrently on one plan (on several streams or host
+ *    threads); pass a workspace of your own per stream for that.
  *  - Filters use cross-correlation order, as deep-learning frameworks do:
  *    weight[o][i][t_h][t_w] multiplies input sample (y + t_h, x + t_w).  The
  *    paper writes the same operation with a flipped filter (Sect. 3.3); the two
@@ -167,8 +177,9 @@ dss_status dss_chain_layer_geometry(const dss_layer* layers, int32_t n_layers, i
 dss_status dss_plan_create(const dss_layer* layers, int32_t n_layers, int32_t ndim,
                            int32_t in_channels, dss_dtype dtype, dss_plan_t* out_plan);
 
-/* Releases the plan's device memory.  NULL is ignored.  Must not race with an
- * evaluation that is still running on the plan. */
+/* Releases the plan's device memory (weights and the plan's own workspace).
+ * NULL is ignored.  Must not race with an evaluation that is still running on
+ * the plan. */
 void dss_plan_destroy(dss_plan_t plan);
 
 /* The geometries above for the plan's network (and dtype). */
@@ -186,12 +197,15 @@ dss_status dss_plan_layer_geometry(dss_plan_t plan, int32_t H, int32_t W, int32_
  *              out[c][i][j] is channel c of the network's output on the window
  *              whose top-left sample is (i, j)
  *   workspace  device scratch of at least dss_geometry.workspace_bytes bytes
- *              (256-byte aligned), owned by the caller and not read afterwards
+ *              (256-byte aligned), owned by the caller and not read afterwards;
+ *              or NULL for the plan's own workspace (see "Workspaces" above)
  *   stream     HIP stream for every launch
  * Concurrent evaluations of one plan are allowed if each uses its own workspace
  * and the plan's timing is off (timed evaluations append to one record list).
- * Errors: DSS_E_INVALID (NULL pointers), DSS_E_SHAPE (signal smaller than the
- * receptive field, workspace too small), DSS_E_HIP (launch failure). */
+ * Errors: DSS_E_INVALID (NULL plan, signal or out; plan of another device),
+ * DSS_E_SHAPE (signal smaller than the receptive field, workspace too small),
+ * DSS_E_NOMEM (the plan's own workspace could not be allocated), DSS_E_HIP
+ * (launch failure). */
 dss_status dss_eval_dense(dss_plan_t plan, const void* signal, int32_t H, int32_t W, float* out,
                           void* workspace, int64_t workspace_bytes, hipStream_t stream);
 
@@ -210,7 +224,8 @@ dss_status dss_eval_dense(dss_plan_t plan, const void* signal, int32_t H, int32_
  *              network's output on the window whose top-left sample is
  *              (step_h * i, step_w * j)
  *   workspace  device scratch of at least dss_geometry.workspace_bytes bytes for
- *              this ell (256-byte aligned), owned by the caller
+ *              this ell (256-byte aligned), owned by the caller, or NULL for the
+ *              plan's own workspace
  * Errors: as dss_eval_dense, and DSS_E_INVALID if ell is outside 0..L. */
 dss_status dss_eval_mixed(dss_plan_t plan, const void* signal, int32_t H, int32_t W, int32_t ell,
                           float* out, void* workspace, int64_t workspace_bytes, hipStream_t stream);
@@ -258,7 +273,7 @@ dss_status dss_plan_stride_geometry(dss_plan_t plan, int32_t count, int64_t* wor
  *   out        device, binary32 [out_c][H - B_h + 1][W - B_w + 1] (the layout of
  *              dss_eval_dense); only the batch's positions are written
  *   workspace  device scratch of at least dss_plan_stride_geometry(count) bytes,
- *              256-byte aligned
+ *              256-byte aligned, or NULL for the plan's own workspace
  * Errors: DSS_E_INVALID (NULL pointers, window range, device), DSS_E_SHAPE
  * (signal smaller than the receptive field, workspace too small), DSS_E_HIP. */
 dss_status dss_eval_stride(dss_plan_t plan, const void* signal, int32_t H, int32_t W, int64_t first,
@@ -291,7 +306,7 @@ dss_status dss_plan_dilate_geometry(dss_plan_t plan, int32_t H, int32_t W, int32
  *   signal     device, [in_c][H][W] in the plan's dtype
  *   out        device, binary32 [C_j][V_j,h][V_j,w] (for j = L: [out_c][H - B_h + 1][W - B_w + 1])
  *   workspace  device scratch of at least the bytes dss_plan_dilate_geometry gives
- *              (256-byte aligned)
+ *              (256-byte aligned), or NULL for the plan's own workspace
  * Errors: as dss_eval_dense, and DSS_E_INVALID if j is outside 0..L. */
 dss_status dss_eval_dilate(dss_plan_t plan, const void* signal, int32_t H, int32_t W, int32_t j,
                            float* out, void* workspace, int64_t workspace_bytes, hipStream_t stream);
@@ -334,7 +349,8 @@ dss_status dss_plan_backward_geometry(dss_plan_t plan, int32_t H, int32_t W, int
  *                concatenated; written, not accumulated
  *   grad_bias    device, binary32: each convolution's [cout], concatenated
  *   grad_signal  device, binary32 [in_c][H][W], or NULL to skip it
- *   workspace    device scratch of dss_plan_backward_geometry bytes (256-byte aligned)
+ *   workspace    device scratch of dss_plan_backward_geometry bytes (256-byte aligned),
+ *                or NULL for the plan's own workspace
  * Errors: DSS_E_UNSUPPORTED for bfloat16 plans; otherwise as dss_eval_dense. */
 dss_status dss_backward_dense(dss_plan_t plan, const void* signal, int32_t H, int32_t W,
                               const float* grad_out, float* grad_weight, float* grad_bias,
@@ -370,7 +386,9 @@ dss_status dss_defrag(int32_t k_h, int32_t k_w, int32_t S_h, int32_t S_w, int32_
 typedef struct dss_launch_record {
     const char* kernel;     /* static string: kernel family and variant */
     int32_t chain_layer;    /* 1..L, 0 for stuffing, L+1 for defragmentation */
-    int32_t reserved;
+    int32_t tile_mode;      /* convolutions on the MFMA kernel: 0 spatial tiles of one fragment,
+                               1 flat tiles (the fragment batch read as one sequence of samples),
+                               2 dilated tiles (one phase of one signal); -1 for every other launch */
     double ms;              /* device time between HIP events around the launch */
     double flops;           /* algorithmic flops of the launch (0 for data movement) */
     double bytes;           /* algorithmic bytes of the launch (each tensor once) */

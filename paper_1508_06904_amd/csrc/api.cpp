@@ -301,6 +301,9 @@ static void free_plan_memory(dss_plan* p) {
         }
     for (hipEvent_t e : p->events) (void)hipEventDestroy(e);
     p->events.clear();
+    if (p->own_ws) (void)hipFree(p->own_ws);
+    p->own_ws = nullptr;
+    p->own_ws_bytes = 0;
 }
 
 extern "C" void dss_plan_destroy(dss_plan_t plan) {
@@ -386,7 +389,7 @@ extern "C" dss_status dss_plan_timings(dss_plan_t plan, dss_launch_record* recor
         if (e != hipSuccess) return hip_fail(e, "hipEventElapsedTime");
         records[i].kernel = r.name;
         records[i].chain_layer = r.layer;
-        records[i].reserved = 0;
+        records[i].tile_mode = r.tile_mode;
         records[i].ms = ms;
         records[i].flops = r.flops;
         records[i].bytes = r.bytes;
@@ -402,7 +405,10 @@ struct Timer {
     hipStream_t s;
     int next = 0;
     bool on;
-    Timer(dss_plan* p_, hipStream_t s_) : p(p_), s(s_), on(p_->timing) { next = 2 * (int)p->recs.size(); }
+    // timed: false for evaluations that must not create events (allocation-free entry points)
+    Timer(dss_plan* p_, hipStream_t s_, bool timed = true) : p(p_), s(s_), on(timed && p_->timing) {
+        next = 2 * (int)p->recs.size();
+    }
     hipError_t event(int* idx) {
         if (next >= (int)p->events.size()) {
             hipEvent_t ev;
@@ -414,9 +420,9 @@ struct Timer {
         return hipEventRecord(p->events[*idx], s);
     }
     template <class F>
-    hipError_t run(const char* name, int layer, double flops, double bytes, F&& launch) {
+    hipError_t run(const char* name, int layer, double flops, double bytes, F&& launch, int tile_mode = -1) {
         if (!on) return launch();
-        LaunchRec r{name, layer, flops, bytes, 0, 0};
+        LaunchRec r{name, layer, flops, bytes, 0, 0, tile_mode};
         hipError_t e = event(&r.ev0);
         if (e != hipSuccess) return e;
         e = launch();
@@ -476,16 +482,19 @@ static dss_status run_layers(dss_plan* p, const Geom& G, int upto, char* const b
             const double bytes = (double)Fin * lg.Uin_h * lg.Uin_w * c.cin * dtype_size(cdt) +
                                  (double)Fin * lg.E_h * lg.E_w * c.cout * dtype_size(tout) +
                                  (double)c.cout * c.cin * c.c_h * c.c_w * es;
-            e = T.run(conv_name(pc, tout), j, flops, bytes, [&]() -> hipError_t {
-                if (pc.impl == CONV_MFMA_F32)
-                    return launch_conv_mfma_f32((const float*)cur, Fin, lg.Uin_h, lg.Uin_w, lg.dil_h, lg.dil_w, pc,
-                                                (float*)dst, stream);
-                if (pc.impl == CONV_MFMA_BF16)
-                    return launch_conv_mfma_bf16(tout, (const uint16_t*)cur, Fin, lg.Uin_h, lg.Uin_w, lg.dil_h,
-                                                 lg.dil_w, pc, dst, stream);
-                return launch_conv_direct(cdt, tout, cur, Fin, lg.Uin_h, lg.Uin_w, lg.dil_h, lg.dil_w, c.cin, pc, dst,
-                                          stream);
-            });
+            e = T.run(
+                conv_name(pc, tout), j, flops, bytes,
+                [&]() -> hipError_t {
+                    if (pc.impl == CONV_MFMA_F32)
+                        return launch_conv_mfma_f32((const float*)cur, Fin, lg.Uin_h, lg.Uin_w, lg.dil_h, lg.dil_w,
+                                                    pc, (float*)dst, stream);
+                    if (pc.impl == CONV_MFMA_BF16)
+                        return launch_conv_mfma_bf16(tout, (const uint16_t*)cur, Fin, lg.Uin_h, lg.Uin_w, lg.dil_h,
+                                                     lg.dil_w, pc, dst, stream);
+                    return launch_conv_direct(cdt, tout, cur, Fin, lg.Uin_h, lg.Uin_w, lg.dil_h, lg.dil_w, c.cin, pc,
+                                              dst, stream);
+                },
+                T.on ? mfma_tile_mode(pc, Fin, lg.Uin_h, lg.Uin_w, lg.dil_h, lg.dil_w) : -1);
             if (e != hipSuccess) return hip_fail(e, "conv launch");
             which ^= 1;
             cur = dst;
@@ -542,16 +551,8 @@ static dss_status run_chain(dss_plan* p, const Geom& G, const void* signal, int 
     return run_layers(p, G, upto, buf, stream, T, cur_out, cur_dt);
 }
 
-static dss_status check_eval_args(dss_plan_t plan, const void* signal, const void* out, void* workspace,
-                                  int64_t workspace_bytes, int32_t H, int32_t W, int32_t ell, Geom* G) {
-    if (!plan || !signal || !out) return fail(DSS_E_INVALID, "NULL plan, signal or out");
-    dss_status s = compute_geometry(plan->chain, plan->dtype, H, W, ell, G);
-    if (s != DSS_OK) return s;
-    if (!workspace) return fail(DSS_E_INVALID, "NULL workspace (need %lld bytes)", (long long)G->ws_bytes);
-    if (workspace_bytes < G->ws_bytes)
-        return fail(DSS_E_SHAPE, "workspace of %lld bytes is smaller than the %lld bytes needed",
-                    (long long)workspace_bytes, (long long)G->ws_bytes);
-    if (((uintptr_t)workspace & 255u) != 0) return fail(DSS_E_INVALID, "workspace is not 256-byte aligned");
+// Checks that the plan belongs to the current device.
+static dss_status check_device(const dss_plan* plan) {
     int cur = -1;
     hipError_t e = hipGetDevice(&cur);
     if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
@@ -560,15 +561,69 @@ static dss_status check_eval_args(dss_plan_t plan, const void* signal, const voi
     return DSS_OK;
 }
 
-extern "C" dss_status dss_eval_mixed(dss_plan_t plan, const void* signal, int32_t H, int32_t W, int32_t ell,
-                                     float* out, void* workspace, int64_t workspace_bytes, hipStream_t stream) {
-    Geom G;
-    dss_status s = check_eval_args(plan, signal, out, workspace, workspace_bytes, H, W, ell, &G);
+// The workspace an evaluation runs in: the caller's (at least `need` bytes,
+// 256-byte aligned), or, for workspace == NULL, the plan's own buffer, grown to
+// `need` bytes if it is smaller.  Growing first waits for the device, since work
+// enqueued earlier may still use the old buffer.  Called after every other
+// argument check, so a failure here (DSS_E_NOMEM, DSS_E_HIP) still leaves
+// nothing enqueued.
+static dss_status resolve_workspace(dss_plan* plan, void* workspace, int64_t workspace_bytes, int64_t need,
+                                    char** ws) {
+    if (workspace) {
+        if (workspace_bytes < need)
+            return fail(DSS_E_SHAPE, "workspace of %lld bytes is smaller than the %lld bytes needed",
+                        (long long)workspace_bytes, (long long)need);
+        if (((uintptr_t)workspace & 255u) != 0) return fail(DSS_E_INVALID, "workspace is not 256-byte aligned");
+        *ws = (char*)workspace;
+        return DSS_OK;
+    }
+    std::lock_guard<std::mutex> lock(plan->ws_mu);
+    if (plan->own_ws_bytes < need) {
+        if (plan->own_ws) {
+            hipError_t e = hipDeviceSynchronize();
+            if (e != hipSuccess) return hip_fail(e, "waiting for the device before growing the plan's workspace");
+            e = hipFree(plan->own_ws);
+            plan->own_ws = nullptr;
+            plan->own_ws_bytes = 0;
+            if (e != hipSuccess) return hip_fail(e, "freeing the plan's workspace");
+        }
+        const int64_t bytes = std::max<int64_t>(need, 256);
+        hipError_t e = hipMalloc(&plan->own_ws, (size_t)bytes);
+        if (e != hipSuccess) {
+            plan->own_ws = nullptr;
+            return hip_fail(e, "allocating the plan's workspace");
+        }
+        plan->own_ws_bytes = bytes;
+    }
+    *ws = (char*)plan->own_ws;
+    return DSS_OK;
+}
+
+static dss_status check_eval_args(dss_plan_t plan, const void* signal, const void* out, void* workspace,
+                                  int64_t workspace_bytes, int32_t H, int32_t W, int32_t ell, Geom* G, char** ws) {
+    dss_status s = dss::eval_prepare(plan, signal, out, H, W, ell, G);
     if (s != DSS_OK) return s;
-    Timer T(plan, stream);
+    if (workspace && workspace_bytes < G->ws_bytes)
+        return fail(DSS_E_SHAPE, "workspace of %lld bytes is smaller than the %lld bytes needed",
+                    (long long)workspace_bytes, (long long)G->ws_bytes);
+    return resolve_workspace(plan, workspace, workspace_bytes, G->ws_bytes, ws);
+}
+
+namespace dss {
+
+dss_status eval_prepare(dss_plan_t plan, const void* signal, const void* out, int H, int W, int ell, Geom* G) {
+    if (!plan || !signal || !out) return fail(DSS_E_INVALID, "NULL plan, signal or out");
+    dss_status s = compute_geometry(plan->chain, plan->dtype, H, W, ell, G);
+    if (s != DSS_OK) return s;
+    return check_device(plan);
+}
+
+dss_status eval_run(dss_plan_t plan, const Geom& G, const void* signal, float* out, char* ws, hipStream_t stream,
+                    bool timed) {
+    Timer T(plan, stream, timed);
     void* cur = nullptr;
     dss_dtype cdt;
-    s = run_chain(plan, G, signal, plan->chain.L(), (char*)workspace, stream, T, &cur, &cdt);
+    dss_status s = run_chain(plan, G, signal, plan->chain.L(), ws, stream, T, &cur, &cdt);
     if (s != DSS_OK) return s;
     const Chain& ch = plan->chain;
     // Defrag_{k*_L / k*_ell}, then keep the first out_h x out_w samples (this is
@@ -584,6 +639,17 @@ extern "C" dss_status dss_eval_mixed(dss_plan_t plan, const void* signal, int32_
     return DSS_OK;
 }
 
+}  // namespace dss
+
+extern "C" dss_status dss_eval_mixed(dss_plan_t plan, const void* signal, int32_t H, int32_t W, int32_t ell,
+                                     float* out, void* workspace, int64_t workspace_bytes, hipStream_t stream) {
+    Geom G;
+    char* ws = nullptr;
+    dss_status s = check_eval_args(plan, signal, out, workspace, workspace_bytes, H, W, ell, &G, &ws);
+    if (s != DSS_OK) return s;
+    return eval_run(plan, G, signal, out, ws, stream, true);
+}
+
 extern "C" dss_status dss_eval_dense(dss_plan_t plan, const void* signal, int32_t H, int32_t W, float* out,
                                      void* workspace, int64_t workspace_bytes, hipStream_t stream) {
     return dss_eval_mixed(plan, signal, H, W, 0, out, workspace, workspace_bytes, stream);
@@ -592,14 +658,16 @@ extern "C" dss_status dss_eval_dense(dss_plan_t plan, const void* signal, int32_
 extern "C" dss_status dss_eval_slide(dss_plan_t plan, const void* signal, int32_t H, int32_t W, int32_t ell,
                                      int32_t j, float* out, void* workspace, int64_t workspace_bytes,
                                      hipStream_t stream) {
+    if (plan && (j < 0 || j > plan->chain.L()))
+        return fail(DSS_E_INVALID, "chain layer %d out of range 0..%d", j, plan->chain.L());
     Geom G;
-    dss_status s = check_eval_args(plan, signal, out, workspace, workspace_bytes, H, W, ell, &G);
+    char* ws = nullptr;
+    dss_status s = check_eval_args(plan, signal, out, workspace, workspace_bytes, H, W, ell, &G, &ws);
     if (s != DSS_OK) return s;
-    if (j < 0 || j > plan->chain.L()) return fail(DSS_E_INVALID, "chain layer %d out of range 0..%d", j, plan->chain.L());
     Timer T(plan, stream);
     void* cur = nullptr;
     dss_dtype cdt;
-    s = run_chain(plan, G, signal, j, (char*)workspace, stream, T, &cur, &cdt);
+    s = run_chain(plan, G, signal, j, ws, stream, T, &cur, &cdt);
     if (s != DSS_OK) return s;
     const Chain& ch = plan->chain;
     const int F = j == 0 ? 1 : G.L[j - 1].Fout_h * G.L[j - 1].Fout_w;
@@ -655,19 +723,18 @@ extern "C" dss_status dss_eval_stride(dss_plan_t plan, const void* signal, int32
     Geom G;
     dss_status s = compute_stride_geometry(ch, plan->dtype, count, &G);
     if (s != DSS_OK) return s;
-    if (!workspace) return fail(DSS_E_INVALID, "NULL workspace (need %lld bytes)", (long long)G.ws_bytes);
-    if (workspace_bytes < G.ws_bytes)
+    if (workspace && workspace_bytes < G.ws_bytes)
         return fail(DSS_E_SHAPE, "workspace of %lld bytes is smaller than the %lld bytes needed",
                     (long long)workspace_bytes, (long long)G.ws_bytes);
-    if (((uintptr_t)workspace & 255u) != 0) return fail(DSS_E_INVALID, "workspace is not 256-byte aligned");
-    int cur_dev = -1;
-    hipError_t e = hipGetDevice(&cur_dev);
-    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
-    if (cur_dev != plan->device)
-        return fail(DSS_E_INVALID, "plan belongs to device %d but device %d is current", plan->device, cur_dev);
+    s = check_device(plan);
+    if (s != DSS_OK) return s;
+    char* ws = nullptr;
+    s = resolve_workspace(plan, workspace, workspace_bytes, G.ws_bytes, &ws);
+    if (s != DSS_OK) return s;
+    hipError_t e;
 
     Timer T(plan, stream);
-    char* const buf[2] = {(char*)workspace, (char*)workspace + G.buf_bytes};
+    char* const buf[2] = {ws, ws + G.buf_bytes};
     const double es = (double)dtype_size(plan->dtype);
     const double pbytes = 2.0 * count * (double)ch.B_h * ch.B_w * ch.in_c * es;
     e = T.run("patch_pack", 0, 0.0, pbytes, [&] {
@@ -730,20 +797,19 @@ extern "C" dss_status dss_eval_dilate(dss_plan_t plan, const void* signal, int32
     Geom G;
     dss_status s = compute_dilate_geometry(ch, plan->dtype, H, W, &G);
     if (s != DSS_OK) return s;
-    if (!workspace) return fail(DSS_E_INVALID, "NULL workspace (need %lld bytes)", (long long)G.ws_bytes);
-    if (workspace_bytes < G.ws_bytes)
+    if (workspace && workspace_bytes < G.ws_bytes)
         return fail(DSS_E_SHAPE, "workspace of %lld bytes is smaller than the %lld bytes needed",
                     (long long)workspace_bytes, (long long)G.ws_bytes);
-    if (((uintptr_t)workspace & 255u) != 0) return fail(DSS_E_INVALID, "workspace is not 256-byte aligned");
-    int cur_dev = -1;
-    hipError_t e = hipGetDevice(&cur_dev);
-    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
-    if (cur_dev != plan->device)
-        return fail(DSS_E_INVALID, "plan belongs to device %d but device %d is current", plan->device, cur_dev);
+    s = check_device(plan);
+    if (s != DSS_OK) return s;
+    char* ws = nullptr;
+    s = resolve_workspace(plan, workspace, workspace_bytes, G.ws_bytes, &ws);
+    if (s != DSS_OK) return s;
+    hipError_t e;
     Timer T(plan, stream);
     void* cur = nullptr;
     dss_dtype cdt;
-    s = run_chain(plan, G, signal, j, (char*)workspace, stream, T, &cur, &cdt);   // D = H x W: a plain pack
+    s = run_chain(plan, G, signal, j, ws, stream, T, &cur, &cdt);   // D = H x W: a plain pack
     if (s != DSS_OK) return s;
     const int h = j == 0 ? H : G.L[j - 1].U_h;
     const int w = j == 0 ? W : G.L[j - 1].U_w;
@@ -887,20 +953,18 @@ extern "C" dss_status dss_backward_dense(dss_plan_t plan, const void* signal, in
     BwdLayout B;
     dss_status s = backward_layout(ch, H, W, grad_signal != nullptr, &B, plan);
     if (s != DSS_OK) return s;
-    if (!workspace) return fail(DSS_E_INVALID, "NULL workspace (need %lld bytes)", (long long)B.total);
-    if (workspace_bytes < B.total)
+    if (workspace && workspace_bytes < B.total)
         return fail(DSS_E_SHAPE, "workspace of %lld bytes is smaller than the %lld bytes needed",
                     (long long)workspace_bytes, (long long)B.total);
-    if (((uintptr_t)workspace & 255u) != 0) return fail(DSS_E_INVALID, "workspace is not 256-byte aligned");
-    int cur_dev = -1;
-    hipError_t e = hipGetDevice(&cur_dev);
-    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
-    if (cur_dev != plan->device)
-        return fail(DSS_E_INVALID, "plan belongs to device %d but device %d is current", plan->device, cur_dev);
+    s = check_device(plan);
+    if (s != DSS_OK) return s;
+    char* ws = nullptr;
+    s = resolve_workspace(plan, workspace, workspace_bytes, B.total, &ws);
+    if (s != DSS_OK) return s;
+    hipError_t e;
 
     const Geom& G = B.G;
     const int L = ch.L();
-    char* ws = (char*)workspace;
     auto A = [&](int j) { return (float*)(ws + B.a_off[j]); };
     auto Cv = [&](int j) { return (float*)(ws + B.c_off[j]); };
     float* gb[2] = {(float*)(ws + B.g_off[0]), (float*)(ws + B.g_off[1])};

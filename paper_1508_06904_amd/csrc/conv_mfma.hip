@@ -642,6 +642,15 @@ PlanConv mfma_launch_variant(const PlanConv& pc, int F, int Hin, int Win, int di
     return alt;
 }
 
+int mfma_tile_mode(const PlanConv& pc, int F, int Hin, int Win, int dil_h, int dil_w, int pad_h, int pad_w) {
+    if (pc.impl == CONV_DIRECT) return -1;
+    if (dil_h * dil_w > 1) return 2;
+    const bool padded = pad_h > 0 || pad_w > 0;
+    const LaunchShape L = launch_shape(256, pc.impl == CONV_MFMA_BF16, F, Hin + 2 * pad_h, Win + 2 * pad_w, dil_h,
+                                       dil_w, pc.fh, pc.fw, pc.cout_pad / pc.bn, !padded);
+    return L.flat ? 1 : 0;
+}
+
 template <bool BF16, typename Tout, int WGM, int WGN, int MT, int NT>
 static hipError_t run_mfma(const void* in, int F, int Hin, int Win, int dil_h, int dil_w, int pad_h, int pad_w,
                            const PlanConv& pc, void* out, hipStream_t s) {

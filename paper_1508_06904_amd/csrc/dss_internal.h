@@ -6,6 +6,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -95,6 +96,9 @@ struct PlanConv {
 // The variant a launch over F fragments of Hin x Win (taps dil apart) should use.
 PlanConv mfma_launch_variant(const PlanConv& pc, int F, int Hin, int Win, int dil_h, int dil_w, int pad_h = 0,
                              int pad_w = 0);
+// How that launch tiles its output: 0 spatial, 1 flat, 2 dilated (dss_launch_record.tile_mode),
+// -1 for the direct kernel.
+int mfma_tile_mode(const PlanConv& pc, int F, int Hin, int Win, int dil_h, int dil_w, int pad_h = 0, int pad_w = 0);
 
 // Host-side description of a weight-gradient launch (backward.hip).
 struct WgradPlan {
@@ -112,6 +116,7 @@ struct LaunchRec {
     int layer;
     double flops, bytes;
     int ev0, ev1;
+    int tile_mode;      // dss_launch_record.tile_mode
 };
 
 }  // namespace dss
@@ -126,9 +131,24 @@ struct dss_plan {
     bool timing = false;
     std::vector<hipEvent_t> events;
     std::vector<dss::LaunchRec> recs;
+    // workspace of the evaluations that pass none: allocated on first need,
+    // grown to the largest request, freed by dss_plan_destroy
+    std::mutex ws_mu;
+    void* own_ws = nullptr;
+    int64_t own_ws_bytes = 0;
 };
 
 namespace dss {
+
+// ------------------------------------------------------------------ evaluation steps (api.cpp)
+// Argument checks and geometry of a dense (ell = 0) or mixed evaluation, and
+// the plan-device check; nothing is enqueued.
+dss_status eval_prepare(dss_plan_t plan, const void* signal, const void* out, int H, int W, int ell, Geom* G);
+// The evaluation itself in the workspace ws (at least G.ws_bytes bytes, 256-byte
+// aligned).  timed = false records no launch events even with the plan's timing
+// on (no event is created).
+dss_status eval_run(dss_plan_t plan, const Geom& G, const void* signal, float* out, char* ws, hipStream_t stream,
+                    bool timed);
 
 // ------------------------------------------------------------------ kernel launchers
 // Element types: binary32 activations are float, bfloat16 activations uint16_t bits.
@@ -159,6 +179,7 @@ hipError_t launch_pool_stride(dss_dtype dt, const void* in, int E_h, int E_w, in
                               void* out, hipStream_t s);
 hipError_t launch_defrag_trim(dss_dtype dt, const void* in, int K_h, int K_w, int U_h, int U_w, int C,
                               float* out, int O_h, int O_w, hipStream_t s);
+
 hipError_t launch_to_planar(dss_dtype dt, const void* in, int F, int h, int w, int C, float* out,
                             hipStream_t s);
 hipError_t launch_frag_planar(int elem_bytes, bool inverse, const void* in, int k_h, int k_w, int S_h,

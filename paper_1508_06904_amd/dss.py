@@ -61,7 +61,7 @@ class LayerGeometry(ctypes.Structure):
 
 
 class LaunchRecord(ctypes.Structure):
-    _fields_ = [("kernel", ctypes.c_char_p), ("chain_layer", ctypes.c_int32), ("reserved", ctypes.c_int32),
+    _fields_ = [("kernel", ctypes.c_char_p), ("chain_layer", ctypes.c_int32), ("tile_mode", ctypes.c_int32),
                 ("ms", ctypes.c_double), ("flops", ctypes.c_double), ("bytes", ctypes.c_double)]
 
 
@@ -208,6 +208,37 @@ def _ptr(t):
     return ctypes.c_void_p(t.data_ptr())
 
 
+def _check_buffer(t, what, dtype, numel=None, min_numel=None, device=None):
+    """Raises ValueError unless t is a contiguous CUDA tensor of `dtype` (a torch
+    dtype, or an element size in bytes) with exactly `numel` (or at least
+    `min_numel`) elements, on `device` if given.  The C ABI takes no sizes for
+    these buffers, so a wrong one would mean out-of-bounds device accesses."""
+    import torch
+    if not isinstance(t, torch.Tensor) or not t.is_cuda or not t.is_contiguous():
+        raise ValueError("%s must be a contiguous CUDA tensor" % what)
+    if isinstance(dtype, int):
+        if t.element_size() != dtype or t.is_complex():
+            raise ValueError("%s must have %d-byte elements (got %s)" % (what, dtype, t.dtype))
+    elif t.dtype != dtype:
+        raise ValueError("%s must be %s (got %s)" % (what, dtype, t.dtype))
+    if device is not None and t.device != device:
+        raise ValueError("%s is on %s, the signal on %s" % (what, t.device, device))
+    if numel is not None and t.numel() != numel:
+        raise ValueError("%s has %d elements, %d expected" % (what, t.numel(), numel))
+    if min_numel is not None and t.numel() < min_numel:
+        raise ValueError("%s has %d elements, at least %d needed" % (what, t.numel(), min_numel))
+
+
+def _workspace_args(ws, device):
+    """(pointer, bytes) of a caller workspace, or (NULL, 0): the plan's own."""
+    if ws is None:
+        return ctypes.c_void_p(None), 0
+    import torch
+    if not isinstance(ws, torch.Tensor) or not ws.is_cuda or not ws.is_contiguous() or ws.device != device:
+        raise ValueError("workspace must be a contiguous CUDA tensor on the signal's device")
+    return _ptr(ws), ws.numel() * ws.element_size()
+
+
 class Plan:
     """A dss plan on the current device."""
 
@@ -221,7 +252,6 @@ class Plan:
         _check(lib().dss_plan_create(la.arr, la.n, ndim, in_channels, DTYPES[dtype], ctypes.byref(h)),
                "dss_plan_create")
         self.handle = h
-        self._ws = None
 
     @classmethod
     def from_workload(cls, wl):
@@ -249,15 +279,12 @@ class Plan:
         return g.as_dict()
 
     def workspace(self, H, W, device=None, ell=0):
-        """A device workspace (uint8 tensor) large enough for an H x W signal at
-        mixed level ell; one buffer per plan, reused by every call that passes no
-        workspace, so calls that run concurrently pass workspaces of their own."""
+        """A new device workspace (uint8 tensor) large enough for dss_eval_dense /
+        dss_eval_mixed on an H x W signal at mixed level ell.  Calls that pass no
+        workspace use the plan's own one inside the library instead."""
         import torch
         need = self.geometry(H, W, ell)["workspace_bytes"]
-        if self._ws is None or self._ws.numel() < need:
-            self._ws = None
-            self._ws = torch.empty(max(need, 256), dtype=torch.uint8, device=device or "cuda")
-        return self._ws
+        return torch.empty(max(need, 256), dtype=torch.uint8, device=device or "cuda")
 
     def _check_signal(self, signal):
         import torch
@@ -274,9 +301,10 @@ class Plan:
         g = self.geometry(H, W)
         if out is None:
             out = torch.empty((g["out_c"], g["out_h"], g["out_w"]), dtype=torch.float32, device=signal.device)
-        ws = workspace if workspace is not None else self.workspace(H, W, signal.device)
-        _check(lib().dss_eval_dense(self.handle, _ptr(signal), H, W, _ptr(out), _ptr(ws), ws.numel(),
-                                    _stream(stream)), "dss_eval_dense")
+        _check_buffer(out, "out", torch.float32, g["out_c"] * g["out_h"] * g["out_w"], device=signal.device)
+        wp, wb = _workspace_args(workspace, signal.device)
+        _check(lib().dss_eval_dense(self.handle, _ptr(signal), H, W, _ptr(out), wp, wb, _stream(stream)),
+               "dss_eval_dense")
         return out
 
     def eval_mixed(self, signal, ell, out=None, workspace=None, stream=None):
@@ -286,9 +314,10 @@ class Plan:
         g = self.geometry(H, W, ell)
         if out is None:
             out = torch.empty((g["out_c"], g["out_h"], g["out_w"]), dtype=torch.float32, device=signal.device)
-        ws = workspace if workspace is not None else self.workspace(H, W, signal.device, ell)
-        _check(lib().dss_eval_mixed(self.handle, _ptr(signal), H, W, ell, _ptr(out), _ptr(ws), ws.numel(),
-                                    _stream(stream)), "dss_eval_mixed")
+        _check_buffer(out, "out", torch.float32, g["out_c"] * g["out_h"] * g["out_w"], device=signal.device)
+        wp, wb = _workspace_args(workspace, signal.device)
+        _check(lib().dss_eval_mixed(self.handle, _ptr(signal), H, W, ell, _ptr(out), wp, wb, _stream(stream)),
+               "dss_eval_mixed")
         return out
 
     def eval_slide(self, signal, j, out=None, workspace=None, stream=None, ell=0):
@@ -299,9 +328,11 @@ class Plan:
         if out is None:
             out = torch.empty((lg["F"], lg["channels"], lg["U_h"], lg["U_w"]), dtype=torch.float32,
                               device=signal.device)
-        ws = workspace if workspace is not None else self.workspace(H, W, signal.device, ell)
-        _check(lib().dss_eval_slide(self.handle, _ptr(signal), H, W, ell, j, _ptr(out), _ptr(ws), ws.numel(),
-                                    _stream(stream)), "dss_eval_slide")
+        _check_buffer(out, "out", torch.float32, lg["F"] * lg["channels"] * lg["U_h"] * lg["U_w"],
+                      device=signal.device)
+        wp, wb = _workspace_args(workspace, signal.device)
+        _check(lib().dss_eval_slide(self.handle, _ptr(signal), H, W, ell, j, _ptr(out), wp, wb, _stream(stream)),
+               "dss_eval_slide")
         return out
 
     def dilate_geometry(self, H, W, j):
@@ -318,14 +349,14 @@ class Plan:
         _, H, W = signal.shape
         n_chain = self.geometry(H, W)["n_chain"]
         j = n_chain if j is None else j
-        vh, vw, need, _ = self.dilate_geometry(H, W, j)
+        vh, vw, _, _ = self.dilate_geometry(H, W, j)
+        C = self.in_channels if j == 0 else self.layer_geometry(H, W, j)["channels"]
         if out is None:
-            C = self.in_channels if j == 0 else self.layer_geometry(H, W, j)["channels"]
             out = torch.empty((C, vh, vw), dtype=torch.float32, device=signal.device)
-        if workspace is None:
-            workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=signal.device)
-        _check(lib().dss_eval_dilate(self.handle, _ptr(signal), H, W, j, _ptr(out), _ptr(workspace),
-                                     workspace.numel(), _stream(stream)), "dss_eval_dilate")
+        _check_buffer(out, "out", torch.float32, C * vh * vw, device=signal.device)
+        wp, wb = _workspace_args(workspace, signal.device)
+        _check(lib().dss_eval_dilate(self.handle, _ptr(signal), H, W, j, _ptr(out), wp, wb, _stream(stream)),
+               "dss_eval_dilate")
         return out
 
     def backward_geometry(self, H, W, with_signal_grad=True):
@@ -344,20 +375,21 @@ class Plan:
         import torch
         self._check_signal(signal)
         _, H, W = signal.shape
-        need, wf, bf, _ = self.backward_geometry(H, W, with_signal_grad)
+        _, wf, bf, _ = self.backward_geometry(H, W, with_signal_grad)
+        g = self.geometry(H, W)
         dev = signal.device
         if grad_weight is None:
             grad_weight = torch.empty(max(wf, 1), dtype=torch.float32, device=dev)
         if grad_bias is None:
             grad_bias = torch.empty(max(bf, 1), dtype=torch.float32, device=dev)
         gx = torch.empty_like(signal) if with_signal_grad else None
-        if workspace is None:
-            workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=dev)
-        if not grad_out.is_cuda or grad_out.dtype != torch.float32 or not grad_out.is_contiguous():
-            raise ValueError("grad_out must be a contiguous CUDA float32 tensor")
+        _check_buffer(grad_out, "grad_out", torch.float32, g["out_c"] * g["out_h"] * g["out_w"], device=dev)
+        _check_buffer(grad_weight, "grad_weight", torch.float32, min_numel=wf, device=dev)
+        _check_buffer(grad_bias, "grad_bias", torch.float32, min_numel=bf, device=dev)
+        wp, wb = _workspace_args(workspace, dev)
         _check(lib().dss_backward_dense(self.handle, _ptr(signal), H, W, _ptr(grad_out), _ptr(grad_weight),
-                                        _ptr(grad_bias), _ptr(gx) if gx is not None else None, _ptr(workspace),
-                                        workspace.numel(), _stream(stream)), "dss_backward_dense")
+                                        _ptr(grad_bias), _ptr(gx) if gx is not None else None, wp, wb,
+                                        _stream(stream)), "dss_backward_dense")
         return grad_weight, grad_bias, gx
 
     def split_grads(self, grad_weight, grad_bias):
@@ -387,14 +419,13 @@ class Plan:
         import torch
         self._check_signal(signal)
         _, H, W = signal.shape
+        g = self.geometry(H, W)
         if out is None:
-            g = self.geometry(H, W)
             out = torch.zeros((g["out_c"], g["out_h"], g["out_w"]), dtype=torch.float32, device=signal.device)
-        if workspace is None:
-            need = self.stride_geometry(count)[0]
-            workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=signal.device)
-        _check(lib().dss_eval_stride(self.handle, _ptr(signal), H, W, first, count, _ptr(out), _ptr(workspace),
-                                     workspace.numel(), _stream(stream)), "dss_eval_stride")
+        _check_buffer(out, "out", torch.float32, g["out_c"] * g["out_h"] * g["out_w"], device=signal.device)
+        wp, wb = _workspace_args(workspace, signal.device)
+        _check(lib().dss_eval_stride(self.handle, _ptr(signal), H, W, first, count, _ptr(out), wp, wb,
+                                     _stream(stream)), "dss_eval_stride")
         return out
 
     def set_timing(self, on=True):
@@ -406,16 +437,24 @@ class Plan:
         recs = (LaunchRecord * max(1, n.value))()
         _check(lib().dss_plan_timings(self.handle, recs, n.value, ctypes.byref(n)), "dss_plan_timings")
         return [{"kernel": r.kernel.decode(), "layer": r.chain_layer, "ms": r.ms, "flops": r.flops,
-                 "bytes": r.bytes} for r in recs[: n.value]]
+                 "bytes": r.bytes, "tile_mode": r.tile_mode} for r in recs[: n.value]]
 
 
 def frag(x, k_h, k_w, S_h, S_w, out=None, stream=None):
     """dss_frag on a CUDA tensor [S_h*S_w][C][H][W] of 4- or 2-byte elements."""
     import torch
+    if not isinstance(x, torch.Tensor) or x.dim() != 4 or x.element_size() not in (2, 4):
+        raise ValueError("x must be a 4-D tensor [S_h*S_w][C][H][W] of 2- or 4-byte elements")
     S, C, H, W = x.shape
+    if S != S_h * S_w:
+        raise ValueError("x holds %d fragments, S_h * S_w = %d" % (S, S_h * S_w))
+    _check_buffer(x, "x", x.element_size())
     dt = DSS_BF16 if x.element_size() == 2 else DSS_F32
     if out is None:
         out = torch.empty((k_h * S_h * k_w * S_w, C, H // k_h, W // k_w), dtype=x.dtype, device=x.device)
+    # extents that k does not divide are the library's DSS_E_SHAPE, before any access
+    if k_h > 0 and k_w > 0 and H % k_h == 0 and W % k_w == 0:
+        _check_buffer(out, "out", x.element_size(), S * C * H * W, device=x.device)
     _check(lib().dss_frag(k_h, k_w, S_h, S_w, C, H, W, dt, _ptr(x), _ptr(out), _stream(stream)), "dss_frag")
     return out
 
@@ -423,9 +462,15 @@ def frag(x, k_h, k_w, S_h, S_w, out=None, stream=None):
 def defrag(x, k_h, k_w, S_h, S_w, out=None, stream=None):
     """dss_defrag on a CUDA tensor [(k_h*S_h)*(k_w*S_w)][C][H][W]."""
     import torch
+    if not isinstance(x, torch.Tensor) or x.dim() != 4 or x.element_size() not in (2, 4):
+        raise ValueError("x must be a 4-D tensor [(k_h*S_h)*(k_w*S_w)][C][H][W] of 2- or 4-byte elements")
     F, C, H, W = x.shape
+    if F != k_h * S_h * k_w * S_w:
+        raise ValueError("x holds %d fragments, (k_h * S_h) * (k_w * S_w) = %d" % (F, k_h * S_h * k_w * S_w))
+    _check_buffer(x, "x", x.element_size())
     dt = DSS_BF16 if x.element_size() == 2 else DSS_F32
     if out is None:
         out = torch.empty((S_h * S_w, C, H * k_h, W * k_w), dtype=x.dtype, device=x.device)
+    _check_buffer(out, "out", x.element_size(), F * C * H * W, device=x.device)
     _check(lib().dss_defrag(k_h, k_w, S_h, S_w, C, H, W, dt, _ptr(x), _ptr(out), _stream(stream)), "dss_defrag")
     return out

@@ -121,6 +121,29 @@ def init_layers(arch, rng, bias=0.01, weight_kind="he"):
     return layers
 
 
+def sparse_integer_layers(layers, nonzeros, rng):
+    """The same layer shapes with exactly-representable parameters: every output
+    channel of conv t gets nonzeros[t] weights of +-1 at random positions of its
+    cin x fh x fw taps (the rest zero) and an integer bias in [-2, 2].  With
+    integer inputs bounded by b_0, every value and every partial sum of conv t
+    stays within b_t = nonzeros[t] * b_{t-1} + 2, so while
+    that is below 2^24 binary32 arithmetic computes the forward pass exactly."""
+    nz = iter(nonzeros)
+    out = []
+    for l in layers:
+        if l["kind"] != "conv":
+            out.append(l)
+            continue
+        d = next(nz)
+        K = l["cin"] * l["fh"] * l["fw"]
+        w = np.zeros((l["cout"], K), dtype=np.float32)
+        for o in range(l["cout"]):
+            w[o, rng.choice(K, size=d, replace=False)] = rng.choice([-1.0, 1.0], size=d)
+        out.append(dict(l, weight=w.reshape(l["cout"], l["cin"], l["fh"], l["fw"]),
+                        bias=rng.integers(-2, 3, size=l["cout"]).astype(np.float32)))
+    return out
+
+
 # --------------------------------------------------------------------------- inputs
 
 def uniform_image(rng, C, H, W):

@@ -9,8 +9,7 @@ import pytest
 import oracle
 from oracle import fragment as fr
 from paper_1508_06904_amd import dss, workloads as wl
-from tests.gpu_helpers import (assert_close, gpu_dense, kstar, log, oracle_layers, oracle_windows, sampled_windows,
-                               to_device)
+from tests.gpu_helpers import assert_close, gpu_dense, kstar, log, oracle_layers, oracle_windows, to_device
 from tests.test_oracle import HAND, _layers_from_json, chain_layers
 
 pytestmark = pytest.mark.gpu
@@ -293,20 +292,88 @@ def test_named_reduced_full_oracle(name, H, W, widths):
     assert_close(out, ref, BF16_TOL if w.dtype == "bf16" else F32_TOL, name)
 
 
-@pytest.mark.parametrize("name,max_phases", [("c2_1d_1m", None), ("c3_512", None), ("c4_hd", None), ("c5_4k", 64)])
-def test_named_full_size_sampled(name, max_phases):
-    """Full-size workloads in the benchmark's launch configuration; the oracle
-    checks a seeded sample covering the corners, edge midpoints and fragment phases."""
-    w = wl.make(name)
-    log("%s full size %s" % (name, w.x.shape))
-    out, plan = gpu_dense(w.layers, w.x, w.ndim, w.dtype)
-    g = plan.geometry(w.x.shape[1], w.x.shape[2])
-    assert out.shape == (g["out_c"], g["out_h"], g["out_w"])
-    assert np.all(np.isfinite(out))
-    i, j = sampled_windows(g["out_h"], g["out_w"], g["K_h"], g["K_w"], per_phase=1, max_phases=max_phases)
-    log("  checking %d windows" % len(i))
+# Full-size workloads in the benchmark's launch configuration.  The dense
+# evaluation of each runs once per session; the oracle then checks every window
+# of the 1-D workload, and on the 2-D frames 8 seeded windows of every fragment
+# phase pair (i mod K, j mod K) plus the corners and edge midpoints, and on the
+# 512x512 and HD frames every window of the last K rows and the last K columns
+# (the outputs whose fragments end next to the stuffed samples and in the
+# masked edge tiles).  The theorem (Sect. 4.3) makes the equality hold at every
+# window and phase.
+_FULL = {}
+
+
+def full_size(name):
+    """(workload, geometry, GPU dense output as float64) of a named workload."""
+    if name not in _FULL:
+        import torch
+        w = wl.make(name)
+        log("%s full size %s" % (name, w.x.shape))
+        plan = dss.Plan.from_workload(w)
+        out = plan.eval_dense(to_device(w.x, w.dtype))
+        torch.cuda.synchronize()
+        g = plan.geometry(w.x.shape[1], w.x.shape[2])
+        plan.close()
+        got = out.cpu().numpy().astype(np.float64)
+        del out
+        torch.cuda.empty_cache()
+        assert got.shape == (g["out_c"], g["out_h"], g["out_w"])
+        assert np.all(np.isfinite(got))
+        _FULL[name] = (w, g, got)
+    return _FULL[name]
+
+
+def _check_windows(name, i, j, what):
+    w, g, got = full_size(name)
+    log("  %s: checking %d windows (%s)" % (name, len(i), what))
     ref = oracle_windows(oracle_layers(w.layers, w.dtype), w.x, i, j)
-    assert_close(out[:, i, j].T, ref, BF16_TOL if w.dtype == "bf16" else F32_TOL, name)
+    assert_close(got[:, i, j].T, ref, BF16_TOL if w.dtype == "bf16" else F32_TOL, "%s %s" % (name, what))
+
+
+def test_c2_full_frame_every_window():
+    w, g, got = full_size("c2_1d_1m")
+    log("  c2_1d_1m: oracle on all %d windows" % (g["out_h"] * g["out_w"]))
+    ref = oracle.eval_stride(w.layers, w.x)
+    assert_close(got, ref, F32_TOL, "c2 every window")
+
+
+@pytest.mark.parametrize("name", ["c3_512", "c4_hd"])
+def test_full_size_every_phase(name):
+    _, g, _ = full_size(name)
+    i, j = wl.sample_windows(g["out_h"], g["out_w"], g["K_h"], g["K_w"], per_phase=8, seed=0)
+    assert len(set(zip((i % g["K_h"]).tolist(), (j % g["K_w"]).tolist()))) == g["K_h"] * g["K_w"]
+    _check_windows(name, i, j, "8 per phase")
+
+
+def _edge_windows(g, part, parts):
+    """Every window of the last K_h rows and the last K_w columns, split into
+    `parts` column ranges of the rows plus the columns block as the last part."""
+    K_h, K_w, oh, ow = g["K_h"], g["K_w"], g["out_h"], g["out_w"]
+    if part < parts:
+        c0, c1 = ow * part // parts, ow * (part + 1) // parts
+        ii, jj = np.meshgrid(np.arange(oh - K_h, oh), np.arange(c0, c1), indexing="ij")
+    else:
+        ii, jj = np.meshgrid(np.arange(0, oh - K_h), np.arange(ow - K_w, ow), indexing="ij")
+    return ii.reshape(-1).astype(np.int64), jj.reshape(-1).astype(np.int64)
+
+
+@pytest.mark.parametrize("name,part,parts", [("c3_512", 0, 1), ("c3_512", 1, 1), ("c4_hd", 0, 3), ("c4_hd", 1, 3),
+                                             ("c4_hd", 2, 3), ("c4_hd", 3, 3)])
+def test_full_size_last_rows_and_columns(name, part, parts):
+    _, g, _ = full_size(name)
+    i, j = _edge_windows(g, part, parts)
+    _check_windows(name, i, j, "edge part %d of %d" % (part, parts + 1))
+
+
+@pytest.mark.parametrize("half", [0, 1])
+def test_c5_full_size_every_phase(half):
+    """The 4K bfloat16 frame: 8 windows for each of the 256 phase pairs (split
+    over two tests by row phase) plus corners and edge midpoints."""
+    _, g, _ = full_size("c5_4k")
+    i, j = wl.sample_windows(g["out_h"], g["out_w"], g["K_h"], g["K_w"], per_phase=8, seed=0)
+    assert len(set(zip((i % g["K_h"]).tolist(), (j % g["K_w"]).tolist()))) == g["K_h"] * g["K_w"]
+    keep = (i % g["K_h"]) // (g["K_h"] // 2) == half
+    _check_windows("c5_4k", i[keep], j[keep], "8 per phase, row phases %s" % ("0-7", "8-15")[half])
 
 
 # ----------------------------------------------------------------------------- robustness

@@ -1,0 +1,123 @@
+"""GPU parity of the convolution kernel's launch variants, every window checked
+against the oracle: the 128-channel N tile (taken only by launches of at least
+512 workgroups) with ragged channel chunks and masked edge tiles, and a seeded
+sweep of small random chains whose sizes straddle the choices between the
+64- and 128-channel tiles and between spatial and flat tiles.  The launch
+records name the kernel and tile mode each layer actually ran."""
+import numpy as np
+import pytest
+
+import oracle
+from paper_1508_06904_amd import dss, workloads as wl
+from tests.gpu_helpers import assert_close, gpu_dense, log, oracle_layers
+
+pytestmark = pytest.mark.gpu
+
+F32_TOL = 1e-4
+BF16_TOL = 2e-2
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    dss.lib()
+    yield
+    torch.cuda.synchronize()
+
+
+def timed_dense(w):
+    """Dense evaluation with launch records: (float64 output, records)."""
+    plan = dss.Plan.from_workload(w)
+    plan.set_timing(True)
+    out, _ = gpu_dense(w.layers, w.x, w.ndim, w.dtype, plan=plan)
+    recs = plan.timings()
+    plan.close()
+    return out, recs
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_n128_tile_every_window(dtype):
+    """Two convolutions with 136 output channels (two N blocks of 128, the second
+    almost all padding) and 44 / 88 input channels (2.75 chunks: the last one
+    ragged), on extents that leave partial edge tiles.  Both launches have more
+    than 512 workgroups, so both run the 128-channel tile."""
+    cin = 44 if dtype == "f32" else 88
+    arch = [("conv", cin, 136, 3, 3, "relu"), ("pool", 2, 2), ("conv", 136, 130, 2, 2, "relu"),
+            ("conv", 130, 3, 1, 1, "none")]
+    w = wl.custom(arch, cin, 260, 291, seed=17, dtype=dtype)
+    log("n128 %s on %s" % (dtype, w.x.shape))
+    out, recs = timed_dense(w)
+    names = [r["kernel"] for r in recs if r["flops"] > 0]
+    log("  launches: %s" % names)
+    assert names[:2] == ["conv_mfma_%s_n128" % dtype] * 2
+    assert all(r["tile_mode"] == 0 for r in recs if r["kernel"].endswith("n128"))
+    ref = oracle.eval_stride(oracle_layers(w.layers, dtype), w.x)
+    assert_close(out, ref, BF16_TOL if dtype == "bf16" else F32_TOL, "n128 %s" % dtype)
+
+
+def _random_chain(seed):
+    """A small random chain and signal size.  Even seeds: one wide layer (132 to
+    256 binary32 / 512 bfloat16 output channels) on signals of 150-330 samples
+    per axis, so that its launch lands on both sides of the 512-workgroup line
+    of the 128-channel tile.  Odd seeds: two or three conv + pool layers on
+    30-110 samples, whose pooled fragments take flat or spatial tiles."""
+    rng = np.random.default_rng(5000 + seed)
+    dtype = "bf16" if seed % 3 == 2 else "f32"
+    q = 8 if dtype == "bf16" else 4
+    if seed % 2 == 0:
+        C0 = int(rng.choice([16, 24, 32]))
+        cout = q * int(rng.integers(33, 65))
+        f = int(rng.integers(1, 3))
+        k = int(rng.integers(1, 3))
+        arch = [("conv", C0, cout, f, f, "relu")] + ([("pool", k, k)] if k > 1 else []) + \
+               [("conv", cout, int(rng.choice([2, 3])), 1, 1, "none")]
+        side = int(rng.integers(150, 330))
+    else:
+        C0 = int(rng.choice([3, 16, 24]))
+        arch, c = [], C0
+        for _ in range(int(rng.integers(2, 4))):
+            cout = q * int(rng.integers(4, 17))
+            f = int(rng.integers(2, 4))
+            arch += [("conv", c, cout, f, f, str(rng.choice(["relu", "tanh"]))), ("pool", 2, 2)]
+            c = cout
+        arch.append(("conv", c, int(rng.choice([1, 2, 3])), int(rng.integers(1, 4)), int(rng.integers(1, 4)),
+                     "none"))
+        side = int(rng.integers(30, 110))
+    B = oracle.receptive_field(wl.custom(arch, C0, 1, 1, seed=0).layers)
+    H = max(side + int(rng.integers(0, 9)), B[0] + int(rng.integers(2, 12)))
+    W = max(side + int(rng.integers(0, 9)), B[1] + int(rng.integers(2, 12)))
+    return arch, C0, H, W, dtype
+
+
+SWEEP = list(range(30))
+
+
+@pytest.fixture(scope="module")
+def sweep_log():
+    seen = []
+    yield seen
+    # the sweep as a whole must reach each variant (checked at module teardown
+    # only when every sweep case ran)
+    if len(seen) == len(SWEEP):
+        kinds = {k for case in seen for k in case}
+        log("sweep variants: %s" % sorted(kinds))
+        for need in ("n64", "n128", "flat", "spatial"):
+            assert any(need in k for k in kinds), "no sweep case ran the %s variant" % need
+
+
+@pytest.mark.parametrize("seed", SWEEP)
+def test_random_chain_sweep(seed, sweep_log):
+    arch, C0, H, W, dtype = _random_chain(seed)
+    w = wl.custom(arch, C0, H, W, seed=seed, dtype=dtype)
+    out, recs = timed_dense(w)
+    kinds = set()
+    for r in recs:
+        if r["tile_mode"] >= 0:
+            kinds.add(r["kernel"].split("_")[-1] if not r["kernel"].endswith("f32out") else
+                      r["kernel"].split("_")[-2])
+            kinds.add(("spatial", "flat", "dilated")[r["tile_mode"]])
+    log("sweep %d: %s %s on %dx%d, variants %s" % (seed, dtype, arch, H, W, sorted(kinds)))
+    sweep_log.append(kinds)
+    ref = oracle.eval_stride(oracle_layers(w.layers, dtype), w.x)
+    assert_close(out, ref, BF16_TOL if dtype == "bf16" else F32_TOL, "sweep %d" % seed)
