@@ -357,6 +357,27 @@ dss_status dss_backward_dense(dss_plan_t plan, const void* signal, int32_t H, in
                               float* grad_signal, void* workspace, int64_t workspace_bytes,
                               hipStream_t stream);
 
+/* ---------------------------------------------------------------- allocation-free evaluation */
+
+/* Bytes of the fixed workspace of dss_eval_dense_noalloc. */
+#define DSS_NOALLOC_SCRATCH_BYTES (64ll * 1024 * 1024)
+
+/* dss_eval_dense for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid allocation):
+ * the same evaluation and kernels, bit for bit the same output, with the
+ * workspace in a fixed device array of the library (DSS_NOALLOC_SCRATCH_BYTES,
+ * held by every device the library runs on until the process ends) instead of
+ * a caller or plan buffer.  No device memory is allocated or freed and no HIP
+ * event is created: the plan's timing records nothing for these calls.
+ *   signal, H, W, out, stream  as for dss_eval_dense
+ * All calls on one device share that device's array and leave their data in
+ * it: calls that overlap on one device (several streams or host threads) race
+ * and must be serialised by the caller.
+ * Errors: as dss_eval_dense, and DSS_E_UNSUPPORTED if the signal needs more
+ * workspace than DSS_NOALLOC_SCRATCH_BYTES (nothing is enqueued then). */
+dss_status dss_eval_dense_noalloc(dss_plan_t plan, const void* signal, int32_t H, int32_t W, float* out,
+                                  hipStream_t stream);
+
 /* ---------------------------------------------------------------- Frag / Defrag */
 
 /* Fragmentation Frag_k per axis (Definition "fragmentation" and Lemma

@@ -17,7 +17,8 @@ BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libdss.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
-SOURCES = ["chain.cpp", "api.cpp", "device_attrs.cpp", "kernels_data.hip", "conv_direct.hip", "conv_mfma.hip", "backward.hip"]
+SOURCES = ["chain.cpp", "api.cpp", "device_attrs.cpp", "kernels_data.hip", "conv_direct.hip", "conv_mfma.hip", "backward.hip",
+           "noalloc.hip"]
 
 # -packed-fp32-ops: no v_pk_*_f32 code generation (device code only; the host
 # pass warns that it does not know the feature, which is harmless).

@@ -69,7 +69,7 @@ EXPORTS = ("dss_chain_geometry", "dss_chain_layer_geometry", "dss_plan_create", 
            "dss_plan_geometry", "dss_plan_layer_geometry", "dss_eval_dense", "dss_eval_mixed", "dss_eval_slide",
            "dss_chain_stride_geometry", "dss_plan_stride_geometry", "dss_eval_stride", "dss_chain_dilate_geometry",
            "dss_plan_dilate_geometry", "dss_eval_dilate", "dss_chain_backward_geometry",
-           "dss_plan_backward_geometry", "dss_backward_dense", "dss_frag", "dss_defrag",
+           "dss_plan_backward_geometry", "dss_backward_dense", "dss_eval_dense_noalloc", "dss_frag", "dss_defrag",
            "dss_plan_set_timing", "dss_plan_timings", "dss_status_string", "dss_last_error", "dss_version")
 
 _lib = None
@@ -104,6 +104,7 @@ def lib():
                                                   P(ctypes.c_double)]
         L.dss_plan_backward_geometry.argtypes = [VP, I32, I32, I32, P(I64), P(I64), P(I64), P(ctypes.c_double)]
         L.dss_backward_dense.argtypes = [VP, VP, I32, I32, VP, VP, VP, VP, VP, I64, VP]
+        L.dss_eval_dense_noalloc.argtypes = [VP, VP, I32, I32, VP, VP]
         L.dss_frag.argtypes = [I32, I32, I32, I32, I32, I32, I32, I32, VP, VP, VP]
         L.dss_defrag.argtypes = [I32, I32, I32, I32, I32, I32, I32, I32, VP, VP, VP]
         L.dss_plan_set_timing.argtypes = [VP, I32]
@@ -119,7 +120,7 @@ def lib():
                      "dss_defrag", "dss_plan_set_timing", "dss_plan_timings", "dss_plan_stride_geometry",
                      "dss_chain_stride_geometry", "dss_eval_stride", "dss_chain_dilate_geometry",
                      "dss_plan_dilate_geometry", "dss_eval_dilate", "dss_chain_backward_geometry",
-                     "dss_plan_backward_geometry", "dss_backward_dense"):
+                     "dss_plan_backward_geometry", "dss_backward_dense", "dss_eval_dense_noalloc"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -305,6 +306,18 @@ class Plan:
         wp, wb = _workspace_args(workspace, signal.device)
         _check(lib().dss_eval_dense(self.handle, _ptr(signal), H, W, _ptr(out), wp, wb, _stream(stream)),
                "dss_eval_dense")
+        return out
+
+    def eval_dense_noalloc(self, signal, out, stream=None):
+        """dss_eval_dense_noalloc: the dense evaluation in the library's fixed
+        scratch array (no device allocation, `out` must be given)."""
+        import torch
+        self._check_signal(signal)
+        _, H, W = signal.shape
+        g = self.geometry(H, W)
+        _check_buffer(out, "out", torch.float32, g["out_c"] * g["out_h"] * g["out_w"], device=signal.device)
+        _check(lib().dss_eval_dense_noalloc(self.handle, _ptr(signal), H, W, _ptr(out), _stream(stream)),
+               "dss_eval_dense_noalloc")
         return out
 
     def eval_mixed(self, signal, ell, out=None, workspace=None, stream=None):
