@@ -295,10 +295,14 @@ static void free_plan_memory(dss_plan* p) {
             if (c.w) (void)hipFree(c.w);
             if (c.b) (void)hipFree(c.b);
             if (c.w_alt) (void)hipFree(c.w_alt);
+            if (c.w2) (void)hipFree(c.w2);
             c.w = nullptr;
             c.b = nullptr;
             c.w_alt = nullptr;
+            c.w2 = nullptr;
         }
+    if (p->proj_b) (void)hipFree(p->proj_b);
+    p->proj_b = nullptr;
     for (hipEvent_t e : p->events) (void)hipEventDestroy(e);
     p->events.clear();
     if (p->own_ws) (void)hipFree(p->own_ws);
@@ -314,6 +318,46 @@ extern "C" void dss_plan_destroy(dss_plan_t plan) {
     free_plan_memory(plan);
     if (cur != plan->device) (void)hipSetDevice(cur);
     delete plan;
+}
+
+// Whether the last chain layer, a 1x1 convolution to at most 4 channels with
+// no pool, can be folded into the epilogue of the convolution before it (an
+// MFMA convolution without a pool), and if so its weights in the layout that
+// epilogue reads.  DSS_FUSE_PROJECTION=0 (read at plan creation) turns the
+// fold off, for cross-checks and A/B timing.
+static dss_status setup_projection_fold(dss_plan* p, const dss_layer* layers) {
+    const Chain& ch = p->chain;
+    const int L = ch.L();
+    const char* env = getenv("DSS_FUSE_PROJECTION");
+    if (env && std::strcmp(env, "0") == 0) return DSS_OK;
+    if (L < 2) return DSS_OK;
+    const ChainLayer& a = ch.layers[L - 2];
+    const ChainLayer& b = ch.layers[L - 1];
+    if (!a.has_conv || a.has_pool || !b.has_conv || b.has_pool || b.c_h != 1 || b.c_w != 1 || b.cout > 4) return DSS_OK;
+    PlanConv& pc = p->convs[L - 2];
+    if (pc.impl != CONV_MFMA_F32 && pc.impl != CONV_MFMA_BF16) return DSS_OK;
+    const int rows = std::max(pc.cout_pad, pc.cout_pad_alt);
+    std::vector<float> w2((size_t)rows * 4, 0.f), b2(4, 0.f);
+    const dss_layer& d = layers[b.desc];
+    for (int n = 0; n < b.cin; ++n)
+        for (int o = 0; o < b.cout; ++o) {
+            float v = d.weight[(size_t)o * b.cin + n];
+            if (p->dtype == DSS_BF16) {   // the plan's bfloat16 weights, as the unfused 1x1 convolution uses them
+                const uint32_t u = (uint32_t)host_f32_to_bf16(v) << 16;
+                std::memcpy(&v, &u, 4);
+            }
+            w2[(size_t)n * 4 + o] = v;
+        }
+    for (int o = 0; o < b.cout; ++o) b2[o] = d.bias ? d.bias[o] : 0.f;
+    hipError_t e = hipMalloc((void**)&pc.w2, sizeof(float) * w2.size());
+    if (e == hipSuccess) e = hipMalloc((void**)&p->proj_b, sizeof(float) * 4);
+    if (e == hipSuccess) e = hipMemcpy(pc.w2, w2.data(), sizeof(float) * w2.size(), hipMemcpyHostToDevice);
+    if (e == hipSuccess) e = hipMemcpy(p->proj_b, b2.data(), sizeof(float) * 4, hipMemcpyHostToDevice);
+    if (e != hipSuccess) return hip_fail(e, "uploading the projection weights");
+    p->fuse_proj = true;
+    p->proj_cout = b.cout;
+    p->proj_act = b.act;
+    return DSS_OK;
 }
 
 extern "C" dss_status dss_plan_create(const dss_layer* layers, int32_t n_layers, int32_t ndim,
@@ -358,6 +402,12 @@ extern "C" dss_status dss_plan_create(const dss_layer* layers, int32_t n_layers,
             delete p;
             return s;
         }
+    }
+    s = setup_projection_fold(p, layers);
+    if (s != DSS_OK) {
+        free_plan_memory(p);
+        delete p;
+        return s;
     }
     *out_plan = p;
     return DSS_OK;
@@ -451,6 +501,15 @@ const char* conv_name(const PlanConv& pc, dss_dtype tout) {
     }
 }
 
+// Telemetry name of a convolution launch with the folded projection.
+const char* conv_proj_name(const PlanConv& pc) {
+    if (pc.impl == CONV_MFMA_F32)
+        return pc.bn == 128 ? "conv_mfma_f32_n128_proj" : pc.bn == 64 ? "conv_mfma_f32_n64_proj"
+                                                                      : "conv_mfma_f32_n32_proj";
+    return pc.bn == 128 ? "conv_mfma_bf16_n128_proj" : pc.bn == 64 ? "conv_mfma_bf16_n64_proj"
+                                                                   : "conv_mfma_bf16_n32_proj";
+}
+
 }  // namespace
 
 // Runs Stuff and chain layers 1..upto.  On return *cur points at the last
@@ -460,8 +519,12 @@ const char* conv_name(const PlanConv& pc, dss_dtype tout) {
 // fragment layout) and *cur_dt is its element type.  A relaxed layer's pooling
 // runs over all Fin fragments at once as one tall signal of Fin * E_h rows:
 // every fragment's extent is a multiple of k_h, so no block straddles two.
+// With fold (and a plan that folds its projection, upto = L), the convolution of
+// layer L - 1 writes the partial projections instead of its activations, layer
+// L is skipped, and *part_nbs receives the number of channel groups summed
+// later (0 when nothing was folded).
 static dss_status run_layers(dss_plan* p, const Geom& G, int upto, char* const buf[2], hipStream_t stream, Timer& T,
-                             void** cur_out, dss_dtype* cur_dt) {
+                             void** cur_out, dss_dtype* cur_dt, bool fold = false, int* part_nbs = nullptr) {
     const Chain& ch = p->chain;
     int which = 0;
     const dss_dtype dt = p->dtype;
@@ -469,10 +532,43 @@ static dss_status run_layers(dss_plan* p, const Geom& G, int upto, char* const b
     hipError_t e;
     void* cur = buf[0];
     dss_dtype cdt = dt;
+    if (part_nbs) *part_nbs = 0;
+    const bool folding = fold && p->fuse_proj && upto == ch.L() && part_nbs;
     for (int j = 1; j <= upto; ++j) {
         const ChainLayer& c = ch.layers[j - 1];
         const LayerGeom& lg = G.L[j - 1];
         const int Fin = lg.Fin_h * lg.Fin_w;
+        const PlanConv fpc = folding && j == ch.L() - 1
+                                 ? mfma_launch_variant(p->convs[j - 1], Fin, lg.Uin_h, lg.Uin_w, lg.dil_h, lg.dil_w)
+                                 : PlanConv{};
+        // the partial projections (16 bytes per sample and channel group of 64,
+        // or 32 for the 32-channel N tile) must fit a ping-pong half, which
+        // holds at least this layer's output
+        const int ngroups = fpc.w2 ? fpc.cout_pad / (fpc.bn == 32 ? 32 : 64) : 0;
+        if (fpc.w2 && (int64_t)ngroups * Fin * lg.E_h * lg.E_w * 16 <= G.buf_bytes) {
+            // conv T_{L-1} with the 1x1 projection T_L folded into its epilogue
+            const PlanConv& pc = fpc;
+            const ChainLayer& cl = ch.layers[j];
+            void* dst = buf[which ^ 1];
+            const double f1 = 2.0 * Fin * (double)lg.E_h * lg.E_w * c.cout * (double)c.cin * c.c_h * c.c_w;
+            const double f2 = 2.0 * Fin * (double)lg.E_h * lg.E_w * cl.cout * (double)cl.cin;
+            const int nbs = ngroups;
+            const double bytes = (double)Fin * lg.Uin_h * lg.Uin_w * c.cin * dtype_size(cdt) +
+                                 (double)nbs * Fin * lg.E_h * lg.E_w * 16.0 +
+                                 (double)c.cout * c.cin * c.c_h * c.c_w * es;
+            e = T.run(
+                conv_proj_name(pc), j, f1 + f2, bytes,
+                [&] {
+                    return launch_conv_mfma_proj(cur, Fin, lg.Uin_h, lg.Uin_w, lg.dil_h, lg.dil_w, pc, (float*)dst,
+                                                 stream);
+                },
+                T.on ? mfma_tile_mode(pc, Fin, lg.Uin_h, lg.Uin_w, lg.dil_h, lg.dil_w) : -1);
+            if (e != hipSuccess) return hip_fail(e, "conv + projection launch");
+            *part_nbs = nbs;
+            *cur_out = dst;
+            *cur_dt = DSS_F32;
+            return DSS_OK;
+        }
         if (c.has_conv) {
             const PlanConv pc = mfma_launch_variant(p->convs[j - 1], Fin, lg.Uin_h, lg.Uin_w, lg.dil_h, lg.dil_w);
             const bool last_op = (j == ch.L()) && !c.has_pool;
@@ -539,7 +635,8 @@ static dss_status run_layers(dss_plan* p, const Geom& G, int upto, char* const b
 
 // Stuff (or trim) into the workspace, then chain layers 1..upto.
 static dss_status run_chain(dss_plan* p, const Geom& G, const void* signal, int upto, char* ws,
-                            hipStream_t stream, Timer& T, void** cur_out, dss_dtype* cur_dt) {
+                            hipStream_t stream, Timer& T, void** cur_out, dss_dtype* cur_dt, bool fold = false,
+                            int* part_nbs = nullptr) {
     const Chain& ch = p->chain;
     char* const buf[2] = {ws, ws + G.buf_bytes};
     const dss_dtype dt = p->dtype;
@@ -548,7 +645,7 @@ static dss_status run_chain(dss_plan* p, const Geom& G, const void* signal, int 
     hipError_t e = T.run("stuff_pack", 0, 0.0, (double)ch.in_c * (in_read + G.D_h * (double)G.D_w) * es,
                          [&] { return launch_stuff_pack(dt, signal, ch.in_c, G.H, G.W, buf[0], G.D_h, G.D_w, stream); });
     if (e != hipSuccess) return hip_fail(e, "stuff_pack launch");
-    return run_layers(p, G, upto, buf, stream, T, cur_out, cur_dt);
+    return run_layers(p, G, upto, buf, stream, T, cur_out, cur_dt, fold, part_nbs);
 }
 
 // Checks that the plan belongs to the current device.
@@ -623,13 +720,24 @@ dss_status eval_run(dss_plan_t plan, const Geom& G, const void* signal, float* o
     Timer T(plan, stream, timed);
     void* cur = nullptr;
     dss_dtype cdt;
-    dss_status s = run_chain(plan, G, signal, plan->chain.L(), ws, stream, T, &cur, &cdt);
+    int part_nbs = 0;
+    dss_status s = run_chain(plan, G, signal, plan->chain.L(), ws, stream, T, &cur, &cdt, true, &part_nbs);
     if (s != DSS_OK) return s;
     const Chain& ch = plan->chain;
     // Defrag_{k*_L / k*_ell}, then keep the first out_h x out_w samples (this is
     // Trim_r of the dense evaluation and the final trimming of the stuffing mode)
     const int Gh = ch.K_h() / G.step_h, Gw = ch.K_w() / G.step_w;
     const int Uh = G.L.back().U_h, Uw = G.L.back().U_w;
+    if (part_nbs > 0) {
+        // the folded projection: sum the channel groups' partial dot products, + bias, activation
+        const double bytes = (double)part_nbs * Gh * Gw * Uh * Uw * 16.0 + (double)G.out_h * G.out_w * ch.out_c() * 4.0;
+        hipError_t e = T.run("defrag_sum", ch.L() + 1, 0.0, bytes, [&] {
+            return launch_defrag_sum((const float*)cur, part_nbs, Gh, Gw, Uh, Uw, ch.out_c(), plan->proj_b,
+                                     plan->proj_act, out, G.out_h, G.out_w, stream);
+        });
+        if (e != hipSuccess) return hip_fail(e, "defrag_sum launch");
+        return DSS_OK;
+    }
     const double bytes = (double)Gh * Gw * Uh * Uw * ch.out_c() * dtype_size(cdt) +
                          (double)G.out_h * G.out_w * ch.out_c() * 4.0;
     hipError_t e = T.run("defrag_trim", ch.L() + 1, 0.0, bytes, [&] {
@@ -744,8 +852,18 @@ extern "C" dss_status dss_eval_stride(dss_plan_t plan, const void* signal, int32
     if (e != hipSuccess) return hip_fail(e, "patch_pack launch");
     void* cur = nullptr;
     dss_dtype cdt;
-    s = run_layers(plan, G, ch.L(), buf, stream, T, &cur, &cdt);
+    int part_nbs = 0;
+    s = run_layers(plan, G, ch.L(), buf, stream, T, &cur, &cdt, true, &part_nbs);
     if (s != DSS_OK) return s;
+    if (part_nbs > 0) {
+        const double pbytes = (double)count * (part_nbs * 16.0 + ch.out_c() * 4.0);
+        e = T.run("window_scatter_sum", ch.L() + 1, 0.0, pbytes, [&] {
+            return launch_window_scatter_sum((const float*)cur, part_nbs, count, ch.out_c(), plan->proj_b,
+                                             plan->proj_act, first, (int64_t)O_h * O_w, out, stream);
+        });
+        if (e != hipSuccess) return hip_fail(e, "window_scatter_sum launch");
+        return DSS_OK;
+    }
     const double sbytes = (double)count * ch.out_c() * (dtype_size(cdt) + 4.0);
     e = T.run("window_scatter", ch.L() + 1, 0.0, sbytes, [&] {
         return launch_window_scatter(cdt, cur, count, ch.out_c(), first, (int64_t)O_h * O_w, out, stream);
@@ -809,11 +927,20 @@ extern "C" dss_status dss_eval_dilate(dss_plan_t plan, const void* signal, int32
     Timer T(plan, stream);
     void* cur = nullptr;
     dss_dtype cdt;
-    s = run_chain(plan, G, signal, j, ws, stream, T, &cur, &cdt);   // D = H x W: a plain pack
+    int part_nbs = 0;
+    s = run_chain(plan, G, signal, j, ws, stream, T, &cur, &cdt, true, &part_nbs);   // D = H x W: a plain pack
     if (s != DSS_OK) return s;
     const int h = j == 0 ? H : G.L[j - 1].U_h;
     const int w = j == 0 ? W : G.L[j - 1].U_w;
     const int C = j == 0 ? ch.in_c : ch.layers[j - 1].cout;
+    if (part_nbs > 0) {
+        const double pbytes = (double)h * w * (part_nbs * 16.0 + C * 4.0);
+        e = T.run("planar_sum", ch.L() + 1, 0.0, pbytes, [&] {
+            return launch_planar_sum((const float*)cur, part_nbs, h, w, C, plan->proj_b, plan->proj_act, out, stream);
+        });
+        if (e != hipSuccess) return hip_fail(e, "planar_sum launch");
+        return DSS_OK;
+    }
     const double bytes = (double)h * w * C * (dtype_size(cdt) + 4.0);
     e = T.run("to_planar", ch.L() + 1, 0.0, bytes, [&] { return launch_to_planar(cdt, cur, 1, h, w, C, out, stream); });
     if (e != hipSuccess) return hip_fail(e, "to_planar launch");

@@ -79,18 +79,21 @@ __device__ __forceinline__ void dma16(const void* src, char* wave_dst) {
     __builtin_amdgcn_global_load_lds(src, (lds_void*)wave_dst, 16, 0, 0);
 }
 
-template <bool BF16, typename Tout, int WGM, int WGN, int MT, int NT>
+template <bool BF16, typename Tout, int WGM, int WGN, int MT, int NT, bool PROJ = false>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void conv_mfma_kernel(
     const char* __restrict__ in,       // [F][Hin][Win][Cin] of BF16 ? bfloat16 : binary32
     int Hin, int Win, int Cin,
     const char* __restrict__ wp,       // packed [nb][chunk][th][tw][BN][chunk channels] (bfloat16: slices in lane order)
     const float* __restrict__ bias,    // [Cout_pad]
     int fh, int fw, int Cout, int act, int nchunks,
-    Tout* __restrict__ out,            // [F][Hout][Wout][Cout]
+    Tout* __restrict__ out,            // [F][Hout][Wout][Cout] (unused with PROJ)
     int Hout, int Wout, int TH, int TW, int tilesY, int tilesX, int nbs, int dbl_halo,
     int flat_h, int flat_w,             // flat mode: input fragments of flat_h x flat_w (0: spatial tiles)
     int dil_h, int dil_w,               // dilated mode (> 1): taps dil apart on one signal, tiled by phase
-    int pad_h, int pad_w) {             // spatial tiles: a zero border of pad samples around every fragment
+    int pad_h, int pad_w,               // spatial tiles: a zero border of pad samples around every fragment
+    const float* __restrict__ w2,       // PROJ: 1x1 projection weights [Cout_pad][4] (binary32, zero padded)
+    float* __restrict__ part,           // PROJ: partial projections [nbs * WGN][F * Hout * Wout][4]
+    int64_t part_stride) {              // PROJ: floats per channel group of part
     using Cfg = MfmaCfg<BF16, WGM, WGN, MT, NT>;
     constexpr int THREADS = Cfg::THREADS;
     extern __shared__ __attribute__((aligned(16))) char lds[];
@@ -447,6 +450,82 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
             }
         }
     };
+    // The following 1x1 convolution folded into this epilogue (PROJ): per output
+    // sample and projection channel o (four, zero padded), the partial dot
+    // product over each wave's group of 32 NT channels (64 with the 64- and
+    // 128-channel N tiles, 32 with the 32-channel one),
+    //   part[group][sample][o] = sum_{n in group} w2[n][o] * act(acc[sample][n] + bias[n]),
+    // summed over the groups in order, with the projection's bias and activation,
+    // by the step that reads it.  The groups do not depend on the N tile of the
+    // launch, so every evaluation fashion sums in the same order.  A lane holds
+    // one channel of 16 samples per 32x32 tile; per sample it first adds its NT
+    // channels' products, then the lanes of a half are reduced in two passes of
+    // 8 samples x 4 outputs by five butterfly exchanges that halve the values a
+    // lane keeps (32 -> 1), so in pass p lane l32 ends with output o = l32 mod 4
+    // of sample slot v = 8 p + l32 / 4.
+    auto store_proj = [&](auto act_c) {
+        constexpr int ACT = decltype(act_c)::value;
+        // keeps the projection weights' loads here: hoisted above the K loop they
+        // would hold registers through it
+        asm volatile("" ::: "memory");
+        float4 wv[NT];
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt)
+            wv[nt] = ncol[nt] < Cout ? *reinterpret_cast<const float4*>(w2 + 4 * (size_t)ncol[nt])
+                                     : make_float4(0.f, 0.f, 0.f, 0.f);
+        // the wave's position as scalars: the vector wm / wn feed the K loop's
+        // addresses, and sharing them would keep those values live through it
+        const int wm_s = __builtin_amdgcn_readfirstlane(wm), wn_s = __builtin_amdgcn_readfirstlane(wn);
+        float* part_g = part + (size_t)(nb * WGN + wn_s) * part_stride;
+        const int oc = l32 & 3;
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+#pragma unroll
+            for (int pass = 0; pass < 2; ++pass) {
+                float v32[32];
+#pragma unroll
+                for (int v = 0; v < 8; ++v) {
+                    float p0 = 0.f, p1 = 0.f, p2 = 0.f, p3 = 0.f;
+#pragma unroll
+                    for (int nt = 0; nt < NT; ++nt) {
+                        const float a = activate(ACT, acc[mt][nt][8 * pass + v] + bn[nt]);
+                        p0 += a * wv[nt].x;
+                        p1 += a * wv[nt].y;
+                        p2 += a * wv[nt].z;
+                        p3 += a * wv[nt].w;
+                    }
+                    v32[4 * v] = p0;
+                    v32[4 * v + 1] = p1;
+                    v32[4 * v + 2] = p2;
+                    v32[4 * v + 3] = p3;
+                }
+#pragma unroll
+                for (int lvl = 0; lvl < 5; ++lvl) {
+                    const int sh = 16 >> lvl, n = 16 >> lvl;   // partner lane ^ sh; keep n of 2n values
+                    const bool upper = (l32 & sh) != 0;
+#pragma unroll
+                    for (int t = 0; t < n; ++t) {
+                        const float give = upper ? v32[t] : v32[t + n];
+                        const float keep = upper ? v32[t + n] : v32[t];
+                        v32[t] = keep + __shfl_xor(give, sh, 64);
+                    }
+                }
+                const int vv = 8 * pass + (l32 >> 2);
+                const int m = wm_s * 32 * MT + mt * 32 + (vv >> 2) * 8 + half * 4 + (vv & 3);
+                size_t o;
+                if (out_pos(m, o)) part_g[o * 4 + oc] = v32[0];
+            }
+        }
+    };
+    if constexpr (PROJ) {
+        if (act == 1)
+            store_proj(std::integral_constant<int, 1>{});
+        else if (act == 2)
+            store_proj(std::integral_constant<int, 2>{});
+        else
+            store_proj(std::integral_constant<int, 0>{});
+        return;
+    }
     if (act == 1)
         store_tile(std::integral_constant<int, 1>{});
     else if (act == 2)
@@ -651,9 +730,9 @@ int mfma_tile_mode(const PlanConv& pc, int F, int Hin, int Win, int dil_h, int d
     return L.flat ? 1 : 0;
 }
 
-template <bool BF16, typename Tout, int WGM, int WGN, int MT, int NT>
+template <bool BF16, typename Tout, int WGM, int WGN, int MT, int NT, bool PROJ>
 static hipError_t run_mfma(const void* in, int F, int Hin, int Win, int dil_h, int dil_w, int pad_h, int pad_w,
-                           const PlanConv& pc, void* out, hipStream_t s) {
+                           const PlanConv& pc, void* out, float* part, hipStream_t s) {
     using Cfg = MfmaCfg<BF16, WGM, WGN, MT, NT>;
     const bool dilated = dil_h * dil_w > 1;
     const bool padded = pad_h > 0 || pad_w > 0;
@@ -670,32 +749,36 @@ static hipError_t run_mfma(const void* in, int F, int Hin, int Win, int dil_h, i
         L.t.lds /= 2;
     }
     if (L.nblocks >= (1ll << 31)) return hipErrorInvalidConfiguration;
-    auto kern = conv_mfma_kernel<BF16, Tout, WGM, WGN, MT, NT>;
+    auto kern = conv_mfma_kernel<BF16, Tout, WGM, WGN, MT, NT, PROJ>;
     hipError_t e = allow_dynamic_lds((const void*)kern, L.t.lds);
     if (e != hipSuccess) return e;
     const int nchunks = pc.cin_pad / Cfg::CC;
     const int Hout = Hin + 2 * pad_h - dil_h * (pc.fh - 1), Wout = Win + 2 * pad_w - dil_w * (pc.fw - 1);
+    if (PROJ && (padded || !pc.w2)) return hipErrorInvalidValue;
+    const int64_t part_stride = PROJ ? (int64_t)F * Hout * Wout * 4 : 0;
     if (L.flat) {
         // one "fragment" of 1 x (F * Hin * Win) samples for the staging and the tile grid
         const int flat_len = (int)((int64_t)F * Hin * Win);   // below 2^30 in flat mode
         kern<<<dim3((unsigned)L.nblocks), Cfg::THREADS, L.t.lds, s>>>(
             (const char*)in, 1, flat_len, pc.cin, (const char*)pc.w, pc.b, pc.fh, pc.fw, pc.cout, pc.act, nchunks,
-            (Tout*)out, Hout, Wout, 1, L.t.TW, 1, L.tilesX, nbs, L.t.dbl, Hin, Win, 1, 1, 0, 0);
+            (Tout*)out, Hout, Wout, 1, L.t.TW, 1, L.tilesX, nbs, L.t.dbl, Hin, Win, 1, 1, 0, 0, pc.w2, part,
+            part_stride);
         return hipGetLastError();
     }
     kern<<<dim3((unsigned)L.nblocks), Cfg::THREADS, L.t.lds, s>>>(
         (const char*)in, Hin, Win, pc.cin, (const char*)pc.w, pc.b, pc.fh, pc.fw, pc.cout, pc.act, nchunks,
-        (Tout*)out, Hout, Wout, L.t.TH, L.t.TW, L.tilesY, L.tilesX, nbs, L.t.dbl, 0, 0, dil_h, dil_w, pad_h, pad_w);
+        (Tout*)out, Hout, Wout, L.t.TH, L.t.TW, L.tilesY, L.tilesX, nbs, L.t.dbl, 0, 0, dil_h, dil_w, pad_h, pad_w,
+        pc.w2, part, part_stride);
     return hipGetLastError();
 }
 
-template <bool BF16, typename Tout>
+template <bool BF16, typename Tout, bool PROJ = false>
 static hipError_t dispatch_bn(const void* in, int F, int Hin, int Win, int dh, int dw, int ph, int pw,
-                              const PlanConv& pc, void* out, hipStream_t s) {
+                              const PlanConv& pc, void* out, hipStream_t s, float* part = nullptr) {
     switch (pc.bn) {
-        case 128: return run_mfma<BF16, Tout, 2, 2, 4, 2>(in, F, Hin, Win, dh, dw, ph, pw, pc, out, s);
-        case 64: return run_mfma<BF16, Tout, 4, 1, 2, 2>(in, F, Hin, Win, dh, dw, ph, pw, pc, out, s);
-        case 32: return run_mfma<BF16, Tout, 4, 1, 2, 1>(in, F, Hin, Win, dh, dw, ph, pw, pc, out, s);
+        case 128: return run_mfma<BF16, Tout, 2, 2, 4, 2, PROJ>(in, F, Hin, Win, dh, dw, ph, pw, pc, out, part, s);
+        case 64: return run_mfma<BF16, Tout, 4, 1, 2, 2, PROJ>(in, F, Hin, Win, dh, dw, ph, pw, pc, out, part, s);
+        case 32: return run_mfma<BF16, Tout, 4, 1, 2, 1, PROJ>(in, F, Hin, Win, dh, dw, ph, pw, pc, out, part, s);
     }
     return hipErrorInvalidValue;
 }
@@ -714,6 +797,15 @@ hipError_t launch_conv_mfma_bf16(dss_dtype tout, const uint16_t* in, int F, int 
                                  const PlanConv& pc, void* out, hipStream_t s) {
     if (tout == DSS_F32) return dispatch_bn<true, float>(in, F, Hin, Win, dil_h, dil_w, 0, 0, pc, out, s);
     return dispatch_bn<true, uint16_t>(in, F, Hin, Win, dil_h, dil_w, 0, 0, pc, out, s);
+}
+
+hipError_t launch_conv_mfma_proj(const void* in, int F, int Hin, int Win, int dil_h, int dil_w, const PlanConv& pc,
+                                 float* part, hipStream_t s) {
+    if (pc.impl == CONV_MFMA_BF16)
+        return dispatch_bn<true, float, true>(in, F, Hin, Win, dil_h, dil_w, 0, 0, pc, nullptr, s, part);
+    if (pc.impl == CONV_MFMA_F32)
+        return dispatch_bn<false, float, true>(in, F, Hin, Win, dil_h, dil_w, 0, 0, pc, nullptr, s, part);
+    return hipErrorInvalidValue;
 }
 
 }  // namespace dss

@@ -91,6 +91,9 @@ struct PlanConv {
     // 64-channel tile, used when a launch would leave the GPU short of workgroups
     void* w_alt = nullptr;
     int bn_alt = 0, cout_pad_alt = 0;
+    // MFMA convolution followed by a folded 1x1 projection: its weights as
+    // [max(cout_pad, cout_pad_alt)][4] binary32 (zero padded), device
+    float* w2 = nullptr;
 };
 
 // The variant a launch over F fragments of Hin x Win (taps dil apart) should use.
@@ -128,6 +131,13 @@ struct dss_plan {
     std::vector<dss::PlanConv> convs;     // one per chain layer (impl unused if no conv)
     std::vector<dss::PlanConv> bconvs;    // binary32 plans: the input-gradient convolutions (transposed,
                                           // flipped filters, no bias, no activation)
+    // The last chain layer is a 1x1 convolution to at most 4 channels without a
+    // pool, after an MFMA convolution without a pool: dense and mixed
+    // evaluations fold it into that convolution's epilogue (convs[L-2].w2) and
+    // sum the N blocks' partial projections in the final defragmentation.
+    bool fuse_proj = false;
+    float* proj_b = nullptr;              // device [4]: the projection's bias, zero padded
+    int proj_cout = 0, proj_act = 0;
     bool timing = false;
     std::vector<hipEvent_t> events;
     std::vector<dss::LaunchRec> recs;
@@ -179,7 +189,21 @@ hipError_t launch_pool_stride(dss_dtype dt, const void* in, int E_h, int E_w, in
                               void* out, hipStream_t s);
 hipError_t launch_defrag_trim(dss_dtype dt, const void* in, int K_h, int K_w, int U_h, int U_w, int C,
                               float* out, int O_h, int O_w, hipStream_t s);
-
+// Defrag + Trim of a folded projection: out = act(bias + sum over nbs channel
+// groups of part[g][fragment sample][c]) for c < C <= 4, the groups summed in order.
+hipError_t launch_defrag_sum(const float* part, int nbs, int K_h, int K_w, int U_h, int U_w, int C, const float* bias,
+                             int act, float* out, int O_h, int O_w, hipStream_t s);
+// The same sum for the strided baseline's windows first..first+count-1 (part
+// [nbs][count][4]) and for the dilated fashion's last layer (part [nbs][h * w][4]).
+hipError_t launch_window_scatter_sum(const float* part, int nbs, int count, int C, const float* bias, int act,
+                                     int64_t first, int64_t plane, float* out, hipStream_t s);
+hipError_t launch_planar_sum(const float* part, int nbs, int h, int w, int C, const float* bias, int act, float* out,
+                             hipStream_t s);
+// The MFMA convolution pc (taps dil apart when dilated) with the folded 1x1
+// projection (pc.w2): partial projections [groups][F * Hout * Wout][4] per group
+// of 64 channels (32 for the 32-channel N tile) instead of the activations.
+hipError_t launch_conv_mfma_proj(const void* in, int F, int Hin, int Win, int dil_h, int dil_w, const PlanConv& pc,
+                                 float* part, hipStream_t s);
 hipError_t launch_to_planar(dss_dtype dt, const void* in, int F, int h, int w, int C, float* out,
                             hipStream_t s);
 hipError_t launch_frag_planar(int elem_bytes, bool inverse, const void* in, int k_h, int k_w, int S_h,

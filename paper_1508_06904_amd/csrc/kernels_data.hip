@@ -321,6 +321,84 @@ hipError_t launch_defrag_trim(dss_dtype dt, const void* in, int K_h, int K_w, in
     return hipGetLastError();
 }
 
+// The final step after a folded 1x1 convolution: the partial projections of
+// the channel groups ([nbs][sample][4] binary32, `stride` floats apart) summed in
+// group order, then the projection's bias and activation, for channels c < C.
+__device__ __forceinline__ void sum_projection(const float* __restrict__ src, int64_t stride, int nbs, int C,
+                                               const float* __restrict__ bias, int act, float* __restrict__ out,
+                                               int64_t plane) {
+    float4 a = *reinterpret_cast<const float4*>(src);
+    for (int nb = 1; nb < nbs; ++nb) {
+        const float4 b = *reinterpret_cast<const float4*>(src + nb * stride);
+        a.x += b.x;
+        a.y += b.y;
+        a.z += b.z;
+        a.w += b.w;
+    }
+    const float v[4] = {a.x, a.y, a.z, a.w};
+    for (int c = 0; c < C; ++c) out[c * plane] = activate(act, v[c] + bias[c]);
+}
+
+// Defrag + Trim of the partial projections (the defrag_trim map).
+__global__ __launch_bounds__(kThreads) void defrag_sum_kernel(const float* __restrict__ part, int64_t stride, int nbs,
+                                                             int K_h, int K_w, int U_h, int U_w, int C,
+                                                             const float* __restrict__ bias, int act,
+                                                             float* __restrict__ out, int O_h, int O_w) {
+    const int64_t p = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (p >= (int64_t)O_h * O_w) return;
+    const int i = (int)(p / O_w), j = (int)(p % O_w);
+    const int f = (i % K_h) * K_w + (j % K_w);
+    sum_projection(part + (((int64_t)f * U_h + i / K_h) * U_w + j / K_w) * 4, stride, nbs, C, bias, act, out + p,
+                   (int64_t)O_h * O_w);
+}
+
+// The strided baseline's per-window outputs (the window_scatter map) from partial projections.
+__global__ __launch_bounds__(kThreads) void window_scatter_sum_kernel(const float* __restrict__ part, int64_t stride,
+                                                                     int nbs, int count, int C,
+                                                                     const float* __restrict__ bias, int act,
+                                                                     int64_t first, int64_t plane,
+                                                                     float* __restrict__ out) {
+    const int64_t n = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (n >= count) return;
+    sum_projection(part + n * 4, stride, nbs, C, bias, act, out + first + n, plane);
+}
+
+// One signal of h x w samples (the dilated fashion's last layer) to planar, from partial projections.
+__global__ __launch_bounds__(kThreads) void planar_sum_kernel(const float* __restrict__ part, int64_t stride, int nbs,
+                                                             int64_t hw, int C, const float* __restrict__ bias,
+                                                             int act, float* __restrict__ out) {
+    const int64_t q = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (q >= hw) return;
+    sum_projection(part + q * 4, stride, nbs, C, bias, act, out + q, hw);
+}
+
+hipError_t launch_defrag_sum(const float* part, int nbs, int K_h, int K_w, int U_h, int U_w, int C, const float* bias,
+                             int act, float* out, int O_h, int O_w, hipStream_t s) {
+    if (C < 1 || C > 4 || nbs < 1) return hipErrorInvalidValue;
+    const dim3 grid((unsigned)ceil_div64((int64_t)O_h * O_w, kThreads));
+    const int64_t stride = (int64_t)K_h * K_w * U_h * U_w * 4;
+    defrag_sum_kernel<<<grid, kThreads, 0, s>>>(part, stride, nbs, K_h, K_w, U_h, U_w, C, bias, act, out, O_h, O_w);
+    return hipGetLastError();
+}
+
+hipError_t launch_window_scatter_sum(const float* part, int nbs, int count, int C, const float* bias, int act,
+                                     int64_t first, int64_t plane, float* out, hipStream_t s) {
+    if (C < 1 || C > 4 || nbs < 1) return hipErrorInvalidValue;
+    const dim3 grid((unsigned)ceil_div64(count, kThreads));
+    window_scatter_sum_kernel<<<grid, kThreads, 0, s>>>(part, (int64_t)count * 4, nbs, count, C, bias, act, first,
+                                                        plane, out);
+    return hipGetLastError();
+}
+
+hipError_t launch_planar_sum(const float* part, int nbs, int h, int w, int C, const float* bias, int act, float* out,
+                             hipStream_t s) {
+    if (C < 1 || C > 4 || nbs < 1) return hipErrorInvalidValue;
+    const int64_t hw = (int64_t)h * w;
+    const dim3 grid((unsigned)ceil_div64(hw, kThreads));
+    planar_sum_kernel<<<grid, kThreads, 0, s>>>(part, hw * 4, nbs, hw, C, bias, act, out);
+    return hipGetLastError();
+}
+
 // ------------------------------------------------------------------ to_planar
 template <typename T>
 __global__ __launch_bounds__(kThreads) void to_planar_kernel(const T* __restrict__ in, int F, int h, int w, int C,

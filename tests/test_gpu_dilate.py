@@ -126,5 +126,7 @@ def test_dilate_timing_records():
     gpu_dilate(plan, w.x)
     recs = plan.timings()
     names = [r["kernel"] for r in recs]
-    assert names[0] == "stuff_pack" and names[-1] == "to_planar" and names.count("pool_dilate") == 3
+    # the final 1x1 projection is folded into the dilated conv6x6 epilogue
+    assert names[0] == "stuff_pack" and names[-1] == "planar_sum" and names.count("pool_dilate") == 3
+    assert names[-2].endswith("_proj")
     assert sum(r["flops"] for r in recs) == pytest.approx(plan.dilate_geometry(120, 130, 5)[3], rel=1e-9)

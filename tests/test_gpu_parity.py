@@ -446,19 +446,26 @@ def test_concurrent_evaluations_one_plan(dtype):
         assert torch.equal(outs[i].cpu(), serial[i]), i
 
 
-def test_timing_records():
+@pytest.mark.parametrize("fold", [True, False])
+def test_timing_records(fold, monkeypatch):
+    if not fold:
+        monkeypatch.setenv("DSS_FUSE_PROJECTION", "0")
     w = wl.make("c3_512", H=120, W=130, widths=(16, 32, 64, 128))
     plan = dss.Plan.from_workload(w)
     plan.set_timing(True)
     gpu_dense(w.layers, w.x, 2, plan=plan)
     recs = plan.timings()
     names = [r["kernel"] for r in recs]
-    assert names[0] == "stuff_pack" and names[-1] == "defrag_trim"
-    # the 128-channel layer runs the 64-channel tile here: at this size the 128-channel
-    # tile would give too few workgroups to fill the GPU
+    assert names[0] == "stuff_pack"
     assert "conv_mfma_f32_n64" in names and "conv_mfma_f32_n32" in names and "pool_frag" in names
-    # the final 1x1 projection to 2 channels runs the LDS-staged direct kernel
-    assert names[-2] == "conv_narrow"
+    if fold:
+        # the final 1x1 projection folded into the conv6x6 epilogue (the 128-channel
+        # layer runs the 64-channel tile here: at this size the 128-channel tile
+        # would give too few workgroups to fill the GPU)
+        assert names[-2:] == ["conv_mfma_f32_n64_proj", "defrag_sum"]
+    else:
+        # the final 1x1 projection to 2 channels runs the LDS-staged direct kernel
+        assert names[-2:] == ["conv_narrow", "defrag_trim"]
     g = plan.geometry(120, 130)
     assert sum(r["flops"] for r in recs) == pytest.approx(g["conv_flops"], rel=1e-9)
     assert all(r["ms"] >= 0 for r in recs)

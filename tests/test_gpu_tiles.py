@@ -38,10 +38,11 @@ def timed_dense(w):
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_n128_tile_every_window(dtype):
-    """Two convolutions with 136 output channels (two N blocks of 128, the second
-    almost all padding) and 44 / 88 input channels (2.75 chunks: the last one
-    ragged), on extents that leave partial edge tiles.  Both launches have more
-    than 512 workgroups, so both run the 128-channel tile."""
+    """Two convolutions with 136 and 130 output channels (two N blocks of 128,
+    the second almost all padding) and 44 / 88 input channels (2.75 chunks: the
+    last one ragged), on extents that leave partial edge tiles.  Both launches
+    have more than 512 workgroups, so both run the 128-channel tile; the second
+    also computes the final 1x1 projection in its epilogue."""
     cin = 44 if dtype == "f32" else 88
     arch = [("conv", cin, 136, 3, 3, "relu"), ("pool", 2, 2), ("conv", 136, 130, 2, 2, "relu"),
             ("conv", 130, 3, 1, 1, "none")]
@@ -50,8 +51,9 @@ def test_n128_tile_every_window(dtype):
     out, recs = timed_dense(w)
     names = [r["kernel"] for r in recs if r["flops"] > 0]
     log("  launches: %s" % names)
-    assert names[:2] == ["conv_mfma_%s_n128" % dtype] * 2
-    assert all(r["tile_mode"] == 0 for r in recs if r["kernel"].endswith("n128"))
+    # the second carries the folded 1x1 projection
+    assert names == ["conv_mfma_%s_n128" % dtype, "conv_mfma_%s_n128_proj" % dtype]
+    assert all(r["tile_mode"] == 0 for r in recs if "n128" in r["kernel"])
     ref = oracle.eval_stride(oracle_layers(w.layers, dtype), w.x)
     assert_close(out, ref, BF16_TOL if dtype == "bf16" else F32_TOL, "n128 %s" % dtype)
 
@@ -114,10 +116,57 @@ def test_random_chain_sweep(seed, sweep_log):
     kinds = set()
     for r in recs:
         if r["tile_mode"] >= 0:
-            kinds.add(r["kernel"].split("_")[-1] if not r["kernel"].endswith("f32out") else
-                      r["kernel"].split("_")[-2])
+            kinds.add([t for t in r["kernel"].split("_") if t in ("n32", "n64", "n128")][0])
             kinds.add(("spatial", "flat", "dilated")[r["tile_mode"]])
     log("sweep %d: %s %s on %dx%d, variants %s" % (seed, dtype, arch, H, W, sorted(kinds)))
     sweep_log.append(kinds)
     ref = oracle.eval_stride(oracle_layers(w.layers, dtype), w.x)
     assert_close(out, ref, BF16_TOL if dtype == "bf16" else F32_TOL, "sweep %d" % seed)
+
+
+FOLD_CASES = {
+    # (arch, channels, H, W, dtype, value kind)
+    "f32_n64": ([("conv", 3, 16, 5, 5, "relu"), ("pool", 2, 2), ("conv", 16, 40, 3, 3, "relu"), ("pool", 2, 2),
+                 ("conv", 40, 72, 3, 3, "tanh"), ("pool", 2, 2), ("conv", 72, 130, 4, 4, "relu"),
+                 ("conv", 130, 2, 1, 1, "none")], 3, 93, 101, "f32", "uniform"),
+    "f32_n32_act": ([("conv", 16, 20, 3, 3, "relu"), ("pool", 2, 2), ("conv", 20, 24, 2, 2, "tanh"),
+                     ("conv", 24, 3, 1, 1, "tanh")], 16, 77, 70, "f32", "normal"),
+    "bf16_n128": ([("conv", 32, 256, 2, 2, "relu"), ("conv", 256, 4, 1, 1, "none")], 32, 300, 310, "bf16", "uniform"),
+    "int_f32": ([("conv", 16, 32, 3, 3, "relu"), ("pool", 2, 2), ("conv", 32, 48, 3, 2, "relu"), ("pool", 2, 2),
+                 ("conv", 48, 136, 2, 3, "relu"), ("conv", 136, 3, 1, 1, "none")], 16, 41, 47, "f32", "int"),
+    # 32 taps of |x| <= 8 with weights in {-1, 0, 1}: the stored bfloat16 activations stay
+    # integers of at most 256, which bfloat16 holds exactly
+    "int_bf16_n128": ([("conv", 16, 200, 1, 2, "relu"), ("conv", 200, 2, 1, 1, "relu")], 16, 290, 285, "bf16", "int"),
+}
+
+
+@pytest.mark.parametrize("case", list(FOLD_CASES))
+def test_projection_fold(case, monkeypatch):
+    """The final 1x1 projection folded into the previous convolution's epilogue
+    (partial dot products per group of 64 channels, or 32 with the 32-channel
+    N tile, summed in group order by the final defragmentation) against the
+    unfused evaluation and the oracle; integer data bit-exact both ways."""
+    arch, C, H, W, dtype, kind = FOLD_CASES[case]
+    w = wl.custom(arch, C, H, W, seed=31, dtype=dtype, value_kind=kind,
+                  weight_kind="int" if kind == "int" else "he")
+    fused, rf = timed_dense(w)
+    monkeypatch.setenv("DSS_FUSE_PROJECTION", "0")
+    plain, rp = timed_dense(w)
+    names_f = [r["kernel"] for r in rf]
+    names_p = [r["kernel"] for r in rp]
+    log("fold %s: %s / %s" % (case, names_f[-2:], names_p[-2:]))
+    assert names_f[-2].endswith("_proj") and names_f[-1] == "defrag_sum"
+    assert not any(n.endswith("_proj") for n in names_p) and names_p[-1] == "defrag_trim"
+    assert sum(r["flops"] for r in rf) == pytest.approx(sum(r["flops"] for r in rp), rel=1e-12)
+    ref = oracle.eval_stride(oracle_layers(w.layers, dtype), w.x)
+    if kind == "int":
+        assert np.abs(ref).max() < 2 ** 23
+        np.testing.assert_array_equal(fused, ref)
+        np.testing.assert_array_equal(plain, ref)
+        return
+    tol = BF16_TOL if dtype == "bf16" else F32_TOL
+    assert_close(fused, ref, tol, "fold %s fused" % case)
+    assert_close(plain, ref, tol, "fold %s unfused" % case)
+    if dtype == "f32":
+        # same products, summed in another order
+        assert_close(fused, plain, 1e-6, "fold %s fused vs unfused" % case)
