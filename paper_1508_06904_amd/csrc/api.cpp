@@ -328,6 +328,8 @@ extern "C" void dss_plan_destroy(dss_plan_t plan) {
 static dss_status setup_projection_fold(dss_plan* p, const dss_layer* layers) {
     const Chain& ch = p->chain;
     const int L = ch.L();
+    const char* pool_env = getenv("DSS_FUSE_POOL");
+    p->fuse_pool = !(pool_env && std::strcmp(pool_env, "0") == 0);
     const char* env = getenv("DSS_FUSE_PROJECTION");
     if (env && std::strcmp(env, "0") == 0) return DSS_OK;
     if (L < 2) return DSS_OK;
@@ -568,6 +570,31 @@ static dss_status run_layers(dss_plan* p, const Geom& G, int upto, char* const b
             *cur_out = dst;
             *cur_dt = DSS_F32;
             return DSS_OK;
+        }
+        if (c.has_conv && c.has_pool && p->fuse_pool && !lg.relaxed && !lg.dilated && lg.E_h == 1 && lg.Fin_h == 1 &&
+            c.k_h == 1 && c.k_w >= 2 && c.cout % 4 == 0) {
+            // one-row fragments: the sliding max-pool and Frag in the convolution's
+            // epilogue, on spatial tiles of 256 samples stepped by 257 - k; taken
+            // when those tiles compute at most 10 % more samples than the layer has
+            const PlanConv pc = mfma_launch_variant(p->convs[j - 1], Fin, lg.Uin_h, lg.Uin_w, 1, 1);
+            const int64_t tiles = ((int64_t)c.k_w * lg.U_w + 256 - c.k_w) / (256 - c.k_w + 1);
+            if (pc.impl == CONV_MFMA_F32 && pc.bn <= 64 && 10 * tiles * 256 <= 11 * (int64_t)lg.E_w) {
+                void* dst = buf[which ^ 1];
+                const double flops = 2.0 * Fin * (double)lg.E_h * lg.E_w * c.cout * (double)c.cin * c.c_h * c.c_w;
+                const double bytes = (double)Fin * lg.Uin_h * lg.Uin_w * c.cin * 4.0 +
+                                     (double)lg.Fout_h * lg.Fout_w * lg.U_h * lg.U_w * c.cout * 4.0 +
+                                     (double)c.cout * c.cin * c.c_h * c.c_w * 4.0;
+                e = T.run(pc.bn == 64 ? "conv_mfma_f32_n64_pool" : "conv_mfma_f32_n32_pool", j, flops, bytes,
+                          [&] {
+                              return launch_conv_mfma_pool((const float*)cur, Fin, lg.Uin_h, lg.Uin_w, pc, c.k_w,
+                                                           (float*)dst, stream);
+                          },
+                          T.on ? 0 : -1);
+                if (e != hipSuccess) return hip_fail(e, "conv + pool launch");
+                which ^= 1;
+                cur = dst;
+                continue;
+            }
         }
         if (c.has_conv) {
             const PlanConv pc = mfma_launch_variant(p->convs[j - 1], Fin, lg.Uin_h, lg.Uin_w, lg.dil_h, lg.dil_w);

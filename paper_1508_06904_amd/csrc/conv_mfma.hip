@@ -79,21 +79,29 @@ __device__ __forceinline__ void dma16(const void* src, char* wave_dst) {
     __builtin_amdgcn_global_load_lds(src, (lds_void*)wave_dst, 16, 0, 0);
 }
 
-template <bool BF16, typename Tout, int WGM, int WGN, int MT, int NT, bool PROJ = false>
+// Epilogue variants: kEpiStore writes the activations, kEpiProj the partial
+// projections of a folded 1x1 convolution, kEpiPool the sliding-window maxima of
+// a 1-D pool written straight to their fragments.
+constexpr int kEpiStore = 0, kEpiProj = 1, kEpiPool = 2;
+
+template <bool BF16, typename Tout, int WGM, int WGN, int MT, int NT, int EPI = kEpiStore>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void conv_mfma_kernel(
     const char* __restrict__ in,       // [F][Hin][Win][Cin] of BF16 ? bfloat16 : binary32
     int Hin, int Win, int Cin,
     const char* __restrict__ wp,       // packed [nb][chunk][th][tw][BN][chunk channels] (bfloat16: slices in lane order)
     const float* __restrict__ bias,    // [Cout_pad]
     int fh, int fw, int Cout, int act, int nchunks,
-    Tout* __restrict__ out,            // [F][Hout][Wout][Cout] (unused with PROJ)
+    Tout* __restrict__ out,            // [F][Hout][Wout][Cout]; kEpiPool: the fragments [k F][1][pool_U][Cout]
+                                       // (unused with kEpiProj)
     int Hout, int Wout, int TH, int TW, int tilesY, int tilesX, int nbs, int dbl_halo,
     int flat_h, int flat_w,             // flat mode: input fragments of flat_h x flat_w (0: spatial tiles)
     int dil_h, int dil_w,               // dilated mode (> 1): taps dil apart on one signal, tiled by phase
     int pad_h, int pad_w,               // spatial tiles: a zero border of pad samples around every fragment
-    const float* __restrict__ w2,       // PROJ: 1x1 projection weights [Cout_pad][4] (binary32, zero padded)
-    float* __restrict__ part,           // PROJ: partial projections [nbs * WGN][F * Hout * Wout][4]
-    int64_t part_stride) {              // PROJ: floats per channel group of part
+    const float* __restrict__ w2,       // kEpiProj: 1x1 projection weights [Cout_pad][4] (binary32, zero padded)
+    float* __restrict__ part,           // kEpiProj: partial projections [nbs * WGN][F * Hout * Wout][4]
+    int64_t part_stride,                // kEpiProj: floats per channel group of part
+    int tile_step_w,                    // columns between neighbouring tiles (TW, or TW - k + 1 with kEpiPool)
+    int pool_k, int pool_U) {           // kEpiPool: pool size along the row, pooled samples per fragment
     using Cfg = MfmaCfg<BF16, WGM, WGN, MT, NT>;
     constexpr int THREADS = Cfg::THREADS;
     extern __shared__ __attribute__((aligned(16))) char lds[];
@@ -132,7 +140,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
     const int f = tile / tiles;
     const int trem = tile % tiles;
     const int ty0 = (trem / tilesX) * TH;
-    const int tx0 = (trem % tilesX) * TW;
+    const int tx0 = (trem % tilesX) * tile_step_w;
 
     // Spatial tiles: a TH x TW block of one fragment, halo (TH + fh - 1) x (TW + fw - 1).
     // Flat mode (small fragments): the fragment batch is read as one sequence of
@@ -450,7 +458,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
             }
         }
     };
-    // The following 1x1 convolution folded into this epilogue (PROJ): per output
+    // The following 1x1 convolution folded into this epilogue (kEpiProj): per output
     // sample and projection channel o (four, zero padded), the partial dot
     // product over each wave's group of 32 NT channels (64 with the 64- and
     // 128-channel N tiles, 32 with the 32-channel one),
@@ -517,7 +525,58 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
             }
         }
     };
-    if constexpr (PROJ) {
+    // kEpiPool (fragments of one row, binary32, one wave column): the tile's
+    // activations go to LDS as [BM][BN + 4] floats; each thread then forms the
+    // maxima of k consecutive samples for the tile's first TW - k + 1 positions
+    // (neighbouring tiles overlap by k - 1 samples, so every window lies inside
+    // one tile) and writes each maximum straight to its fragment: sample x of
+    // input fragment f goes to sample x div k of fragment (x mod k) F + f, F the
+    // launch's fragment count (Lemma "frag-ops" along the row).
+    auto store_pool = [&](auto act_c) {
+        constexpr int ACT = decltype(act_c)::value;
+        constexpr int PITCH = Cfg::BN + 4;
+        constexpr int CQ = Cfg::BN / 4;
+        float* tl = reinterpret_cast<float*>(lds);
+        __syncthreads();                                         // every wave is done with the halo
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) {
+                    const int m = wm * 32 * MT + mt * 32 + (v >> 2) * 8 + half * 4 + (v & 3);
+                    tl[m * PITCH + nt * 32 + l32] = activate(ACT, acc[mt][nt][v] + bn[nt]);
+                }
+        __syncthreads();
+        const int nfrag = ntiles / tilesX;                       // fragments of the launch (tilesY = 1)
+        const int npos = TW - pool_k + 1;
+        for (int idx = tid; idx < npos * CQ; idx += THREADS) {
+            const int pp = idx / CQ, cq = idx - pp * CQ;
+            const int x = tx0 + pp;                              // first sample of the window
+            const int c0 = n_base + cq * 4;
+            if (x >= pool_k * pool_U || c0 >= Cout) continue;
+            float4 mx = *reinterpret_cast<const float4*>(tl + pp * PITCH + cq * 4);
+            for (int t = 1; t < pool_k; ++t) {
+                const float4 q = *reinterpret_cast<const float4*>(tl + (pp + t) * PITCH + cq * 4);
+                mx.x = fmaxf(mx.x, q.x);
+                mx.y = fmaxf(mx.y, q.y);
+                mx.z = fmaxf(mx.z, q.z);
+                mx.w = fmaxf(mx.w, q.w);
+            }
+            const size_t fo = (size_t)(x % pool_k) * nfrag + f;
+            *reinterpret_cast<float4*>(reinterpret_cast<float*>(out) + (fo * pool_U + x / pool_k) * Cout + c0) = mx;
+        }
+    };
+    if constexpr (EPI == kEpiPool) {
+        if (act == 1)
+            store_pool(std::integral_constant<int, 1>{});
+        else if (act == 2)
+            store_pool(std::integral_constant<int, 2>{});
+        else
+            store_pool(std::integral_constant<int, 0>{});
+        return;
+    }
+    if constexpr (EPI == kEpiProj) {
         if (act == 1)
             store_proj(std::integral_constant<int, 1>{});
         else if (act == 2)
@@ -730,9 +789,9 @@ int mfma_tile_mode(const PlanConv& pc, int F, int Hin, int Win, int dil_h, int d
     return L.flat ? 1 : 0;
 }
 
-template <bool BF16, typename Tout, int WGM, int WGN, int MT, int NT, bool PROJ>
+template <bool BF16, typename Tout, int WGM, int WGN, int MT, int NT, int EPI>
 static hipError_t run_mfma(const void* in, int F, int Hin, int Win, int dil_h, int dil_w, int pad_h, int pad_w,
-                           const PlanConv& pc, void* out, float* part, hipStream_t s) {
+                           const PlanConv& pc, void* out, float* part, int pool_k, hipStream_t s) {
     using Cfg = MfmaCfg<BF16, WGM, WGN, MT, NT>;
     const bool dilated = dil_h * dil_w > 1;
     const bool padded = pad_h > 0 || pad_w > 0;
@@ -748,37 +807,62 @@ static hipError_t run_mfma(const void* in, int F, int Hin, int Win, int dil_h, i
         L.t.dbl = 0;
         L.t.lds /= 2;
     }
+    // kEpiPool: spatial tiles of one row of BM samples, stepped by BM - k + 1
+    // columns, and LDS for the tile's activations
+    int tile_step_w = L.t.TW, pool_U = 0;
+    if constexpr (EPI == kEpiPool) {
+        const int Wout = Win - pc.fw + 1;
+        if (BF16 || WGN != 1 || dil_h * dil_w > 1 || pad_h || pad_w || Hin != pc.fh || pool_k < 2 ||
+            pool_k >= Cfg::BM || (Wout - pool_k + 1) % pool_k != 0 || pc.cout % 4 != 0)
+            return hipErrorInvalidValue;
+        pool_U = (Wout - pool_k + 1) / pool_k;
+        tile_step_w = Cfg::BM - pool_k + 1;
+        const int64_t halo_b = ((int64_t)pc.fh * (Cfg::BM + pc.fw - 1) * kPitchBytes + 127) / 128 * 128;
+        if (halo_b > kMaxLds) return hipErrorInvalidValue;
+        L.t = Tile{1, Cfg::BM, (size_t)halo_b, 0};
+        if (pc.cin_pad > Cfg::CC && 2 * halo_b <= kMaxLds) {
+            L.t.dbl = 1;
+            L.t.lds = 2 * halo_b;
+        }
+        L.t.lds = std::max(L.t.lds, (size_t)Cfg::BM * (Cfg::BN + 4) * sizeof(float));
+        L.flat = 0;
+        L.tilesY = 1;
+        L.tilesX = (int)ceil_div64((int64_t)pool_k * pool_U, tile_step_w);
+        L.nblocks = (int64_t)F * L.tilesX * nbs;
+    }
     if (L.nblocks >= (1ll << 31)) return hipErrorInvalidConfiguration;
-    auto kern = conv_mfma_kernel<BF16, Tout, WGM, WGN, MT, NT, PROJ>;
+    auto kern = conv_mfma_kernel<BF16, Tout, WGM, WGN, MT, NT, EPI>;
     hipError_t e = allow_dynamic_lds((const void*)kern, L.t.lds);
     if (e != hipSuccess) return e;
     const int nchunks = pc.cin_pad / Cfg::CC;
     const int Hout = Hin + 2 * pad_h - dil_h * (pc.fh - 1), Wout = Win + 2 * pad_w - dil_w * (pc.fw - 1);
-    if (PROJ && (padded || !pc.w2)) return hipErrorInvalidValue;
-    const int64_t part_stride = PROJ ? (int64_t)F * Hout * Wout * 4 : 0;
+    if (EPI == kEpiProj && (padded || !pc.w2)) return hipErrorInvalidValue;
+    const int64_t part_stride = EPI == kEpiProj ? (int64_t)F * Hout * Wout * 4 : 0;
     if (L.flat) {
         // one "fragment" of 1 x (F * Hin * Win) samples for the staging and the tile grid
         const int flat_len = (int)((int64_t)F * Hin * Win);   // below 2^30 in flat mode
         kern<<<dim3((unsigned)L.nblocks), Cfg::THREADS, L.t.lds, s>>>(
             (const char*)in, 1, flat_len, pc.cin, (const char*)pc.w, pc.b, pc.fh, pc.fw, pc.cout, pc.act, nchunks,
             (Tout*)out, Hout, Wout, 1, L.t.TW, 1, L.tilesX, nbs, L.t.dbl, Hin, Win, 1, 1, 0, 0, pc.w2, part,
-            part_stride);
+            part_stride, L.t.TW, 0, 0);
         return hipGetLastError();
     }
     kern<<<dim3((unsigned)L.nblocks), Cfg::THREADS, L.t.lds, s>>>(
         (const char*)in, Hin, Win, pc.cin, (const char*)pc.w, pc.b, pc.fh, pc.fw, pc.cout, pc.act, nchunks,
         (Tout*)out, Hout, Wout, L.t.TH, L.t.TW, L.tilesY, L.tilesX, nbs, L.t.dbl, 0, 0, dil_h, dil_w, pad_h, pad_w,
-        pc.w2, part, part_stride);
+        pc.w2, part, part_stride, tile_step_w, pool_k, pool_U);
     return hipGetLastError();
 }
 
-template <bool BF16, typename Tout, bool PROJ = false>
+template <bool BF16, typename Tout, int EPI = kEpiStore>
 static hipError_t dispatch_bn(const void* in, int F, int Hin, int Win, int dh, int dw, int ph, int pw,
-                              const PlanConv& pc, void* out, hipStream_t s, float* part = nullptr) {
+                              const PlanConv& pc, void* out, hipStream_t s, float* part = nullptr, int pool_k = 0) {
     switch (pc.bn) {
-        case 128: return run_mfma<BF16, Tout, 2, 2, 4, 2, PROJ>(in, F, Hin, Win, dh, dw, ph, pw, pc, out, part, s);
-        case 64: return run_mfma<BF16, Tout, 4, 1, 2, 2, PROJ>(in, F, Hin, Win, dh, dw, ph, pw, pc, out, part, s);
-        case 32: return run_mfma<BF16, Tout, 4, 1, 2, 1, PROJ>(in, F, Hin, Win, dh, dw, ph, pw, pc, out, part, s);
+        case 128:
+            if constexpr (EPI == kEpiPool) return hipErrorInvalidValue;   // one wave column only
+            else return run_mfma<BF16, Tout, 2, 2, 4, 2, EPI>(in, F, Hin, Win, dh, dw, ph, pw, pc, out, part, 0, s);
+        case 64: return run_mfma<BF16, Tout, 4, 1, 2, 2, EPI>(in, F, Hin, Win, dh, dw, ph, pw, pc, out, part, pool_k, s);
+        case 32: return run_mfma<BF16, Tout, 4, 1, 2, 1, EPI>(in, F, Hin, Win, dh, dw, ph, pw, pc, out, part, pool_k, s);
     }
     return hipErrorInvalidValue;
 }
@@ -802,10 +886,16 @@ hipError_t launch_conv_mfma_bf16(dss_dtype tout, const uint16_t* in, int F, int 
 hipError_t launch_conv_mfma_proj(const void* in, int F, int Hin, int Win, int dil_h, int dil_w, const PlanConv& pc,
                                  float* part, hipStream_t s) {
     if (pc.impl == CONV_MFMA_BF16)
-        return dispatch_bn<true, float, true>(in, F, Hin, Win, dil_h, dil_w, 0, 0, pc, nullptr, s, part);
+        return dispatch_bn<true, float, kEpiProj>(in, F, Hin, Win, dil_h, dil_w, 0, 0, pc, nullptr, s, part);
     if (pc.impl == CONV_MFMA_F32)
-        return dispatch_bn<false, float, true>(in, F, Hin, Win, dil_h, dil_w, 0, 0, pc, nullptr, s, part);
+        return dispatch_bn<false, float, kEpiProj>(in, F, Hin, Win, dil_h, dil_w, 0, 0, pc, nullptr, s, part);
     return hipErrorInvalidValue;
+}
+
+hipError_t launch_conv_mfma_pool(const float* in, int F, int Hin, int Win, const PlanConv& pc, int pool_k, float* out,
+                                 hipStream_t s) {
+    if (pc.impl != CONV_MFMA_F32) return hipErrorInvalidValue;
+    return dispatch_bn<false, float, kEpiPool>(in, F, Hin, Win, 1, 1, 0, 0, pc, out, s, nullptr, pool_k);
 }
 
 }  // namespace dss

@@ -136,6 +136,9 @@ struct dss_plan {
     // evaluations fold it into that convolution's epilogue (convs[L-2].w2) and
     // sum the N blocks' partial projections in the final defragmentation.
     bool fuse_proj = false;
+    // Sliding max-pool + Frag of one-row fragments in the epilogue of the binary32
+    // MFMA convolution before it (off with DSS_FUSE_POOL=0 at plan creation).
+    bool fuse_pool = true;
     float* proj_b = nullptr;              // device [4]: the projection's bias, zero padded
     int proj_cout = 0, proj_act = 0;
     bool timing = false;
@@ -199,6 +202,11 @@ hipError_t launch_window_scatter_sum(const float* part, int nbs, int count, int 
                                      int64_t first, int64_t plane, float* out, hipStream_t s);
 hipError_t launch_planar_sum(const float* part, int nbs, int h, int w, int C, const float* bias, int act, float* out,
                              hipStream_t s);
+// The binary32 MFMA convolution pc (32- or 64-channel N tile) on fragments of
+// one output row, with the sliding max-pool of k samples along the row and
+// Frag_k in its epilogue: out is the pool's fragment tensor [k F][1][U][Cout].
+hipError_t launch_conv_mfma_pool(const float* in, int F, int Hin, int Win, const PlanConv& pc, int pool_k, float* out,
+                                 hipStream_t s);
 // The MFMA convolution pc (taps dil apart when dilated) with the folded 1x1
 // projection (pc.w2): partial projections [groups][F * Hout * Wout][4] per group
 // of 64 channels (32 for the 32-channel N tile) instead of the activations.

@@ -165,3 +165,29 @@ def test_binding_rejects_bad_buffers():
     y = dss.frag(t, 2, 2, 2, 2)
     torch.cuda.synchronize()
     assert y.shape == (16, 3, 4, 4)
+
+
+@pytest.mark.parametrize("name", ["c3_512", "c5_4k", "c2_1d_1m"])
+def test_nan_samples_beyond_the_windows(name):
+    """Samples past the last window that a kept output reads play the role of
+    the dummy samples of Stuff (Theorem "processing chain": the kept outputs do
+    not depend on them).  A signal extended by NaN samples must give finite
+    outputs on every window that lies inside the original signal, equal to the
+    evaluation of the original signal; a leak through Frag, Defrag, Trim or an
+    edge tile would carry a NaN there."""
+    import torch
+    sizes = {"c3_512": dict(H=97, W=110, widths=(16, 32, 48, 64)),
+             "c5_4k": dict(H=170, W=177, widths=(16, 16, 32, 32)), "c2_1d_1m": dict(W=2500)}
+    w = wl.make(name, **sizes[name])
+    plan = dss.Plan.from_workload(w)
+    C, H, W = w.x.shape
+    eh = 0 if name == "c2_1d_1m" else 13
+    xl = np.full((C, H + eh, W + 21), np.nan, dtype=np.float32)
+    xl[:, :H, :W] = w.x
+    a = plan.eval_dense(to_device(w.x, w.dtype))
+    b = plan.eval_dense(to_device(xl, w.dtype))
+    torch.cuda.synchronize()
+    a = a.cpu().numpy().astype(np.float64)
+    b = b.cpu().numpy().astype(np.float64)[:, :a.shape[1], :a.shape[2]]
+    assert np.all(np.isfinite(b)), "a NaN sample reached the output of a window that does not contain it"
+    assert_close(b, a, 1e-6, "%s with NaN samples appended" % name)
