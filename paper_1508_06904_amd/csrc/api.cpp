@@ -320,12 +320,15 @@ extern "C" void dss_plan_destroy(dss_plan_t plan) {
     delete plan;
 }
 
-// Whether the last chain layer, a 1x1 convolution to at most 4 channels with
-// no pool, can be folded into the epilogue of the convolution before it (an
-// MFMA convolution without a pool), and if so its weights in the layout that
-// epilogue reads.  DSS_FUSE_PROJECTION=0 (read at plan creation) turns the
-// fold off, for cross-checks and A/B timing.
-static dss_status setup_projection_fold(dss_plan* p, const dss_layer* layers) {
+// The fusions a plan uses (both can be turned off at plan creation, for
+// cross-checks and A/B timing):
+//  - the sliding max-pool + Frag of one-row fragments in the epilogue of the
+//    convolution before it (decided per launch; DSS_FUSE_POOL=0 turns it off);
+//  - the last chain layer, a 1x1 convolution to at most 4 channels with no
+//    pool, folded into the epilogue of the convolution before it (an MFMA
+//    convolution without a pool), with its weights uploaded in the layout that
+//    epilogue reads (DSS_FUSE_PROJECTION=0 turns it off).
+static dss_status setup_fusions(dss_plan* p, const dss_layer* layers) {
     const Chain& ch = p->chain;
     const int L = ch.L();
     const char* pool_env = getenv("DSS_FUSE_POOL");
@@ -405,7 +408,7 @@ extern "C" dss_status dss_plan_create(const dss_layer* layers, int32_t n_layers,
             return s;
         }
     }
-    s = setup_projection_fold(p, layers);
+    s = setup_fusions(p, layers);
     if (s != DSS_OK) {
         free_plan_memory(p);
         delete p;
