@@ -501,7 +501,9 @@ const char* conv_name(const PlanConv& pc, dss_dtype tout) {
                                                                    : "conv_mfma_bf16_n32_f32out";
             return pc.bn == 128 ? "conv_mfma_bf16_n128" : pc.bn == 64 ? "conv_mfma_bf16_n64" : "conv_mfma_bf16_n32";
         default:
-            // the direct kernel's LDS-staged form for few outputs and many inputs
+            // the direct kernel's forms for few outputs and many inputs: lanes over
+            // input channels, or LDS-staged tiles
+            if (conv_lanesum_ok(pc.cin, pc)) return "conv_lanesum";
             return pc.cin >= 16 && pc.cout_pad <= 8 ? "conv_narrow" : "conv_direct";
     }
 }

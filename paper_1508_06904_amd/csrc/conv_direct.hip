@@ -201,6 +201,177 @@ __global__ __launch_bounds__(256) void conv_narrow_kernel(const Tin* __restrict_
     if (active) store_outputs<Tout, COB>(out, ((int64_t)f * Hout + y) * Wout + x, Cout, og, act, acc);
 }
 
+// Few output channels and input channels a multiple of 64 (the lane-sum form).
+// A wavefront computes P = 64 / COB output samples of one row, consecutive or,
+// in the dilated fashion, dil_w apart (one phase of the row), for COB output
+// channels; lane c owns the input channels c, c + 64, ...  Per filter row and
+// channel group it loads the P + FW - 1 input samples of its channel that the
+// P outputs touch (one 256-byte load per sample across the wavefront, binary32)
+// and its FW x COB weights, and accumulates P x COB partial sums over its own
+// channels: no LDS and no scalar loads in the loop.  A butterfly across the
+// lanes then adds up the 64 partial sums of each output: at each of six steps a
+// lane keeps half of its values, sends the other half to the lane whose index
+// differs in one bit and adds what it receives, so lane l ends with output
+// value l (sample l / COB, channel l % COB), which it stores with bias and
+// activation.  An output's sum has the same order wherever its tile lies, so
+// the dense, strided, mixed and dilated fashions agree bit for bit.
+template <int N>
+__device__ __forceinline__ void lane_reduce_scatter(float (&v)[64], int lane) {
+    // v[0 .. 2N) -> v[0 .. N): lanes with bit N set keep the upper half
+    if constexpr (N >= 16) {
+        // across rows of 16 lanes: swap the upper half-wave (N = 32) or the odd
+        // rows (N = 16) of the lower values with the lower half-wave or the even
+        // rows of the upper values; each lane then holds its own and its
+        // partner's copy of the value it keeps
+#pragma unroll
+        for (int i = 0; i < N; ++i) {
+            const uint32_t a = __float_as_uint(v[i]), b = __float_as_uint(v[i + N]);
+            const auto r = N == 32 ? __builtin_amdgcn_permlane32_swap(a, b, false, false)
+                                   : __builtin_amdgcn_permlane16_swap(a, b, false, false);
+            v[i] = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+        }
+    } else {
+        // within a row: the lower lanes of each pair read lane + N, the upper
+        // ones lane - N (row shifts of the data-parallel primitives)
+        const bool upper = (lane & N) != 0;
+#pragma unroll
+        for (int i = 0; i < N; ++i) {
+            const uint32_t a = __float_as_uint(v[i]), b = __float_as_uint(v[i + N]);
+            const float lo = v[i] + __uint_as_float(__builtin_amdgcn_update_dpp(0u, a, 0x100 + N, 0xf, 0xf, false));
+            const float hi = v[i + N] + __uint_as_float(__builtin_amdgcn_update_dpp(0u, b, 0x110 + N, 0xf, 0xf, false));
+            v[i] = upper ? hi : lo;
+        }
+    }
+    if constexpr (N > 1) lane_reduce_scatter<N / 2>(v, lane);
+}
+
+template <typename Tin, typename Tout, int COB, int FW>
+__global__ __launch_bounds__(256) void conv_lanesum_kernel(const Tin* __restrict__ in, int Hin, int Win, int Cin,
+                                                          const float* __restrict__ w, const float* __restrict__ bias,
+                                                          int fh, int dil_h, int dil_w, int Cout, int CoutP, int act,
+                                                          Tout* __restrict__ out, int Hout, int Wout, int tiles_row,
+                                                          int64_t ntiles) {
+    constexpr int P = 64 / COB;
+    constexpr int NW = P + FW - 1;                    // input samples per row of taps
+    const int lane = threadIdx.x & 63;
+    // A wavefront takes the tiles wave, wave + nwaves, ...; per tile the steps
+    // (filter row, channel group).  The next step's samples and weights load
+    // while this step computes (two register sets, alternating).  Tiles and
+    // addresses but the lane's channel offset are uniform: scalar registers.
+    const int64_t nwaves = (int64_t)gridDim.x * 4;
+    int64_t tile = (int64_t)blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    if (tile >= ntiles) return;
+    const int og = blockIdx.y * COB;
+    const int groups = Cin / 64, steps = fh * groups;
+
+    auto fetch = [&](int64_t tl, int st, float (&win)[NW], float (&wv)[FW][COB]) {
+        const int64_t fr = tl / tiles_row;            // fragment * Hout + output row
+        const int t = (int)(tl - fr * tiles_row);
+        const int x0 = t % dil_w + (t / dil_w) * P * dil_w;
+        const int th = st / groups, c0 = (st - th * groups) * 64;
+        const int64_t f = fr / Hout;
+        const int y = (int)(fr - f * Hout);
+        const Tin* row = in + ((f * Hin + y + th * dil_h) * (int64_t)Win) * Cin + c0;
+#pragma unroll
+        for (int i = 0; i < NW; ++i) {
+            // samples past the row end feed only outputs past its end: read the
+            // last sample instead (no branch around the load), then zero it
+            const int xs = x0 + i * dil_w;
+            const Tin* sample = row + (int64_t)min(xs, Win - 1) * Cin;
+            const float v = to_f32(sample[lane]);
+            win[i] = xs < Win ? v : 0.f;
+        }
+        const float* wrow = w + ((int64_t)th * FW * Cin + c0) * CoutP + og;
+#pragma unroll
+        for (int tw = 0; tw < FW; ++tw)
+#pragma unroll
+            for (int o = 0; o < COB; ++o) wv[tw][o] = (wrow + (int64_t)tw * Cin * CoutP)[lane * CoutP + o];
+    };
+
+    float acc[64];
+#pragma unroll
+    for (int v = 0; v < 64; ++v) acc[v] = 0.f;
+    int st = 0;
+    // one step on (win, wv) with the next step's loads into (nwin, nwv); false
+    // when no step is left
+    auto step = [&](float (&win)[NW], float (&wv)[FW][COB], float (&nwin)[NW], float (&nwv)[FW][COB]) {
+        int64_t ntile = tile;
+        int nst = st + 1;
+        if (nst == steps) {
+            nst = 0;
+            ntile += nwaves;
+        }
+        const bool more = ntile < ntiles;
+        if (more) fetch(ntile, nst, nwin, nwv);
+#pragma unroll
+        for (int tw = 0; tw < FW; ++tw)
+#pragma unroll
+            for (int p = 0; p < P; ++p)
+#pragma unroll
+                for (int o = 0; o < COB; ++o) acc[p * COB + o] = fmaf(win[p + tw], wv[tw][o], acc[p * COB + o]);
+        if (nst == 0) {                               // the tile is complete
+            lane_reduce_scatter<32>(acc, lane);
+            const int64_t fr = tile / tiles_row;
+            const int t = (int)(tile - fr * tiles_row);
+            const int p = lane / COB, o = lane - (lane / COB) * COB;
+            const int x = t % dil_w + (t / dil_w) * P * dil_w + p * dil_w;
+            if (x < Wout && og + o < Cout)
+                store_elem(out + (fr * Wout + x) * Cout + og + o, activate(act, acc[0] + bias[og + o]));
+#pragma unroll
+            for (int v = 0; v < 64; ++v) acc[v] = 0.f;
+        }
+        tile = ntile;
+        st = nst;
+        return more;
+    };
+    float winA[NW], winB[NW], wvA[FW][COB], wvB[FW][COB];
+    fetch(tile, 0, winA, wvA);
+    while (step(winA, wvA, winB, wvB) && step(winB, wvB, winA, wvA)) {
+    }
+}
+
+template <typename Tin, typename Tout, int COB, int FW>
+static void run_lanesum(const void* in, int F, int Hin, int Win, int dh, int dw, int Cin, const PlanConv& pc,
+                        void* out, int Hout, int Wout, hipStream_t s) {
+    constexpr int P = 64 / COB;
+    const int64_t blocks = ceil_div64(ceil_div64(Wout, dw), P);     // per phase of a row
+    const int tiles_row = (int)(blocks * dw);
+    const int64_t ntiles = (int64_t)F * Hout * tiles_row;
+    // as many workgroups as the GPU holds at once, each wavefront looping over
+    // its tiles
+    static const int64_t resident = [] {
+        int per_cu = 0, dev = 0, cus = 0;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, conv_lanesum_kernel<Tin, Tout, COB, FW>, 256, 0) !=
+                hipSuccess ||
+            per_cu < 1)
+            per_cu = 2;
+        if (hipGetDevice(&dev) != hipSuccess ||
+            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1)
+            cus = 256;
+        return (int64_t)per_cu * cus;
+    }();
+    const int64_t wgs = std::min<int64_t>(ceil_div64(ntiles, 4), resident);
+    const dim3 grid((unsigned)wgs, (unsigned)(pc.cout_pad / COB));
+    conv_lanesum_kernel<Tin, Tout, COB, FW><<<grid, 256, 0, s>>>(
+        (const Tin*)in, Hin, Win, Cin, (const float*)pc.w, pc.b, pc.fh, dh, dw, pc.cout, pc.cout_pad, pc.act,
+        (Tout*)out, Hout, Wout, tiles_row, ntiles);
+}
+
+template <typename Tin, typename Tout, int COB>
+static void dispatch_lanesum(const void* in, int F, int Hin, int Win, int dh, int dw, int Cin, const PlanConv& pc,
+                             void* out, int Hout, int Wout, hipStream_t s) {
+    switch (pc.fw) {
+        case 1: run_lanesum<Tin, Tout, COB, 1>(in, F, Hin, Win, dh, dw, Cin, pc, out, Hout, Wout, s); break;
+        case 2: run_lanesum<Tin, Tout, COB, 2>(in, F, Hin, Win, dh, dw, Cin, pc, out, Hout, Wout, s); break;
+        case 3: run_lanesum<Tin, Tout, COB, 3>(in, F, Hin, Win, dh, dw, Cin, pc, out, Hout, Wout, s); break;
+        case 4: run_lanesum<Tin, Tout, COB, 4>(in, F, Hin, Win, dh, dw, Cin, pc, out, Hout, Wout, s); break;
+        case 5: run_lanesum<Tin, Tout, COB, 5>(in, F, Hin, Win, dh, dw, Cin, pc, out, Hout, Wout, s); break;
+        case 6: run_lanesum<Tin, Tout, COB, 6>(in, F, Hin, Win, dh, dw, Cin, pc, out, Hout, Wout, s); break;
+        case 7: run_lanesum<Tin, Tout, COB, 7>(in, F, Hin, Win, dh, dw, Cin, pc, out, Hout, Wout, s); break;
+        default: run_lanesum<Tin, Tout, COB, 8>(in, F, Hin, Win, dh, dw, Cin, pc, out, Hout, Wout, s); break;
+    }
+}
+
 // Tile of the narrow kernel: the width (16 .. 256, a power of two) that computes
 // the fewest masked samples among those whose halo fits 64 KB of LDS and the
 // staging registers; TH = 0 if none does.
@@ -227,6 +398,12 @@ template <typename Tin, typename Tout, int COB>
 static void run_direct(const void* in, int F, int Hin, int Win, int dh, int dw, int Cin, const PlanConv& pc, void* out,
                        hipStream_t s) {
     const int Hout = Hin - dh * (pc.fh - 1), Wout = Win - dw * (pc.fw - 1);
+    if constexpr (COB <= 8) {
+        if (conv_lanesum_ok(Cin, pc)) {
+            dispatch_lanesum<Tin, Tout, COB>(in, F, Hin, Win, dh, dw, Cin, pc, out, Hout, Wout, s);
+            return;
+        }
+    }
     const int kc = pc.fh * pc.fw == 1 ? 32 : 16;
     if (Cin >= 16 && pc.cout_pad <= 8) {
         int TH, TW;

@@ -96,6 +96,14 @@ struct PlanConv {
     float* w2 = nullptr;
 };
 
+// Whether a direct-kernel convolution with Cin input channels runs the lane-sum
+// form (conv_direct.hip): few outputs per launch column, filters at most 8 wide,
+// input channels a multiple of the wavefront width.  Depends on the layer only,
+// so every evaluation fashion sums a layer's outputs in the same order.
+inline bool conv_lanesum_ok(int cin, const PlanConv& pc) {
+    return cin > 0 && cin % 64 == 0 && pc.cob <= 8 && pc.fw >= 1 && pc.fw <= 8;
+}
+
 // The variant a launch over F fragments of Hin x Win (taps dil apart) should use.
 PlanConv mfma_launch_variant(const PlanConv& pc, int F, int Hin, int Win, int dil_h, int dil_w, int pad_h = 0,
                              int pad_w = 0);

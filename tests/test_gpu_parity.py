@@ -464,8 +464,9 @@ def test_timing_records(fold, monkeypatch):
         # would give too few workgroups to fill the GPU)
         assert names[-2:] == ["conv_mfma_f32_n64_proj", "defrag_sum"]
     else:
-        # the final 1x1 projection to 2 channels runs the LDS-staged direct kernel
-        assert names[-2:] == ["conv_narrow", "defrag_trim"]
+        # the final 1x1 projection 128 -> 2 runs the
+        # lane-sum form of the direct kernel
+        assert names[-2:] == ["conv_lanesum", "defrag_trim"]
     g = plan.geometry(120, 130)
     assert sum(r["flops"] for r in recs) == pytest.approx(g["conv_flops"], rel=1e-9)
     assert all(r["ms"] >= 0 for r in recs)

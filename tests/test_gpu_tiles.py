@@ -208,3 +208,52 @@ def test_pool_in_conv_epilogue_1d(case, monkeypatch):
         np.testing.assert_array_equal(fused, ref)
     else:
         assert_close(fused, ref, F32_TOL, "pool fusion %s" % case)
+
+
+LANESUM_CASES = {
+    # (arch, channels, H, W, ndim, dtype, value kind): last layers with input
+    # channels in multiples of 64 and at most 8 output channels per launch column
+    "1d_fw8_cout2": ([("conv", 16, 64, 1, 3, "relu"), ("pool", 1, 2), ("conv", 64, 2, 1, 8, "none")], 16, 1, 3001,
+                     1, "f32", "normal"),
+    "1d_fw5_cout1_c192": ([("conv", 16, 192, 1, 2, "relu"), ("pool", 1, 3), ("conv", 192, 1, 1, 5, "tanh")], 16, 1,
+                          2113, 1, "f32", "uniform"),
+    "2d_3x3_cout3": ([("conv", 16, 64, 3, 3, "relu"), ("pool", 2, 2), ("conv", 64, 3, 3, 3, "none")], 16, 61, 75, 2,
+                     "f32", "uniform"),
+    "2d_2x7_cout8": ([("conv", 16, 128, 2, 2, "relu"), ("conv", 128, 8, 2, 7, "relu")], 16, 40, 77, 2, "f32",
+                     "normal"),
+    "2d_1x1_cout5_bf16": ([("conv", 16, 128, 3, 3, "relu"), ("pool", 2, 2), ("conv", 128, 5, 1, 1, "none")], 16, 57,
+                          66, 2, "bf16", "uniform"),
+    "2d_4x4_cout2_bf16": ([("conv", 32, 64, 2, 2, "relu"), ("pool", 2, 2), ("conv", 64, 64, 2, 2, "relu"),
+                           ("conv", 64, 2, 4, 4, "none")], 32, 70, 53, 2, "bf16", "uniform"),
+    # integer data and weights: every sum exact in binary32, so any summation order
+    # gives the oracle's value bit for bit
+    "int_2d_fw6": ([("conv", 16, 64, 2, 2, "relu"), ("pool", 2, 2), ("conv", 64, 4, 2, 6, "none")], 16, 50, 67, 2,
+                   "f32", "int"),
+}
+
+
+@pytest.mark.parametrize("case", list(LANESUM_CASES))
+def test_lanesum_last_layer(case, monkeypatch):
+    """The lane-sum form of the direct kernel (lanes over input channels, a
+    butterfly across the lanes at the end) on every window against the oracle,
+    for 1 to 8 output channels per launch column, filters 1 to 8 wide, one and
+    two dimensions, binary32 and bfloat16; the launch records name it for the
+    last layer.  Binary32 plans take it for such layers by themselves; bfloat16
+    plans run those on the MFMA tile, so their cases select the direct kernels
+    for every layer."""
+    monkeypatch.setenv("DSS_FUSE_PROJECTION", "0")
+    arch, C, H, W, ndim, dtype, kind = LANESUM_CASES[case]
+    if dtype == "bf16":
+        monkeypatch.setenv("DSS_CONV_KERNEL", "direct")
+    w = wl.custom(arch, C, H, W, seed=53, dtype=dtype, ndim=ndim, value_kind=kind,
+                  weight_kind="int" if kind == "int" else "he")
+    out, recs = timed_dense(w)
+    names = [r["kernel"] for r in recs]
+    log("lanesum %s: %s" % (case, names))
+    assert names[-2] == "conv_lanesum"
+    ref = oracle.eval_stride(oracle_layers(w.layers, dtype), w.x)
+    if kind == "int":
+        assert np.abs(ref).max() < 2 ** 23
+        np.testing.assert_array_equal(out, ref)
+        return
+    assert_close(out, ref, BF16_TOL if dtype == "bf16" else F32_TOL, "lanesum %s" % case)
