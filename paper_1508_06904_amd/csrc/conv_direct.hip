@@ -245,7 +245,10 @@ __device__ __forceinline__ void lane_reduce_scatter(float (&v)[64], int lane) {
     if constexpr (N > 1) lane_reduce_scatter<N / 2>(v, lane);
 }
 
-template <typename Tin, typename Tout, int COB, int FW>
+// Word 3 of a raw buffer resource on gfx9-family GPUs (32-bit data format).
+constexpr int kBufferWord3 = 0x00020000;
+
+template <typename Tin, typename Tout, int COB, int FW, bool ONE_STEP>
 __global__ __launch_bounds__(256) void conv_lanesum_kernel(const Tin* __restrict__ in, int Hin, int Win, int Cin,
                                                           const float* __restrict__ w, const float* __restrict__ bias,
                                                           int fh, int dil_h, int dil_w, int Cout, int CoutP, int act,
@@ -255,32 +258,54 @@ __global__ __launch_bounds__(256) void conv_lanesum_kernel(const Tin* __restrict
     constexpr int NW = P + FW - 1;                    // input samples per row of taps
     const int lane = threadIdx.x & 63;
     // A wavefront takes the tiles wave, wave + nwaves, ...; per tile the steps
-    // (filter row, channel group).  The next step's samples and weights load
-    // while this step computes (two register sets, alternating).  Tiles and
-    // addresses but the lane's channel offset are uniform: scalar registers.
+    // (filter row, channel group).  Loads run ahead of the arithmetic in
+    // rotating register sets: with one step per tile (ONE_STEP: one filter row,
+    // 64 input channels, at least two output channels) the weights stay in
+    // registers and the samples load two tiles ahead, otherwise samples and
+    // weights load one step ahead.  Tiles
+    // and addresses but the lane's channel offset are uniform: scalar registers.
     const int64_t nwaves = (int64_t)gridDim.x * 4;
     int64_t tile = (int64_t)blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     if (tile >= ntiles) return;
     const int og = blockIdx.y * COB;
     const int groups = Cin / 64, steps = fh * groups;
 
-    auto fetch = [&](int64_t tl, int st, float (&win)[NW], float (&wv)[FW][COB]) {
+    auto fetch_samples = [&](int64_t tl, int st, float (&win)[NW]) {
         const int64_t fr = tl / tiles_row;            // fragment * Hout + output row
         const int t = (int)(tl - fr * tiles_row);
         const int x0 = t % dil_w + (t / dil_w) * P * dil_w;
         const int th = st / groups, c0 = (st - th * groups) * 64;
         const int64_t f = fr / Hout;
         const int y = (int)(fr - f * Hout);
+        // the row as a buffer: the sample offset goes in a scalar register, the
+        // lane's channel offset in a vector register, so a load costs no vector
+        // address arithmetic
         const Tin* row = in + ((f * Hin + y + th * dil_h) * (int64_t)Win) * Cin + c0;
+        const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+            (void*)row, 0, (int)(((int64_t)Win * Cin - c0) * (int64_t)sizeof(Tin)), kBufferWord3);
+        const int voff = lane * (int)sizeof(Tin);
+        auto sample = [&](int xs) {
+            // past the row end: the last sample (its outputs are past the end too)
+            const int soff = min(xs, Win - 1) * Cin * (int)sizeof(Tin);
+            if constexpr (sizeof(Tin) == 4)
+                return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs, voff, soff, 0));
+            else
+                return bf16_to_f32(__builtin_amdgcn_raw_buffer_load_b16(rs, voff, soff, 0));
+        };
+        if (x0 + (NW - 1) * dil_w < Win) {            // the whole window lies in the row
 #pragma unroll
-        for (int i = 0; i < NW; ++i) {
-            // samples past the row end feed only outputs past its end: read the
-            // last sample instead (no branch around the load), then zero it
-            const int xs = x0 + i * dil_w;
-            const Tin* sample = row + (int64_t)min(xs, Win - 1) * Cin;
-            const float v = to_f32(sample[lane]);
-            win[i] = xs < Win ? v : 0.f;
+            for (int i = 0; i < NW; ++i) win[i] = sample(x0 + i * dil_w);
+        } else {
+#pragma unroll
+            for (int i = 0; i < NW; ++i) {
+                const int xs = x0 + i * dil_w;
+                const float v = sample(xs);
+                win[i] = xs < Win ? v : 0.f;
+            }
         }
+    };
+    auto fetch_weights = [&](int st, float (&wv)[FW][COB]) {
+        const int th = st / groups, c0 = (st - th * groups) * 64;
         const float* wrow = w + ((int64_t)th * FW * Cin + c0) * CoutP + og;
 #pragma unroll
         for (int tw = 0; tw < FW; ++tw)
@@ -291,58 +316,85 @@ __global__ __launch_bounds__(256) void conv_lanesum_kernel(const Tin* __restrict
     float acc[64];
 #pragma unroll
     for (int v = 0; v < 64; ++v) acc[v] = 0.f;
-    int st = 0;
-    // one step on (win, wv) with the next step's loads into (nwin, nwv); false
-    // when no step is left
-    auto step = [&](float (&win)[NW], float (&wv)[FW][COB], float (&nwin)[NW], float (&nwv)[FW][COB]) {
-        int64_t ntile = tile;
-        int nst = st + 1;
-        if (nst == steps) {
-            nst = 0;
-            ntile += nwaves;
-        }
-        const bool more = ntile < ntiles;
-        if (more) fetch(ntile, nst, nwin, nwv);
+    auto accumulate = [&](const float (&win)[NW], const float (&wv)[FW][COB]) {
 #pragma unroll
         for (int tw = 0; tw < FW; ++tw)
 #pragma unroll
             for (int p = 0; p < P; ++p)
 #pragma unroll
                 for (int o = 0; o < COB; ++o) acc[p * COB + o] = fmaf(win[p + tw], wv[tw][o], acc[p * COB + o]);
-        if (nst == 0) {                               // the tile is complete
-            lane_reduce_scatter<32>(acc, lane);
-            const int64_t fr = tile / tiles_row;
-            const int t = (int)(tile - fr * tiles_row);
-            const int p = lane / COB, o = lane - (lane / COB) * COB;
-            const int x = t % dil_w + (t / dil_w) * P * dil_w + p * dil_w;
-            if (x < Wout && og + o < Cout)
-                store_elem(out + (fr * Wout + x) * Cout + og + o, activate(act, acc[0] + bias[og + o]));
-#pragma unroll
-            for (int v = 0; v < 64; ++v) acc[v] = 0.f;
-        }
-        tile = ntile;
-        st = nst;
-        return more;
     };
-    float winA[NW], winB[NW], wvA[FW][COB], wvB[FW][COB];
-    fetch(tile, 0, winA, wvA);
-    while (step(winA, wvA, winB, wvB) && step(winB, wvB, winA, wvA)) {
+    // the tile is complete: sum across the lanes, store, clear
+    auto finish = [&]() {
+        lane_reduce_scatter<32>(acc, lane);
+        const int64_t fr = tile / tiles_row;
+        const int t = (int)(tile - fr * tiles_row);
+        const int p = lane / COB, o = lane - (lane / COB) * COB;
+        const int x = t % dil_w + (t / dil_w) * P * dil_w + p * dil_w;
+        if (x < Wout && og + o < Cout)
+            store_elem(out + (fr * Wout + x) * Cout + og + o, activate(act, acc[0] + bias[og + o]));
+#pragma unroll
+        for (int v = 0; v < 64; ++v) acc[v] = 0.f;
+    };
+
+    if constexpr (ONE_STEP) {
+        float wv[FW][COB];
+        fetch_weights(0, wv);
+        // tile on `win` while the tile two ahead loads into `nwin`; false when
+        // no tile is left
+        auto step = [&](const float (&win)[NW], float (&nwin)[NW]) {
+            const int64_t ahead = tile + 2 * nwaves;
+            if (ahead < ntiles) fetch_samples(ahead, 0, nwin);
+            accumulate(win, wv);
+            finish();
+            tile += nwaves;
+            return tile < ntiles;
+        };
+        float winA[NW], winB[NW], winC[NW];
+        fetch_samples(tile, 0, winA);
+        if (tile + nwaves < ntiles) fetch_samples(tile + nwaves, 0, winB);
+        while (step(winA, winC) && step(winB, winA) && step(winC, winB)) {
+        }
+    } else {
+        int st = 0;
+        // one step on (win, wv) with the next step's loads into (nwin, nwv);
+        // false when no step is left
+        auto step = [&](const float (&win)[NW], const float (&wv)[FW][COB], float (&nwin)[NW],
+                        float (&nwv)[FW][COB]) {
+            int64_t ntile = tile;
+            int nst = st + 1;
+            if (nst == steps) {
+                nst = 0;
+                ntile += nwaves;
+            }
+            const bool more = ntile < ntiles;
+            if (more) {
+                fetch_samples(ntile, nst, nwin);
+                fetch_weights(nst, nwv);
+            }
+            accumulate(win, wv);
+            if (nst == 0) finish();
+            tile = ntile;
+            st = nst;
+            return more;
+        };
+        float winA[NW], winB[NW], wvA[FW][COB], wvB[FW][COB];
+        fetch_samples(tile, 0, winA);
+        fetch_weights(0, wvA);
+        while (step(winA, wvA, winB, wvB) && step(winB, wvB, winA, wvA)) {
+        }
     }
 }
 
-template <typename Tin, typename Tout, int COB, int FW>
-static void run_lanesum(const void* in, int F, int Hin, int Win, int dh, int dw, int Cin, const PlanConv& pc,
-                        void* out, int Hout, int Wout, hipStream_t s) {
-    constexpr int P = 64 / COB;
-    const int64_t blocks = ceil_div64(ceil_div64(Wout, dw), P);     // per phase of a row
-    const int tiles_row = (int)(blocks * dw);
-    const int64_t ntiles = (int64_t)F * Hout * tiles_row;
+template <typename Tin, typename Tout, int COB, int FW, bool ONE_STEP>
+static void launch_lanesum(const void* in, int Hin, int Win, int dh, int dw, int Cin, const PlanConv& pc, void* out,
+                           int Hout, int Wout, int tiles_row, int64_t ntiles, hipStream_t s) {
     // as many workgroups as the GPU holds at once, each wavefront looping over
     // its tiles
     static const int64_t resident = [] {
         int per_cu = 0, dev = 0, cus = 0;
-        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, conv_lanesum_kernel<Tin, Tout, COB, FW>, 256, 0) !=
-                hipSuccess ||
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, conv_lanesum_kernel<Tin, Tout, COB, FW, ONE_STEP>,
+                                                         256, 0) != hipSuccess ||
             per_cu < 1)
             per_cu = 2;
         if (hipGetDevice(&dev) != hipSuccess ||
@@ -352,9 +404,27 @@ static void run_lanesum(const void* in, int F, int Hin, int Win, int dh, int dw,
     }();
     const int64_t wgs = std::min<int64_t>(ceil_div64(ntiles, 4), resident);
     const dim3 grid((unsigned)wgs, (unsigned)(pc.cout_pad / COB));
-    conv_lanesum_kernel<Tin, Tout, COB, FW><<<grid, 256, 0, s>>>(
+    conv_lanesum_kernel<Tin, Tout, COB, FW, ONE_STEP><<<grid, 256, 0, s>>>(
         (const Tin*)in, Hin, Win, Cin, (const float*)pc.w, pc.b, pc.fh, dh, dw, pc.cout, pc.cout_pad, pc.act,
         (Tout*)out, Hout, Wout, tiles_row, ntiles);
+}
+
+template <typename Tin, typename Tout, int COB, int FW>
+static void run_lanesum(const void* in, int F, int Hin, int Win, int dh, int dw, int Cin, const PlanConv& pc,
+                        void* out, int Hout, int Wout, hipStream_t s) {
+    constexpr int P = 64 / COB;
+    const int64_t blocks = ceil_div64(ceil_div64(Wout, dw), P);     // per phase of a row
+    const int tiles_row = (int)(blocks * dw);
+    const int64_t ntiles = (int64_t)F * Hout * tiles_row;
+    // three sample windows of up to 32 + 7 samples fit beside the accumulators
+    if constexpr (COB >= 2) {
+        if (pc.fh == 1 && Cin == 64) {
+            launch_lanesum<Tin, Tout, COB, FW, true>(in, Hin, Win, dh, dw, Cin, pc, out, Hout, Wout, tiles_row, ntiles,
+                                                     s);
+            return;
+        }
+    }
+    launch_lanesum<Tin, Tout, COB, FW, false>(in, Hin, Win, dh, dw, Cin, pc, out, Hout, Wout, tiles_row, ntiles, s);
 }
 
 template <typename Tin, typename Tout, int COB>
