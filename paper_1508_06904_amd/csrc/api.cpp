@@ -577,6 +577,26 @@ static dss_status run_layers(dss_plan* p, const Geom& G, int upto, char* const b
             return DSS_OK;
         }
         if (c.has_conv && c.has_pool && p->fuse_pool && !lg.relaxed && !lg.dilated && lg.E_h == 1 && lg.Fin_h == 1 &&
+            c.k_h == 1 && c.k_w >= 2 && c.k_w <= 4 && p->convs[j - 1].impl == CONV_DIRECT && c.c_h == 1 && c.cin < 16) {
+            // one-row fragments with few input channels (the first layer of a 1-D
+            // chain; every fashion runs such a layer on the plain direct kernel,
+            // whose summation order the fused kernel keeps): each thread computes
+            // k outputs and writes their maximum straight to its fragment
+            const PlanConv& pc = p->convs[j - 1];
+            void* dst = buf[which ^ 1];
+            const double flops = 2.0 * Fin * (double)lg.E_h * lg.E_w * c.cout * (double)c.cin * c.c_h * c.c_w;
+            const double bytes = (double)Fin * lg.Uin_h * lg.Uin_w * c.cin * dtype_size(cdt) +
+                                 (double)lg.Fout_h * lg.Fout_w * lg.U_h * lg.U_w * c.cout * dtype_size(cdt) +
+                                 (double)c.cout * c.cin * c.c_h * c.c_w * es;
+            e = T.run("conv_direct_pool", j, flops, bytes, [&] {
+                return launch_conv_direct_pool(cdt, cur, Fin, lg.Uin_w, c.cin, pc, c.k_w, lg.U_w, dst, stream);
+            });
+            if (e != hipSuccess) return hip_fail(e, "conv + pool launch");
+            which ^= 1;
+            cur = dst;
+            continue;
+        }
+        if (c.has_conv && c.has_pool && p->fuse_pool && !lg.relaxed && !lg.dilated && lg.E_h == 1 && lg.Fin_h == 1 &&
             c.k_h == 1 && c.k_w >= 2 && c.cout % 4 == 0) {
             // one-row fragments: the sliding max-pool and Frag in the convolution's
             // epilogue, on spatial tiles of 256 samples stepped by 257 - k; taken

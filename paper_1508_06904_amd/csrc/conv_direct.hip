@@ -513,6 +513,98 @@ static void dispatch_cob(const void* in, int F, int Hin, int Win, int dh, int dw
     }
 }
 
+// A direct-kernel convolution of one-row fragments with the following sliding
+// max-pool of k samples along the row and Frag_k (EvalSlide_j = Frag_k o
+// Slide_k o T_j of Definition "processing chain", one launch): a thread takes
+// pooled position x of fragment f and COB output channels, computes the k
+// activated convolution outputs x .. x + k - 1 (each summed in the same order
+// as conv_direct_kernel, from the bias over taps and channels) and writes
+// their maximum to sample x div k of fragment (x mod k) F + f (Lemma
+// "frag-ops" along the row).  The unpooled activations are never stored.
+template <typename Tin, typename Tout, int COB, int KP>
+__global__ __launch_bounds__(256) void conv_direct_pool_kernel(const Tin* __restrict__ in, int Win, int Cin,
+                                                              const float* __restrict__ w,
+                                                              const float* __restrict__ bias, int fw, int Cout,
+                                                              int CoutP, int act, int pool_U, int F,
+                                                              Tout* __restrict__ out, int64_t npos) {
+    // KP = k: the k outputs accumulate side by side, each weight read once per thread
+    const int64_t p = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (p >= npos) return;
+    const int og = blockIdx.y * COB;
+    const int row = KP * pool_U;                       // pooled positions per fragment (before Frag)
+    const int64_t f = p / row;
+    const int x = (int)(p - f * row);
+    const Tin* base = in + (f * Win + x) * Cin;
+    float acc[KP][COB];
+#pragma unroll
+    for (int t = 0; t < KP; ++t)
+#pragma unroll
+        for (int o = 0; o < COB; ++o) acc[t][o] = bias[og + o];
+    for (int tw = 0; tw < fw; ++tw) {
+        const float* wr = w + (int64_t)tw * Cin * CoutP + og;
+        for (int i = 0; i < Cin; ++i) {
+            float wv[COB];
+#pragma unroll
+            for (int o = 0; o < COB; ++o) wv[o] = wr[(int64_t)i * CoutP + o];
+#pragma unroll
+            for (int t = 0; t < KP; ++t) {
+                const float v = to_f32(base[(int64_t)(t + tw) * Cin + i]);
+#pragma unroll
+                for (int o = 0; o < COB; ++o) acc[t][o] = fmaf(v, wv[o], acc[t][o]);
+            }
+        }
+    }
+    float mx[COB];
+#pragma unroll
+    for (int o = 0; o < COB; ++o) {
+        mx[o] = activate(act, acc[0][o]);
+#pragma unroll
+        for (int t = 1; t < KP; ++t) mx[o] = fmaxf(mx[o], activate(act, acc[t][o]));
+    }
+    const int64_t fo = (int64_t)(x % KP) * F + f;
+    store_outputs<Tout, COB>(out, fo * pool_U + x / KP, Cout, og, 0, mx);
+}
+
+template <typename Tin, typename Tout, int KP>
+static void dispatch_direct_pool(const void* in, int F, int Win, int Cin, const PlanConv& pc, int pool_U, void* out,
+                                 hipStream_t s) {
+    const int64_t npos = (int64_t)F * KP * pool_U;
+    const dim3 grid((unsigned)ceil_div64(npos, 256), (unsigned)(pc.cout_pad / pc.cob));
+#define DSS_DIRECT_POOL(C)                                                                                            \
+    conv_direct_pool_kernel<Tin, Tout, C, KP><<<grid, 256, 0, s>>>((const Tin*)in, Win, Cin, (const float*)pc.w, pc.b, \
+                                                                   pc.fw, pc.cout, pc.cout_pad, pc.act, pool_U, F,      \
+                                                                   (Tout*)out, npos)
+    switch (pc.cob) {
+        case 16: DSS_DIRECT_POOL(16); break;
+        case 8: DSS_DIRECT_POOL(8); break;
+        case 4: DSS_DIRECT_POOL(4); break;
+        case 2: DSS_DIRECT_POOL(2); break;
+        default: DSS_DIRECT_POOL(1); break;
+    }
+#undef DSS_DIRECT_POOL
+}
+
+template <typename Tin, typename Tout>
+static hipError_t dispatch_pool_k(const void* in, int F, int Win, int Cin, const PlanConv& pc, int pool_k, int pool_U,
+                                  void* out, hipStream_t s) {
+    switch (pool_k) {
+        case 2: dispatch_direct_pool<Tin, Tout, 2>(in, F, Win, Cin, pc, pool_U, out, s); break;
+        case 3: dispatch_direct_pool<Tin, Tout, 3>(in, F, Win, Cin, pc, pool_U, out, s); break;
+        case 4: dispatch_direct_pool<Tin, Tout, 4>(in, F, Win, Cin, pc, pool_U, out, s); break;
+        default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_conv_direct_pool(dss_dtype dt, const void* in, int F, int Win, int Cin, const PlanConv& pc,
+                                   int pool_k, int pool_U, void* out, hipStream_t s) {
+    if (pc.fh != 1 || pool_k < 2 || pool_k > 4 || (Win - pc.fw + 1) - pool_k + 1 != pool_k * pool_U)
+        return hipErrorInvalidValue;
+    if (F <= 0 || pool_U <= 0) return hipSuccess;
+    if (dt == DSS_F32) return dispatch_pool_k<float, float>(in, F, Win, Cin, pc, pool_k, pool_U, out, s);
+    return dispatch_pool_k<uint16_t, uint16_t>(in, F, Win, Cin, pc, pool_k, pool_U, out, s);
+}
+
 hipError_t launch_conv_direct(dss_dtype tin, dss_dtype tout, const void* in, int F, int Hin, int Win, int dil_h,
                               int dil_w, int Cin, const PlanConv& pc, void* out, hipStream_t s) {
     if (tin == DSS_F32)

@@ -525,46 +525,50 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
             }
         }
     };
-    // kEpiPool (fragments of one row, binary32, one wave column): the tile's
-    // activations go to LDS as [BM][BN + 4] floats; each thread then forms the
-    // maxima of k consecutive samples for the tile's first TW - k + 1 positions
+    // kEpiPool (fragments of one row, binary32, one wave column): per group of
+    // 32 channels (one accumulator column of every wave) the tile's activations
+    // go to LDS as [BM][32 + 4] floats (37 KB: with the halo buffers, three
+    // workgroups still fit a CU); each thread then forms the maxima of k
+    // consecutive samples for the tile's first TW - k + 1 positions
     // (neighbouring tiles overlap by k - 1 samples, so every window lies inside
     // one tile) and writes each maximum straight to its fragment: sample x of
     // input fragment f goes to sample x div k of fragment (x mod k) F + f, F the
     // launch's fragment count (Lemma "frag-ops" along the row).
     auto store_pool = [&](auto act_c) {
         constexpr int ACT = decltype(act_c)::value;
-        constexpr int PITCH = Cfg::BN + 4;
-        constexpr int CQ = Cfg::BN / 4;
+        constexpr int PITCH = 32 + 4;
+        constexpr int CQ = 32 / 4;
         float* tl = reinterpret_cast<float*>(lds);
-        __syncthreads();                                         // every wave is done with the halo
+        const int nfrag = ntiles / tilesX;                       // fragments of the launch (tilesY = 1)
+        const int npos = TW - pool_k + 1;
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
+        for (int nt = 0; nt < NT; ++nt) {
+            __syncthreads();                                     // the halo / the previous group is done with
 #pragma unroll
-            for (int nt = 0; nt < NT; ++nt)
+            for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
                 for (int v = 0; v < 16; ++v) {
                     const int m = wm * 32 * MT + mt * 32 + (v >> 2) * 8 + half * 4 + (v & 3);
-                    tl[m * PITCH + nt * 32 + l32] = activate(ACT, acc[mt][nt][v] + bn[nt]);
+                    tl[m * PITCH + l32] = activate(ACT, acc[mt][nt][v] + bn[nt]);
                 }
-        __syncthreads();
-        const int nfrag = ntiles / tilesX;                       // fragments of the launch (tilesY = 1)
-        const int npos = TW - pool_k + 1;
-        for (int idx = tid; idx < npos * CQ; idx += THREADS) {
-            const int pp = idx / CQ, cq = idx - pp * CQ;
-            const int x = tx0 + pp;                              // first sample of the window
-            const int c0 = n_base + cq * 4;
-            if (x >= pool_k * pool_U || c0 >= Cout) continue;
-            float4 mx = *reinterpret_cast<const float4*>(tl + pp * PITCH + cq * 4);
-            for (int t = 1; t < pool_k; ++t) {
-                const float4 q = *reinterpret_cast<const float4*>(tl + (pp + t) * PITCH + cq * 4);
-                mx.x = fmaxf(mx.x, q.x);
-                mx.y = fmaxf(mx.y, q.y);
-                mx.z = fmaxf(mx.z, q.z);
-                mx.w = fmaxf(mx.w, q.w);
+            __syncthreads();
+            for (int idx = tid; idx < npos * CQ; idx += THREADS) {
+                const int pp = idx / CQ, cq = idx - pp * CQ;
+                const int x = tx0 + pp;                          // first sample of the window
+                const int c0 = n_base + nt * 32 + cq * 4;
+                if (x >= pool_k * pool_U || c0 >= Cout) continue;
+                float4 mx = *reinterpret_cast<const float4*>(tl + pp * PITCH + cq * 4);
+                for (int t = 1; t < pool_k; ++t) {
+                    const float4 q = *reinterpret_cast<const float4*>(tl + (pp + t) * PITCH + cq * 4);
+                    mx.x = fmaxf(mx.x, q.x);
+                    mx.y = fmaxf(mx.y, q.y);
+                    mx.z = fmaxf(mx.z, q.z);
+                    mx.w = fmaxf(mx.w, q.w);
+                }
+                const size_t fo = (size_t)(x % pool_k) * nfrag + f;
+                *reinterpret_cast<float4*>(reinterpret_cast<float*>(out) + (fo * pool_U + x / pool_k) * Cout + c0) =
+                    mx;
             }
-            const size_t fo = (size_t)(x % pool_k) * nfrag + f;
-            *reinterpret_cast<float4*>(reinterpret_cast<float*>(out) + (fo * pool_U + x / pool_k) * Cout + c0) = mx;
         }
     };
     if constexpr (EPI == kEpiPool) {
@@ -824,7 +828,7 @@ static hipError_t run_mfma(const void* in, int F, int Hin, int Win, int dil_h, i
             L.t.dbl = 1;
             L.t.lds = 2 * halo_b;
         }
-        L.t.lds = std::max(L.t.lds, (size_t)Cfg::BM * (Cfg::BN + 4) * sizeof(float));
+        L.t.lds = std::max(L.t.lds, (size_t)Cfg::BM * (32 + 4) * sizeof(float));
         L.flat = 0;
         L.tilesY = 1;
         L.tilesX = (int)ceil_div64((int64_t)pool_k * pool_U, tile_step_w);

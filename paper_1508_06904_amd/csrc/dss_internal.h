@@ -145,7 +145,8 @@ struct dss_plan {
     // sum the N blocks' partial projections in the final defragmentation.
     bool fuse_proj = false;
     // Sliding max-pool + Frag of one-row fragments in the epilogue of the binary32
-    // MFMA convolution before it (off with DSS_FUSE_POOL=0 at plan creation).
+    // MFMA convolution before it, or in the direct kernel of a first layer (off
+    // with DSS_FUSE_POOL=0 at plan creation).
     bool fuse_pool = true;
     float* proj_b = nullptr;              // device [4]: the projection's bias, zero padded
     int proj_cout = 0, proj_act = 0;
@@ -180,6 +181,12 @@ hipError_t launch_stuff_pack(dss_dtype dt, const void* in, int C, int H, int W, 
 // Hin - dil_h (fh - 1) x Win - dil_w (fw - 1) samples.
 hipError_t launch_conv_direct(dss_dtype tin, dss_dtype tout, const void* in, int F, int Hin, int Win,
                               int dil_h, int dil_w, int Cin, const PlanConv& pc, void* out, hipStream_t s);
+// A direct-kernel convolution of F one-row fragments of Win samples (dtype dt in
+// and out) with the following sliding max-pool of pool_k (2 to 4) samples and Frag:
+// pool_k F fragments of pool_U samples (the convolution's Win - fw + 1 outputs
+// must be pool_k pool_U + pool_k - 1).
+hipError_t launch_conv_direct_pool(dss_dtype dt, const void* in, int F, int Win, int Cin, const PlanConv& pc,
+                                   int pool_k, int pool_U, void* out, hipStream_t s);
 hipError_t launch_conv_mfma_f32(const float* in, int F, int Hin, int Win, int dil_h, int dil_w,
                                 const PlanConv& pc, float* out, hipStream_t s);
 hipError_t launch_conv_mfma_bf16(dss_dtype tout, const uint16_t* in, int F, int Hin, int Win, int dil_h,

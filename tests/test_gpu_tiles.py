@@ -173,41 +173,51 @@ def test_projection_fold(case, monkeypatch):
 
 
 POOL_CASES = {
-    # (arch, channels, W, value kind): 1-D chains whose MFMA layers carry the pool
+    # (arch, channels, W, value kind, dtype): 1-D chains whose convolutions carry the pool
     "c2_pattern": ([("conv", 1, 16, 1, 9, "relu"), ("pool", 1, 2), ("conv", 16, 32, 1, 9, "relu"), ("pool", 1, 2),
-                    ("conv", 32, 64, 1, 9, "relu"), ("pool", 1, 2), ("conv", 64, 2, 1, 8, "none")], 1, 20011, "normal"),
+                    ("conv", 32, 64, 1, 9, "relu"), ("pool", 1, 2), ("conv", 64, 2, 1, 8, "none")], 1, 20011, "normal",
+                   "f32"),
     "k3_ragged": ([("conv", 16, 20, 1, 7, "tanh"), ("pool", 1, 3), ("conv", 20, 36, 1, 5, "relu"), ("pool", 1, 2),
-                   ("conv", 36, 2, 1, 4, "none")], 16, 6007, "uniform"),
+                   ("conv", 36, 2, 1, 4, "none")], 16, 6007, "uniform", "f32"),
     "int_exact": ([("conv", 16, 24, 1, 3, "relu"), ("pool", 1, 2), ("conv", 24, 40, 1, 2, "relu"), ("pool", 1, 3),
-                   ("conv", 40, 3, 1, 2, "none")], 16, 5003, "int"),
+                   ("conv", 40, 3, 1, 2, "none")], 16, 5003, "int", "f32"),
+    # first layers on the direct kernel: 3 channels, tanh, k = 3; bfloat16 (the
+    # MFMA convolutions of bfloat16 plans keep the separate pool)
+    "direct_k3_tanh": ([("conv", 3, 8, 1, 4, "tanh"), ("pool", 1, 3), ("conv", 8, 2, 1, 3, "none")], 3, 4001, "normal",
+                       "f32"),
+    "direct_bf16": ([("conv", 1, 16, 1, 9, "relu"), ("pool", 1, 2), ("conv", 16, 32, 1, 5, "relu"), ("pool", 1, 2),
+                     ("conv", 32, 2, 1, 4, "none")], 1, 8009, "uniform", "bf16"),
 }
 
 
 @pytest.mark.parametrize("case", list(POOL_CASES))
 def test_pool_in_conv_epilogue_1d(case, monkeypatch):
     """One-row fragments: the sliding max-pool and Frag computed in the MFMA
-    convolution's epilogue (tiles overlapping by k - 1 samples) against the
+    convolution's epilogue (tiles overlapping by k - 1 samples) or, for layers
+    with few input channels, in the direct convolution kernel, against the
     separate pool + Frag kernel (bit-identical: maxima of the same values) and
     the oracle."""
-    arch, C, W, kind = POOL_CASES[case]
-    w = wl.custom(arch, C, 1, W, seed=41, ndim=1, value_kind=kind, weight_kind="int" if kind == "int" else "he")
+    arch, C, W, kind, dtype = POOL_CASES[case]
+    w = wl.custom(arch, C, 1, W, seed=41, ndim=1, dtype=dtype, value_kind=kind,
+                  weight_kind="int" if kind == "int" else "he")
     fused, rf = timed_dense(w)
     monkeypatch.setenv("DSS_FUSE_POOL", "0")
     plain, rp = timed_dense(w)
     nf = [r["kernel"] for r in rf]
     npl = [r["kernel"] for r in rp]
     log("pool fusion %s: %s / %s" % (case, nf, npl))
-    n_mfma_pooled = sum(1 for t in range(len(arch) - 1) if arch[t][0] == "conv" and arch[t][1] >= 16
-                        and arch[t + 1][0] == "pool")
-    assert sum(n.endswith("_pool") for n in nf) == n_mfma_pooled >= 1
+    pairs = [arch[t] for t in range(len(arch) - 1) if arch[t][0] == "conv" and arch[t + 1][0] == "pool"]
+    n_fused = sum(1 for c in pairs if c[1] < 16 or dtype == "f32")
+    assert sum(n.endswith("_pool") for n in nf) == n_fused >= 1
+    assert nf.count("conv_direct_pool") == sum(1 for c in pairs if c[1] < 16)
     assert not any(n.endswith("_pool") for n in npl)
-    assert npl.count("pool_frag") - nf.count("pool_frag") == n_mfma_pooled
+    assert npl.count("pool_frag") - nf.count("pool_frag") == n_fused
     np.testing.assert_array_equal(fused, plain)
-    ref = oracle.eval_stride(w.layers, w.x)
+    ref = oracle.eval_stride(oracle_layers(w.layers, dtype), w.x)
     if kind == "int":
         np.testing.assert_array_equal(fused, ref)
     else:
-        assert_close(fused, ref, F32_TOL, "pool fusion %s" % case)
+        assert_close(fused, ref, BF16_TOL if dtype == "bf16" else F32_TOL, "pool fusion %s" % case)
 
 
 LANESUM_CASES = {
