@@ -607,6 +607,9 @@ hipError_t launch_conv_direct_pool(dss_dtype dt, const void* in, int F, int Win,
 
 hipError_t launch_conv_direct(dss_dtype tin, dss_dtype tout, const void* in, int F, int Hin, int Win, int dil_h,
                               int dil_w, int Cin, const PlanConv& pc, void* out, hipStream_t s) {
+    // the lane-sum form addresses a row as a buffer of at most 2^31 bytes
+    if (conv_lanesum_ok(Cin, pc) && (int64_t)Win * Cin * (tin == DSS_F32 ? 4 : 2) > INT32_MAX)
+        return hipErrorInvalidValue;
     if (tin == DSS_F32)
         dispatch_cob<float, float>(in, F, Hin, Win, dil_h, dil_w, Cin, pc, out, s);
     else if (tout == DSS_F32)
