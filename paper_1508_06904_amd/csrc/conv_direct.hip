@@ -8,10 +8,16 @@
 // (t_h, t_w) reads sample (y + dil_h t_h, x + dil_w t_w) of a single signal.
 // Used for the layers that do not suit the MFMA implicit GEMM: the first layer
 // (few input channels) and the final projections (few output channels, where
-// an MFMA tile of 32 channels would be mostly idle).  One thread computes COB
-// consecutive output channels of one output sample; the weight reads are
-// uniform across the wavefront and go through the scalar cache.  Accumulation
-// is binary32 (bfloat16 activations are widened).
+// an MFMA tile of 32 channels would be mostly idle).  Three forms:
+//  - conv_direct_kernel: one thread computes COB consecutive output channels of
+//    one output sample; the weight reads are uniform across the wavefront and
+//    go through the scalar cache (first layers; conv_direct_pool_kernel is its
+//    1-D variant with the following sliding max-pool and Frag);
+//  - conv_lanesum_kernel: lanes over input channels (a multiple of 64), a
+//    butterfly across the lanes per output (few output channels);
+//  - conv_narrow_kernel: LDS-staged tiles, one thread per output sample (few
+//    output channels, 16 or more input channels not a multiple of 64).
+// Accumulation is binary32 (bfloat16 activations are widened).
 #include "dev_common.h"
 #include "dss_internal.h"
 
