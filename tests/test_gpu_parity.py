@@ -135,6 +135,10 @@ CHAINS = {
     "1d_c2_like": ([("conv", 1, 16, 1, 9, "relu"), ("pool", 1, 2), ("conv", 16, 32, 1, 9, "relu"), ("pool", 1, 2),
                     ("conv", 32, 64, 1, 9, "relu"), ("pool", 1, 2), ("conv", 64, 2, 1, 8, "none")], 1, 1),
     "2d_ragged_cin": ([("conv", 20, 36, 3, 3, "relu"), ("pool", 2, 2), ("conv", 36, 20, 2, 2, "none")], 20, 2),
+    # last layer on the lane-sum kernel (64 input channels, 3 outputs in two launch
+    # columns, a 3 x 2 filter): taps k*_2 = 4 apart in the dilated fashion
+    "2d_lanesum_last": ([("conv", 3, 16, 3, 3, "relu"), ("pool", 2, 2), ("conv", 16, 64, 2, 2, "relu"), ("pool", 2, 2),
+                         ("conv", 64, 3, 3, 2, "none")], 3, 2),
 }
 
 
