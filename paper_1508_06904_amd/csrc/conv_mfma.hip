@@ -33,8 +33,8 @@
 // every product pairs an input sample with its own weight.
 //
 // Epilogue: + bias, activation, masked store (edge tiles, padded channels) in
-// the channels-last output layout; binary32, or bfloat16 (round to nearest even)
-// transposed through LDS into 16-byte stores of 8 channels.
+// the channels-last output layout, transposed through LDS into 16-byte stores
+// (4 binary32 or 8 bfloat16 channels, round to nearest even, of one position).
 #include <algorithm>
 
 #include <type_traits>
@@ -423,6 +423,42 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
                                 *reinterpret_cast<const u32x4*>(st + row * WCOLS + c8);
                     }
                     __builtin_amdgcn_wave_barrier();
+                }
+                return;
+            }
+        } else {
+            // binary32 output: the same transposition, per 32 x 32 block (4.5 KB per
+            // wave, within any halo buffer; a 36-float pitch puts the two lane
+            // halves' rows in different banks), into 16-byte units of 4 channels:
+            // 4x fewer store instructions, each lane-group writing 128 contiguous
+            // bytes of one position
+            if (Cout % 4 == 0 && ((uintptr_t)out & 15) == 0) {
+                constexpr int PITCH = 36;
+                float* st = reinterpret_cast<float*>(lds) + wave * (32 * PITCH);
+                __syncthreads();                                        // every wave is done with the halo
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt) {
+#pragma unroll
+                    for (int nt = 0; nt < NT; ++nt) {
+#pragma unroll
+                        for (int v = 0; v < 16; ++v) {
+                            const int i = (v >> 2) * 8 + half * 4 + (v & 3);
+                            st[i * PITCH + l32] = activate(ACT, acc[mt][nt][v] + bn[nt]);
+                        }
+                        // this wave's own region, LDS operations in order: no workgroup barrier
+                        __builtin_amdgcn_wave_barrier();
+#pragma unroll
+                        for (int r = 0; r < 4; ++r) {                   // 32 rows x 8 units, 64 per round
+                            const int u = r * 64 + lane;
+                            const int row = u >> 3, c4 = (u & 7) * 4;
+                            const int c = n_base + nt * 32 + c4;
+                            size_t o;
+                            if (out_pos(wm * 32 * MT + mt * 32 + row, o) && c < Cout)
+                                *reinterpret_cast<float4*>(out + o * Cout + c) =
+                                    *reinterpret_cast<const float4*>(st + row * PITCH + c4);
+                        }
+                        __builtin_amdgcn_wave_barrier();
+                    }
                 }
                 return;
             }
