@@ -30,7 +30,10 @@
 // K-index assignment inside one MFMA issue: lane half h (lanes 32h..32h+31)
 // holds input channels h*8 + s (binary32, issue s of 8) or h*16 + 8s .. +7
 // (bfloat16, issue s of 2) of the chunk; A and B use the same assignment, so
-// every product pairs an input sample with its own weight.
+// every product pairs an input sample with its own weight.  The bfloat16
+// variant with a folded 1x1 projection computes the transposed blocks
+// (B^T A^T), which puts one sample and runs of four channels in each lane for
+// its dot products.
 //
 // Epilogue: + bias, activation, masked store (edge tiles, padded channels) in
 // the channels-last output layout, transposed through LDS into 16-byte stores
@@ -114,7 +117,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int wave = tid >> 6;
+    // The wave index is uniform; held as a scalar it frees the vector registers
+    // that its derived values would keep through the K loop (bfloat16 layers
+    // 1-4 % faster, binary32 ones 0.4-0.7 %), except in the binary32 kernel
+    // with the folded projection, which measured 0.3 % slower that way.
+    const int wave = (BF16 || EPI != kEpiProj) ? __builtin_amdgcn_readfirstlane(tid >> 6) : tid >> 6;
     const int wm = wave % WGM;           // wave position along M
     const int wn = wave / WGM;           // wave position along N
     const int half = lane >> 5;          // lane half: K slot of the MFMA operands
@@ -261,6 +268,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt)
                 a[s][mt] = *reinterpret_cast<const u32x4*>(halo + a_off[mt] + tap_off + 16 * s);
+        // bfloat16 kEpiProj computes the transposed block (weights first)
+        constexpr bool TR = EPI == kEpiProj && BF16;
         if constexpr (BF16) {
 #pragma unroll
             for (int s = 0; s < 2; ++s)
@@ -268,18 +277,22 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
                 for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
                     for (int nt = 0; nt < NT; ++nt)
-                        acc[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                            as_bf16x8(a[s][mt]), as_bf16x8(bb[nt][s]), acc[mt][nt], 0, 0, 0);
+                        acc[mt][nt] = TR ? __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                                               as_bf16x8(bb[nt][s]), as_bf16x8(a[s][mt]), acc[mt][nt], 0, 0, 0)
+                                         : __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                                               as_bf16x8(a[s][mt]), as_bf16x8(bb[nt][s]), acc[mt][nt], 0, 0, 0);
         } else {
 #pragma unroll
             for (int s = 0; s < 8; ++s)
 #pragma unroll
                 for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-                    for (int nt = 0; nt < NT; ++nt)
-                        acc[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x2f32(
-                            __uint_as_float(a[s >> 2][mt][s & 3]), __uint_as_float(bb[nt][s >> 2][s & 3]),
-                            acc[mt][nt], 0, 0, 0);
+                    for (int nt = 0; nt < NT; ++nt) {
+                        const float av = __uint_as_float(a[s >> 2][mt][s & 3]);
+                        const float bv = __uint_as_float(bb[nt][s >> 2][s & 3]);
+                        acc[mt][nt] = TR ? __builtin_amdgcn_mfma_f32_32x32x2f32(bv, av, acc[mt][nt], 0, 0, 0)
+                                         : __builtin_amdgcn_mfma_f32_32x32x2f32(av, bv, acc[mt][nt], 0, 0, 0);
+                    }
         }
     };
     // The next chunk's halo is staged by the same copies as stage_halo, but
@@ -501,13 +514,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
     //   part[group][sample][o] = sum_{n in group} w2[n][o] * act(acc[sample][n] + bias[n]),
     // summed over the groups in order, with the projection's bias and activation,
     // by the step that reads it.  The groups do not depend on the N tile of the
-    // launch, so every evaluation fashion sums in the same order.  A lane holds
-    // one channel of 16 samples per 32x32 tile; per sample it first adds its NT
-    // channels' products, then the lanes of a half are reduced in two passes of
-    // 8 samples x 4 outputs by five butterfly exchanges that halve the values a
-    // lane keeps (32 -> 1), so in pass p lane l32 ends with output o = l32 mod 4
-    // of sample slot v = 8 p + l32 / 4.
-    auto store_proj = [&](auto act_c) {
+    // launch, so every evaluation fashion sums in the same order.
+    //
+    // binary32 (store_proj_lanes): a lane holds one channel of 16 samples per
+    // 32x32 tile; per sample it first adds its NT channels' products, then the
+    // lanes of a half are reduced in two passes of 8 samples x 4 outputs by five
+    // butterfly exchanges that halve the values a lane keeps (32 -> 1), so in
+    // pass p lane l32 ends with output o = l32 mod 4 of sample slot v = 8 p + l32 / 4.
+    auto store_proj_lanes = [&](auto act_c) {
         constexpr int ACT = decltype(act_c)::value;
         // keeps the projection weights' loads here: hoisted above the K loop they
         // would hold registers through it
@@ -517,8 +531,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
         for (int nt = 0; nt < NT; ++nt)
             wv[nt] = ncol[nt] < Cout ? *reinterpret_cast<const float4*>(w2 + 4 * (size_t)ncol[nt])
                                      : make_float4(0.f, 0.f, 0.f, 0.f);
-        // the wave's position as scalars: the vector wm / wn feed the K loop's
-        // addresses, and sharing them would keep those values live through it
+        // the wave's position as scalars: when the vector wm / wn feed the K
+        // loop's addresses, sharing them would keep those values live through it
         const int wm_s = __builtin_amdgcn_readfirstlane(wm), wn_s = __builtin_amdgcn_readfirstlane(wn);
         float* part_g = part + (size_t)(nb * WGN + wn_s) * part_stride;
         const int oc = l32 & 3;
@@ -559,6 +573,94 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
                 size_t o;
                 if (out_pos(m, o)) part_g[o * 4 + oc] = v32[0];
             }
+        }
+    };
+    // bfloat16 (store_proj): the kernel computes the transposed 32x32 blocks
+    // (the MFMAs take the weights as their first operand), so D[i][j], i a
+    // channel and j a sample, sits in lane j + 32*((i/4)%2), register
+    // (i/8)*4 + i%4: a lane holds one sample and, in its register group
+    // g = v/4, the four consecutive channels 8g + 4*half .. +3.  A lane adds the
+    // products of its 16 NT channels of its sample (columns nt, then register
+    // groups, then the group's channels, in order), and one exchange between
+    // the lane halves (v_permlane32_swap) adds the other 16 NT: the lower half's
+    // sum first, outputs 0 and 1 in the lower lane and 2 and 3 in the upper one.
+    // On the 4K frame's 6x6 layer that ran 4.7-5.9 % faster than the butterfly
+    // form; the binary32 HD frame's 6x6 layer ran 0.3 % slower with it.
+    auto store_proj = [&](auto act_c) {
+        constexpr int ACT = decltype(act_c)::value;
+        // The lane's position again, from the lane-id instructions: the values
+        // computed at entry feed the K loop, and sharing them would keep them
+        // live through it.
+        const int lane_e = __builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u));
+        const int ll = lane_e & 31, lh = lane_e >> 5;
+        const int p_base = nb * Cfg::BN + wn * 32 * NT;
+        // Loads from the read-only kernel arguments are invariant to the
+        // compiler, which may move them anywhere, up to before the K loop, where
+        // their registers would stay live through it: an opaque zero added to
+        // the pointer per use keeps each load in its place.
+        auto pinned = [](const float* q) {
+            int zero = 0;
+            asm volatile("" : "+s"(zero));
+            return q + zero;
+        };
+        // first channel of register group g of accumulator column nt (a multiple
+        // of 4; bias and w2 hold at least p_base + 32 NT rows)
+        auto group_chan = [&](int nt, int g) { return p_base + nt * 32 + g * 8 + lh * 4; };
+        auto bias4 = [&](int nt, int g) {
+            return *reinterpret_cast<const float4*>(pinned(bias) + group_chan(nt, g));
+        };
+        float ps[MT][4];
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int o = 0; o < 4; ++o) ps[mt][o] = 0.f;
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+                // One register group at a time: its weights, then its values.
+                // Each value passes through an (empty) ordered asm statement, so
+                // the activations cannot all be computed up front, where their
+                // results would not fit beside the accumulators.
+                const int c = group_chan(nt, g);
+                const float4 b = bias4(nt, g);
+                const float bv[4] = {b.x, b.y, b.z, b.w};
+                const float* w2g = pinned(w2);
+                float4 wq[4];
+#pragma unroll
+                for (int u = 0; u < 4; ++u) wq[u] = *reinterpret_cast<const float4*>(w2g + 4 * (size_t)(c + u));
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+                    for (int u = 0; u < 4; ++u) {
+                        float x = acc[mt][nt][4 * g + u];
+                        asm volatile("" : "+v"(x));
+                        const float a = activate(ACT, x + bv[u]);
+                        ps[mt][0] += a * wq[u].x;
+                        ps[mt][1] += a * wq[u].y;
+                        ps[mt][2] += a * wq[u].z;
+                        ps[mt][3] += a * wq[u].w;
+                    }
+                // ... and the group's sums are complete before the next group's values
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+                    for (int o = 0; o < 4; ++o) asm volatile("" : "+v"(ps[mt][o]));
+            }
+        float* part_g = part + (size_t)(nb * WGN + wn) * part_stride;
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+            size_t o;
+            const bool ok = out_pos(wm * 32 * MT + mt * 32 + ll, o);
+            const auto r0 = __builtin_amdgcn_permlane32_swap(__float_as_uint(ps[mt][0]), __float_as_uint(ps[mt][2]),
+                                                             false, false);
+            const auto r1 = __builtin_amdgcn_permlane32_swap(__float_as_uint(ps[mt][1]), __float_as_uint(ps[mt][3]),
+                                                             false, false);
+            // lower lanes hold (own, partner's) sums of outputs 0 and 1, upper
+            // lanes (partner's, own) of outputs 2 and 3: the lower half first
+            const float2 val = make_float2(__uint_as_float(r0[0]) + __uint_as_float(r0[1]),
+                                           __uint_as_float(r1[0]) + __uint_as_float(r1[1]));
+            if (ok) *reinterpret_cast<float2*>(part_g + o * 4 + 2 * lh) = val;
         }
     };
     // kEpiPool (fragments of one row, binary32, one wave column): per group of
@@ -617,12 +719,16 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
         return;
     }
     if constexpr (EPI == kEpiProj) {
+        auto proj = [&](auto act_c) {
+            if constexpr (BF16) store_proj(act_c);
+            else store_proj_lanes(act_c);
+        };
         if (act == 1)
-            store_proj(std::integral_constant<int, 1>{});
+            proj(std::integral_constant<int, 1>{});
         else if (act == 2)
-            store_proj(std::integral_constant<int, 2>{});
+            proj(std::integral_constant<int, 2>{});
         else
-            store_proj(std::integral_constant<int, 0>{});
+            proj(std::integral_constant<int, 0>{});
         return;
     }
     if (act == 1)
