@@ -137,7 +137,17 @@ FOLD_CASES = {
     # 32 taps of |x| <= 8 with weights in {-1, 0, 1}: the stored bfloat16 activations stay
     # integers of at most 256, which bfloat16 holds exactly
     "int_bf16_n128": ([("conv", 16, 200, 1, 2, "relu"), ("conv", 200, 2, 1, 1, "relu")], 16, 290, 285, "bf16", "int"),
+    # the bfloat16 launch with a folded projection computes transposed blocks; its
+    # 64- and 32-channel tiles (NT = 2 and 1), ragged channel groups (96 of 128,
+    # 40 of 64) and tanh on both sides of the fold
+    "bf16_n64_tanh": ([("conv", 16, 96, 3, 3, "tanh"), ("conv", 96, 3, 1, 1, "tanh")], 16, 83, 95, "bf16", "uniform"),
+    "bf16_n32": ([("conv", 24, 40, 2, 3, "relu"), ("conv", 40, 2, 1, 1, "none")], 24, 70, 66, "bf16", "normal"),
+    "int_bf16_n64": ([("conv", 16, 100, 2, 1, "relu"), ("conv", 100, 4, 1, 1, "none")], 16, 120, 131, "bf16", "int"),
 }
+
+
+FOLD_KERNEL = {"bf16_n64_tanh": "conv_mfma_bf16_n64_proj", "bf16_n32": "conv_mfma_bf16_n32_proj",
+               "int_bf16_n64": "conv_mfma_bf16_n64_proj"}
 
 
 @pytest.mark.parametrize("case", list(FOLD_CASES))
@@ -156,6 +166,8 @@ def test_projection_fold(case, monkeypatch):
     names_p = [r["kernel"] for r in rp]
     log("fold %s: %s / %s" % (case, names_f[-2:], names_p[-2:]))
     assert names_f[-2].endswith("_proj") and names_f[-1] == "defrag_sum"
+    if case in FOLD_KERNEL:
+        assert names_f[-2] == FOLD_KERNEL[case], names_f
     assert not any(n.endswith("_proj") for n in names_p) and names_p[-1] == "defrag_trim"
     assert sum(r["flops"] for r in rf) == pytest.approx(sum(r["flops"] for r in rp), rel=1e-12)
     ref = oracle.eval_stride(oracle_layers(w.layers, dtype), w.x)
