@@ -10,6 +10,8 @@ Used by `tests/`, `__graft_entry__.smoke()` and the CPU-baseline leg of
 * `receptive_field` finds B by brute force (smallest patch on which the strided
   network ends in one sample).
 * `fragment` holds the literal vec-based Frag/Defrag and Stuff/Trim.
+* `bf16` models bfloat16 storage of the intermediate activations on top of the
+  dense (dilated) evaluation, for tighter checks of bfloat16 results.
 
 Weights come in cross-correlation order ([cout][cin][fh][fw], tap t multiplies
 input sample i+t), the order deep-learning frameworks use.  The paper writes the

@@ -75,12 +75,27 @@ EXPORTS = ("dss_chain_geometry", "dss_chain_layer_geometry", "dss_plan_create", 
 _lib = None
 
 
+def _torch_device_first():
+    """With torch in the process there are two HIP runtimes: torch's own copy and
+    the system one that libdss.so links.  If the system one brings the device up
+    first, torch's then reports no device; bringing torch's up first (when torch
+    is installed and sees a device) works in either use.  Nothing happens on a
+    machine without a GPU."""
+    try:
+        import torch
+    except ImportError:
+        return
+    if torch.cuda.is_available():
+        torch.cuda.init()
+
+
 def lib():
     """Load libdss.so; raises if it has not been built."""
     global _lib
     if _lib is None:
         if not os.path.exists(LIB_PATH):
             raise DssError(-1, "loading libdss.so", "%s does not exist; run __graft_entry__.build()" % LIB_PATH)
+        _torch_device_first()
         L = ctypes.CDLL(LIB_PATH)
         P, I32, I64, VP = ctypes.POINTER, ctypes.c_int32, ctypes.c_int64, ctypes.c_void_p
         L.dss_chain_geometry.argtypes = [P(Layer), I32, I32, I32, I32, I32, I32, I32, P(Geometry)]

@@ -77,3 +77,15 @@ def sampled_windows(out_h, out_w, Kh, Kw, per_phase=1, max_phases=None, seed=0):
 def oracle_windows(layers, x, i, j):
     """Oracle output at listed windows: [nwin][Cout]."""
     return oracle.eval_stride(layers, x, windows=(i, j))
+
+
+def check_bf16_storage_model(out, layers, x, plan_records, tol, what):
+    """A bfloat16 result against the oracle's bfloat16 storage model: the exact
+    evaluation with every stored activation rounded to bfloat16, except before a
+    final projection folded into the previous convolution (the launch records
+    show the fold), which reads binary32 activations."""
+    import oracle.bf16
+    fold = any(r["kernel"].endswith("_proj") for r in plan_records)
+    emu = oracle.bf16.eval_dilate_bf16_storage(layers, x, fold=fold)
+    assert_close(out, emu, tol, "%s vs bfloat16 storage model" % what)
+

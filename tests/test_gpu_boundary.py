@@ -191,3 +191,36 @@ def test_nan_samples_beyond_the_windows(name):
     b = b.cpu().numpy().astype(np.float64)[:, :a.shape[1], :a.shape[2]]
     assert np.all(np.isfinite(b)), "a NaN sample reached the output of a window that does not contain it"
     assert_close(b, a, 1e-6, "%s with NaN samples appended" % name)
+
+
+def test_library_first_then_torch_in_a_fresh_process():
+    """A fresh process that creates a plan (the library's HIP runtime) before it
+    makes any torch tensor must still get torch's device and a correct result:
+    the binding brings torch's runtime up before it loads the library."""
+    import os
+    import subprocess
+    import sys
+    code = (
+        "import numpy as np\n"
+        "from paper_1508_06904_amd import dss, workloads as wl\n"
+        "w = wl.make('c1_64x64')\n"
+        "plan = dss.Plan.from_workload(w)\n"
+        "import torch\n"
+        "x = torch.from_numpy(w.x).cuda().contiguous()\n"
+        "out = plan.eval_dense(x)\n"
+        "torch.cuda.synchronize()\n"
+        "o = out.cpu().numpy()\n"
+        "print('shape', o.shape, 'finite', bool(np.isfinite(o).all()), flush=True)\n"
+        "np.save(sys.argv[1], o)\n")
+    import tempfile
+    with tempfile.TemporaryDirectory() as d:
+        path = os.path.join(d, "out.npy")
+        root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+        r = subprocess.run([sys.executable, "-c", "import sys\n" + code, path], cwd=root, capture_output=True,
+                           text=True, timeout=110)
+        log(r.stdout.strip() + " " + r.stderr.strip()[-300:])
+        assert r.returncode == 0, r.stderr[-2000:]
+        got = np.load(path).astype(np.float64)
+    w = wl.make("c1_64x64")
+    ref = oracle.eval_stride(oracle_layers(w.layers, w.dtype), w.x)
+    assert_close(got, ref, 1e-4, "library first, then torch")

@@ -9,13 +9,15 @@ import pytest
 import oracle
 from oracle import fragment as fr
 from paper_1508_06904_amd import dss, workloads as wl
-from tests.gpu_helpers import assert_close, gpu_dense, kstar, log, oracle_layers, oracle_windows, to_device
+from tests.gpu_helpers import (assert_close, check_bf16_storage_model, gpu_dense, kstar, log, oracle_layers,
+                               oracle_windows, to_device)
 from tests.test_oracle import HAND, _layers_from_json, chain_layers
 
 pytestmark = pytest.mark.gpu
 
 F32_TOL = 1e-4
 BF16_TOL = 2e-2
+BF16_STORAGE_TOL = 1e-2   # against the bfloat16 storage model (see test_gpu_tiles)
 
 
 @pytest.fixture(scope="module", autouse=True)
@@ -167,9 +169,13 @@ def test_random_chain_bf16(name):
     K = kstar(arch)
     w = wl.custom(arch, C, B[0] + 2 * K[0] + 1, B[1] + 3 * K[1] + 2, seed=4, dtype="bf16")
     log("bf16 chain %s on %s" % (name, w.x.shape))
-    out, _ = gpu_dense(w.layers, w.x, nd, "bf16")
-    ref = oracle.eval_stride(oracle_layers(w.layers, "bf16"), w.x)
+    plan = dss.Plan(w.layers, nd, w.x.shape[0], "bf16")
+    plan.set_timing(True)
+    out, _ = gpu_dense(w.layers, w.x, nd, "bf16", plan=plan)
+    L = oracle_layers(w.layers, "bf16")
+    ref = oracle.eval_stride(L, w.x)
     assert_close(out, ref, BF16_TOL, name)
+    check_bf16_storage_model(out, L, w.x, plan.timings(), BF16_STORAGE_TOL, name)
 
 
 # The MFMA kernel runs its steps (input-channel chunk x filter tap) in threes
@@ -291,9 +297,14 @@ def test_named_reduced_full_oracle(name, H, W, widths):
     """The named layer patterns at reduced extents and widths, every window checked."""
     w = wl.make(name, H=H, W=W, widths=widths)
     log("%s reduced %s widths=%s" % (name, w.x.shape, widths))
-    out, _ = gpu_dense(w.layers, w.x, w.ndim, w.dtype)
-    ref = oracle.eval_stride(oracle_layers(w.layers, w.dtype), w.x)
+    plan = dss.Plan.from_workload(w)
+    plan.set_timing(True)
+    out, _ = gpu_dense(w.layers, w.x, w.ndim, w.dtype, plan=plan)
+    L = oracle_layers(w.layers, w.dtype)
+    ref = oracle.eval_stride(L, w.x)
     assert_close(out, ref, BF16_TOL if w.dtype == "bf16" else F32_TOL, name)
+    if w.dtype == "bf16":
+        check_bf16_storage_model(out, L, w.x, plan.timings(), BF16_STORAGE_TOL, name)
 
 
 # Full-size workloads in the benchmark's launch configuration.  The dense

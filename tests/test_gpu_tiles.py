@@ -8,6 +8,7 @@ import numpy as np
 import pytest
 
 import oracle
+import oracle.bf16
 from paper_1508_06904_amd import dss, workloads as wl
 from tests.gpu_helpers import assert_close, gpu_dense, log, oracle_layers
 
@@ -15,6 +16,10 @@ pytestmark = pytest.mark.gpu
 
 F32_TOL = 1e-4
 BF16_TOL = 2e-2
+# against the oracle's bfloat16 storage model: the GPU rounds at the same places,
+# so only single rounding-boundary flips (binary32 sums in another order) remain;
+# 4.6e-3 at worst over 80 random bfloat16 chains
+BF16_STORAGE_TOL = 1e-2
 
 
 @pytest.fixture(scope="module", autouse=True)
@@ -120,8 +125,15 @@ def test_random_chain_sweep(seed, sweep_log):
             kinds.add(("spatial", "flat", "dilated")[r["tile_mode"]])
     log("sweep %d: %s %s on %dx%d, variants %s" % (seed, dtype, arch, H, W, sorted(kinds)))
     sweep_log.append(kinds)
-    ref = oracle.eval_stride(oracle_layers(w.layers, dtype), w.x)
+    L = oracle_layers(w.layers, dtype)
+    ref = oracle.eval_stride(L, w.x)
     assert_close(out, ref, BF16_TOL if dtype == "bf16" else F32_TOL, "sweep %d" % seed)
+    if dtype == "bf16":
+        # tighter: against the exact evaluation with bfloat16-stored activations
+        # (kept in binary32 before a folded projection, as the launch records show)
+        fold = any(r["kernel"].endswith("_proj") for r in recs)
+        emu = oracle.bf16.eval_dilate_bf16_storage(L, w.x, fold=fold)
+        assert_close(out, emu, BF16_STORAGE_TOL, "sweep %d vs bfloat16 storage model" % seed)
 
 
 FOLD_CASES = {
