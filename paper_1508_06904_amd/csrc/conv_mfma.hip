@@ -162,12 +162,42 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
     char* halo0 = lds;
     char* halo1 = dbl_halo ? lds + halo_bytes : lds;
 
+    // Tile sample m -> tile row.  A 16-lane pass of an A read takes 16
+    // consecutive m; in an 8-wide tile (32 rows) they span two rows, and with
+    // the 80-byte sample pitch two rows d apart fall on disjoint LDS banks only
+    // if HW * d = 8 (mod 16).  So such tiles take the four groups of 8 samples
+    // of each 32-sample MFMA block from rows d apart, d = 8 >> (trailing zero
+    // bits of HW) (d = 1: consecutive rows, the plain row-major order), and the
+    // epilogue maps m back the same way.
+    // bfloat16 kernels use one branch-free form of both orders, row =
+    // ((m >> sa) << sb) + ((m >> 5) & mb) + (((m >> 3) & mk) << row_lg)
+    // (row-major: sa = log2 TW, sb = mb = mk = 0; rows d = 2^row_lg apart:
+    // sa = 5 + row_lg, sb = 2 + row_lg, mb = d - 1, mk = 3); binary32 kernels a
+    // branch on the (uniform) order, which measured faster there (HD 6x6 layer
+    // 0.8 % against 0.3 % faster than row-major), while the branch-free form
+    // slowed the small bfloat16 layers less (1 % against 2-3 %).
+    const int tw_log2 = __builtin_ctz(TW);   // spatial and dilated tiles are 2^k samples wide
+    const int row_lg = TW == 8 ? 3 - min(3, __builtin_ctz(HW)) : 0;
+    const bool rows_apart = TW == 8 && row_lg > 0;
+    const int sa = rows_apart ? 5 + row_lg : tw_log2, sb = rows_apart ? 2 + row_lg : 0;
+    const int mb = rows_apart ? (1 << row_lg) - 1 : 0, mk = rows_apart ? 3 : 0;
+    const int row_lg_b = TW == 8 ? row_lg : -1;   // binary32: -1 selects row-major
+    auto tile_dy = [&](int m) -> int {
+        if constexpr (BF16) {
+            return ((m >> sa) << sb) + ((m >> 5) & mb) + (((m >> 3) & mk) << row_lg);
+        } else {
+            if (row_lg_b < 0) return m >> tw_log2;
+            const int blk = m >> 5;
+            return (((blk >> row_lg_b) << 2) << row_lg_b) + (blk & ((1 << row_lg_b) - 1)) +
+                   (((m & 31) >> 3) << row_lg_b);
+        }
+    };
     // per-lane operand offsets (bytes) inside the halo / weight slice
     int a_off[MT];
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
         const int m = wm * 32 * MT + mt * 32 + l32;
-        a_off[mt] = ((m / TW) * HW + (m % TW)) * kPitchBytes + half * 32;
+        a_off[mt] = (tile_dy(m) * HW + (m & (TW - 1))) * kPitchBytes + half * 32;
     }
 
     floatx16 acc[MT][NT];
@@ -373,7 +403,6 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
 
     // -- epilogue: D[i][j] of a 32x32 tile sits in lane j + 32*((i/4)%2), register (i/8)*4 + i%4
     const int n_base = nb * Cfg::BN + wn * 32 * NT;
-    const int tw_log2 = __builtin_ctz(TW);   // spatial and dilated tiles are 2^k samples wide
     const size_t f_off = (size_t)f * Hout * Wout;
     const int frag_px = flat_h * flat_w;
     // output sample of tile position m: whether it exists, and its index
@@ -386,11 +415,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
             return p < Win && y < Hout && x < Wout;
         }
         if (dilated) {
-            const int y = py + dil_h * (ty0 + (m >> tw_log2)), x = px + dil_w * (tx0 + (m & (TW - 1)));
+            const int y = py + dil_h * (ty0 + tile_dy(m)), x = px + dil_w * (tx0 + (m & (TW - 1)));
             o = (size_t)y * Wout + x;
             return y < Hout && x < Wout;
         }
-        const int y = ty0 + (m >> tw_log2), x = tx0 + (m & (TW - 1));
+        const int y = ty0 + tile_dy(m), x = tx0 + (m & (TW - 1));
         o = f_off + (size_t)y * Wout + x;
         return y < Hout && x < Wout;
     };
@@ -491,11 +520,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
                     ok = p < Win && y < Hout && x < Wout;
                     o = ((size_t)fr * Hout + y) * Wout + x;
                 } else if (dilated) {
-                    const int y = py + dil_h * (ty0 + (m >> tw_log2)), x = px + dil_w * (tx0 + (m & (TW - 1)));
+                    const int y = py + dil_h * (ty0 + tile_dy(m)), x = px + dil_w * (tx0 + (m & (TW - 1)));
                     ok = y < Hout && x < Wout;
                     o = (size_t)y * Wout + x;
                 } else {
-                    const int y = ty0 + (m >> tw_log2), x = tx0 + (m & (TW - 1));
+                    const int y = ty0 + tile_dy(m), x = tx0 + (m & (TW - 1));
                     ok = y < Hout && x < Wout;
                     o = f_off + (size_t)y * Wout + x;
                 }
