@@ -822,12 +822,15 @@ struct Tile {
 // Spatial tile TH x TW = BM output samples: the shape that wastes the fewest
 // masked samples on this layer's fragment extent; among those, one whose halo can
 // be double-buffered within the LDS budget of two workgroups per CU, then the
-// smallest halo.  With TW = 8 a 16-lane group of an A read spans two halo rows,
-// whose samples share LDS banks unless the halo row is 8 mod 16 samples long;
-// the bfloat16 kernel, whose steps are short enough for that to show, counts
-// such a tile's work 3 % higher (measured: 8 x 32 -> 16 x 16 tiles make the 3x3
-// layers of the 4K frame 18 % faster, while 16 x 16 tiles with 3.4 % more
-// masked work make its 6x6 layer 4.7 % slower).
+// smallest halo.  The bfloat16 kernel counts the work of an 8-wide tile whose
+// halo row is not 8 mod 16 samples long 3 % higher: such tiles once read
+// consecutive halo rows in one 16-lane pass of an A read, on shared LDS banks
+// (8 x 32 -> 16 x 16 tiles made the 3x3 layers of the 4K frame 18 % faster,
+// while 16 x 16 tiles with 3.4 % more masked work made its 6x6 layer 4.7 %
+// slower).  The kernel now reads 8-wide tiles with their rows interleaved
+// (tile_dy), conflict-free; the weight stays: the layers where it decides have
+// under 0.3 % of masked work between the two shapes, and 16 x 16 stages a
+// smaller halo.
 static Tile pick_tile(int BM, int Hout, int Wout, int fh, int fw, size_t lds_max, bool bf16) {
     Tile best{0, 0, 0, 0};
     int64_t best_work = -1, best_halo = -1;
