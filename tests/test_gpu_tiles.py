@@ -10,7 +10,7 @@ import pytest
 import oracle
 import oracle.bf16
 from paper_1508_06904_amd import dss, workloads as wl
-from tests.gpu_helpers import assert_close, gpu_dense, log, oracle_layers
+from tests.gpu_helpers import assert_close, check_bf16_storage_model, gpu_dense, log, oracle_layers
 
 pytestmark = pytest.mark.gpu
 
@@ -61,6 +61,41 @@ def test_n128_tile_every_window(dtype):
     assert all(r["tile_mode"] == 0 for r in recs if "n128" in r["kernel"])
     ref = oracle.eval_stride(oracle_layers(w.layers, dtype), w.x)
     assert_close(out, ref, BF16_TOL if dtype == "bf16" else F32_TOL, "n128 %s" % dtype)
+
+
+# Output extents whose least-masked spatial tile is 16 x 16 (48 x 80: 8-wide tiles
+# would pad 48 rows to 64, 32-wide ones 80 columns to 96) or 32 x 8 (96 x 40: 16-wide
+# tiles would pad 40 columns to 48), and filter widths giving every row distance
+# of the interleaved order: halo rows HW = TW + fw - 1 samples long, rows d apart
+# with d = 8 >> tz(HW) (8-wide) or 16 >> tz(HW) (16-wide, HW even), else d = 1.
+NARROW_TILE_CASES = [(16, 2), (16, 3), (16, 5), (16, 9), (8, 2), (8, 3), (8, 5), (8, 6), (8, 9)]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("tw,fw", NARROW_TILE_CASES, ids=["tw%d_fw%d" % c for c in NARROW_TILE_CASES])
+def test_narrow_tile_row_order_every_window(tw, fw, dtype):
+    """An fw x fw convolution 32 -> 64 on extents that make 8- or 16-wide tiles
+    the least-masked shape, whose samples the kernel takes from rows d apart
+    (the LDS bank-conflict-free order), then a 1x1 convolution 64 -> 16, checked
+    at every output position.  The first launch stores its activations through
+    the store epilogue (bfloat16 or binary32), which maps the samples back by
+    the same order; a row order that is not a bijection of the tile, or an
+    epilogue that maps differently, shows up as wrong or missing outputs."""
+    hout, wout = (48, 80) if tw == 16 else (96, 40)
+    arch = [("conv", 32, 64, fw, fw, "relu"), ("conv", 64, 16, 1, 1, "none")]
+    w = wl.custom(arch, 32, hout + fw - 1, wout + fw - 1, seed=100 + 10 * tw + fw, dtype=dtype)
+    log("narrow tile %s tw=%d fw=%d on %s" % (dtype, tw, fw, w.x.shape))
+    out, recs = timed_dense(w)
+    names = [r["kernel"] for r in recs if r["flops"] > 0]
+    log("  launches: %s" % names)
+    assert names[0] == "conv_mfma_%s_n64" % dtype, names
+    assert all(r["tile_mode"] == 0 for r in recs if r["kernel"].startswith("conv_mfma"))
+    layers = oracle_layers(w.layers, dtype)
+    ref = oracle.eval_stride(layers, w.x)
+    assert out.shape == ref.shape == (16, hout, wout)
+    if dtype == "bf16":
+        check_bf16_storage_model(out, layers, w.x, recs, BF16_STORAGE_TOL, "narrow tile tw=%d fw=%d" % (tw, fw))
+    assert_close(out, ref, BF16_TOL if dtype == "bf16" else F32_TOL, "narrow tile %s tw=%d fw=%d" % (dtype, tw, fw))
 
 
 def _random_chain(seed):
